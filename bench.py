@@ -1,0 +1,191 @@
+#!/usr/bin/env python3
+"""Jorge optimizer steps/s on one MI355X, with roofline and CPU-oracle context.
+
+A step is one full Jorge update (Algorithm 2 with SGD grafting, momentum and
+decoupled weight decay) over every layer of the workload, with the factors
+updated every step (interval 1). Inputs are synthetic, seeded and resident in
+HBM before the timed region. Prints one JSON line.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "Jorge optimizer steps/sec (ResNet-50 weight set); fp32 MFMA util %"
+PEAK_FP32_MFMA_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+WORKLOAD_NAMES = {
+    "resnet50": "ResNet-50 weight set: 53 conv + fc weights as out x in*kh*kw, fp32, G ~ N(0, 1e-3^2)",
+    "single_64x576": "single 64x576 layer, G ~ N(0, 1e-2^2)",
+    "single_512x4608": "single 512x4608 layer, G ~ N(0, 1e-3^2)",
+    "large_dense": "8 x 4096x4096 + 8 x 4096x1024 layers, G ~ N(0, 1e-3^2)",
+    "many_small": "512 layers, m, n in {32, 64, 128, 256}, G ~ N(0, 1e-2^2)",
+}
+
+
+def stage_flops(shapes):
+    """Algorithmic flops of one update step per GEMM stage (symmetric products count half)."""
+    f = {k: 0 for k in ("gram_L", "gram_R", "pow2", "pow4", "xform", "poly", "update", "precond_L",
+                        "precond_R")}
+    for m, n in shapes:
+        f["gram_L"] += m * m * n
+        f["gram_R"] += n * n * m
+        for d in (m, n):
+            f["pow2"] += d ** 3
+            f["pow4"] += d ** 3
+            f["xform"] += 2 * d ** 3
+            f["poly"] += 2 * d ** 3
+            f["update"] += 2 * d ** 3
+        f["precond_L"] += 2 * m * m * n
+        f["precond_R"] += 2 * m * n * n
+    return f
+
+
+def falg(m, n):
+    return 8 * m ** 3 + 8 * n ** 3 + 3 * m * m * n + 3 * m * n * n
+
+
+def stage_bytes(shapes):
+    """Algorithmic HBM bytes per launch of the bandwidth-bound stages."""
+    mn = sum(m * n for m, n in shapes)
+    return {"weight": 12 * mn,       # read theta and m, write theta
+            "stage_in": 16 * mn}     # read G, write the padded copy, read and write m_SGD
+
+
+def cpu_baseline(shapes, sigma, seed, budget_s):
+    """The fp64 oracle timed on the host over a bounded, deterministic sample.
+
+    Layers are taken in the workload's order, one oracle step each, until the
+    time budget is spent; steps/s is extrapolated by algorithmic-flop share.
+    """
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import JorgeOracle
+    from paper_2310_12298_amd.workloads import gradient, initial_params
+
+    total_f = sum(falg(m, n) for m, n in shapes)
+    done_f, spent, used = 0, 0.0, 0
+    for l, s in enumerate(shapes):
+        G = [gradient(seed, l, 1, s, sigma)]
+        P = [initial_params(seed, l, s).astype(np.float64)]
+        orc = JorgeOracle([s])
+        t0 = time.perf_counter()
+        orc.step(P, G, 0.1, 0.9, 0.9, 5e-5)
+        spent += time.perf_counter() - t0
+        done_f += falg(*s)
+        used += 1
+        if spent >= budget_s:
+            break
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    return {"value": (done_f / total_f) / spent, "unit": "steps/s", "cores": threads, "kind": "oracle",
+            "sample": f"one fp64 oracle step on the first {used} of {len(shapes)} layers "
+                      f"({100.0 * done_f / total_f:.1f}% of the step's algorithmic flops) in {spent:.1f} s, "
+                      f"scaled by flop share"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=None, help="timed steps (default: the workload's run)")
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="resnet50", choices=sorted(WORKLOAD_NAMES))
+    ap.add_argument("--interval", type=int, default=1, help="preconditioner update interval k")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time (0 = skip)")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py runs on exactly one GPU (asked for {max(args.gpus, world)}): the Jorge step is "
+              f"replicated per data-parallel rank and this build measures one GPU's step.", file=sys.stderr)
+        return 2
+
+    import torch
+
+    from paper_2310_12298_amd.jorge import Jorge
+    from paper_2310_12298_amd.workloads import CONFIGS, DEFAULT_HPARAMS, device_gradient, device_initial_params
+
+    torch.cuda.set_device(0)
+    shapes, sigma, run_steps = CONFIGS[args.config]
+    steps = args.steps if args.steps is not None else run_steps
+    hp = DEFAULT_HPARAMS
+    opt = Jorge(shapes, eps=hp["eps"], precond_interval=args.interval)
+    params = [device_initial_params(args.seed, l, s) for l, s in enumerate(shapes)]
+    grads = [[device_gradient(args.seed, l, t, s, sigma) for l, s in enumerate(shapes)]
+             for t in range(1, args.warmup + steps + 1)]
+    pp = Jorge.pointer_array(params)
+    gp = [Jorge.pointer_array(g) for g in grads]
+
+    def step(i):
+        opt.step_ptrs(pp, gp[i], hp["lr"], hp["beta2"], hp["beta1"], hp["weight_decay"])
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    opt.set_timing(True)
+    opt.reset_timing()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(steps):
+        step(args.warmup + i)
+    stop.record()
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(stop)
+    timing = opt.read_timing()
+    opt.set_timing(False)
+    for t in params:
+        if not torch.isfinite(t).all():
+            raise RuntimeError("non-finite parameters after the timed steps")
+
+    updates = sum(1 for i in range(args.warmup, args.warmup + steps) if i % args.interval == 0)
+    flops = stage_flops(shapes)
+    per_stage = {k: {"ms_per_launch": (v[0] / v[1]) if v[1] else 0.0, "launches": v[1]}
+                 for k, v in timing.items()}
+    gemm_ms = sum(timing[k][0] for k in flops)
+    gemm_flops = sum(flops[k] * timing[k][1] for k in flops)
+    dom = max(flops, key=lambda k: timing[k][0])
+    dom_ms = timing[dom][0] / max(1, timing[dom][1])
+    achieved = flops[dom] / (dom_ms * 1e-3) / 1e12
+    hbm = stage_bytes(shapes)
+    w_ms = timing["weight"][0] / max(1, timing["weight"][1])
+    for k, v in per_stage.items():
+        if k in flops:
+            v["tflops"] = flops[k] / (v["ms_per_launch"] * 1e-3) / 1e12 if v["ms_per_launch"] else 0.0
+    out = {
+        "metric": METRIC,
+        "value": steps / (total_ms * 1e-3),
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": args.warmup,
+        "ms_per_step": total_ms / steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": WORKLOAD_NAMES[args.config], "name": args.config, "layers": len(shapes),
+                   "params": sum(m * n for m, n in shapes), "precond_interval": args.interval,
+                   "factor_updates": updates, "seed": args.seed},
+        "roofline": {"bound": "mfma", "kernel": f"gemm_grouped ({dom} stage)", "achieved": achieved,
+                     "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s", "frac": achieved / PEAK_FP32_MFMA_TFLOPS,
+                     "traffic": None},
+        "mfma_util_pct": 100.0 * (gemm_flops / (gemm_ms * 1e-3) / 1e12) / PEAK_FP32_MFMA_TFLOPS if gemm_ms else 0.0,
+        "hbm": {"kernel": "weight", "achieved": hbm["weight"] / (w_ms * 1e-3) / 1e9 if w_ms else 0.0,
+                "peak": PEAK_HBM_GBS, "unit": "GB/s"},
+        "stages": per_stage,
+    }
+    if args.cpu_budget > 0:
+        out["cpu_baseline"] = cpu_baseline(shapes, sigma, args.seed, args.cpu_budget)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

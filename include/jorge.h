@@ -1,0 +1,184 @@
+/*
+ * jorge.h - C ABI of an MI355X (gfx950) implementation of the Jorge optimizer step.
+ *
+ * Jorge (Singh, Sating, Bhatele, arXiv 2310.12298) keeps, per 2-D layer
+ * theta (m x n), two preconditioner factors L_hat (m x m) and R_hat (n x n)
+ * that approximate the inverse fourth roots of Shampoo's Kronecker factors,
+ * and updates them with matrix products only (Section 3, Algorithm 2,
+ * Eq. 3-7; the dynamic beta_2 of Appendix A.1, Eq. 8-9). The gradient is
+ * preconditioned as L_hat G R_hat and applied with momentum, SGD grafting
+ * (Appendix A.2, Algorithm 3) and decoupled weight decay (Section 4).
+ *
+ * Every entry point returns a jorge_status (0 = JORGE_OK, negative = error)
+ * except jorge_destroy and the string helpers. No C++ exception crosses the
+ * ABI. Pointers documented as "device" are HIP device pointers; every other
+ * pointer is a host pointer. Work is queued on the context's HIP stream and
+ * does not synchronise the host unless the comment says so. Arguments are
+ * validated before any HIP call; an invalid call changes no state.
+ *
+ * A context is not re-entrant: calls on one context must not overlap.
+ * Distinct contexts are independent.
+ */
+#ifndef JORGE_H
+#define JORGE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t jorge_status;
+#define JORGE_OK                    0
+#define JORGE_ERR_INVALID_ARGUMENT (-1) /* null pointer, bad size, bad mode, out-of-range value */
+#define JORGE_ERR_OUT_OF_MEMORY    (-2) /* device or host allocation failed */
+#define JORGE_ERR_HIP              (-3) /* a HIP runtime call or kernel launch failed */
+#define JORGE_ERR_UNSUPPORTED      (-4) /* a size above the library's limits */
+
+/* How beta_2 is chosen for each factor update (Section 3 and Appendix A.1).
+ * FIXED:   beta = beta2 as passed (Algorithm 2 as printed).
+ * DYNAMIC: beta = ||X||_F / (||X||_F + 1) (Eq. 8 with equality, Eq. 9); beta2
+ *          is used only when ||X||_F = 0.
+ * CLAMPED: beta = max(beta2, ||X||_F / (||X||_F + 1)): the dynamic value
+ *          exactly when the truncated series would otherwise leave its domain
+ *          ||(1-beta)/beta X|| < 1. Default.
+ * In every mode the update uses c = (1-beta)/beta and s = beta^(-1/4), formed
+ * on the dynamic branch as c = 1/||X||_F, s = (1 + 1/||X||_F)^(1/4) (Eq. 9). */
+#define JORGE_BETA_FIXED   0
+#define JORGE_BETA_DYNAMIC 1
+#define JORGE_BETA_CLAMPED 2
+
+/* State tensors of one layer (Algorithm 2 and Algorithm 3). */
+#define JORGE_STATE_L       0 /* L_hat, rows x rows, fp32, symmetric        */
+#define JORGE_STATE_R       1 /* R_hat, cols x cols, fp32, symmetric        */
+#define JORGE_STATE_MOM     2 /* Jorge momentum m_t, rows x cols, fp32      */
+#define JORGE_STATE_MOM_SGD 3 /* SGD heavy-ball momentum m_SGD, rows x cols */
+
+/* Per-layer diagnostics of the last step (jorge_read_diag). */
+#define JORGE_DIAG_NU_L     0 /* ||X_L||_F of the last factor update            */
+#define JORGE_DIAG_NU_R     1 /* ||X_R||_F                                      */
+#define JORGE_DIAG_BETA_L   2 /* beta used for L_hat in the last factor update  */
+#define JORGE_DIAG_BETA_R   3 /* beta used for R_hat                            */
+#define JORGE_DIAG_NORM_M   4 /* ||m_t||_F after the last step                  */
+#define JORGE_DIAG_NORM_SGD 5 /* ||m_SGD,t||_F after the last step              */
+#define JORGE_DIAG_STEP     6 /* step size g applied to m_t in the last step    */
+#define JORGE_DIAG_COUNT    7
+
+/* One layer: theta and G are dense row-major rows x cols fp32 (an N-d weight
+ * collapsed to out x in*kh*kw, Section 3). */
+typedef struct jorge_shape {
+    int64_t rows;
+    int64_t cols;
+} jorge_shape;
+
+/* Per-context options fixed at creation. */
+typedef struct jorge_hparams {
+    double  eps;              /* factors start at eps^(-1/4) I (Algorithm 2); > 0, finite.
+                                 Default 1e-6. */
+    int32_t precond_interval; /* k >= 1: factors update on steps t with (t-1) mod k == 0
+                                 (Section 3, preconditioner update interval). Default 1. */
+    int32_t beta_mode;        /* JORGE_BETA_*. Default JORGE_BETA_CLAMPED. */
+    int32_t graft;            /* 1: SGD grafting (Algorithm 3); 0: theta -= lr * m_t. Default 1. */
+    int32_t symmetrize;       /* 1: each updated factor is replaced by (Z + Z^T)/2, Z being
+                                 Algorithm 2's product; 0: Z itself. Default 1. */
+} jorge_hparams;
+
+/* Largest rows or cols of a layer the library accepts. */
+#define JORGE_MAX_DIM 32768
+/* Largest number of layers in one context. */
+#define JORGE_MAX_LAYERS 65536
+
+typedef struct jorge_ctx jorge_ctx;
+
+/* Fills *hp with the defaults listed above. hp: non-NULL. */
+jorge_status jorge_hparams_default(jorge_hparams* hp);
+
+/* Creates a context for num_layers layers (Algorithm 2's initialisation).
+ * shapes: num_layers entries, each rows, cols in [1, JORGE_MAX_DIM].
+ * hp: options, or NULL for the defaults.
+ * hip_stream: the hipStream_t all work is queued on (NULL = the null stream).
+ * Allocates all device state (factors eps^(-1/4) I, momenta zero) and the
+ * workspace in one device allocation owned by the context; the step counter
+ * starts at 0. Synchronises the stream before returning. On error *out is
+ * set to NULL and nothing stays allocated. */
+jorge_status jorge_create(const jorge_shape* shapes, int32_t num_layers,
+                          const jorge_hparams* hp, void* hip_stream, jorge_ctx** out);
+
+/* One Jorge step for every layer (Algorithm 2 with Algorithm 3 and decoupled
+ * weight decay). With t the new step number (1 for the first call):
+ *   if (t-1) mod k == 0, for A in {L_hat (statistic G G^T), R_hat (G^T G)}:
+ *     X = A^4 * stat;  nu = ||X||_F;  (c, s) from beta_mode, beta2 and nu;
+ *     Z = s * A * (I - (c/4) X + (5 c^2/32) X^2);  A <- (Z + Z^T)/2 or Z;
+ *   G~ = L_hat G R_hat;  m = beta1 m + (1-beta1) G~;  m_SGD = beta1 m_SGD + G;
+ *   g = lr ||m_SGD||_F / ||m||_F (graft, 0 if ||m||_F = 0) or lr (no graft);
+ *   theta <- theta (1 - lr weight_decay) - g m.
+ * params: host array of num_layers device pointers, each a dense row-major
+ *   rows x cols fp32 tensor, updated in place.
+ * grads: host array of num_layers device pointers (same layout), read only.
+ * lr >= 0, 0 < beta2 < 1, 0 <= beta1 < 1, weight_decay >= 0, all finite.
+ * The host arrays are read before the call returns; the tensors must stay
+ * valid until the stream has executed the step. */
+jorge_status jorge_step(jorge_ctx* ctx, float* const* params, const float* const* grads,
+                        double lr, double beta2, double beta1, double weight_decay);
+
+/* Copies one state tensor (dense, row-major; sizes as listed for JORGE_STATE_*)
+ * into dst, a device buffer with row stride ld_dst >= its columns. Stream-ordered. */
+jorge_status jorge_get_state(jorge_ctx* ctx, int32_t layer, int32_t kind, float* dst,
+                             int64_t ld_dst);
+
+/* Overwrites one state tensor from src, a device buffer with row stride
+ * ld_src >= its columns (for checkpoint restore and state injection). The
+ * caller keeps factors symmetric if it relies on symmetry. Stream-ordered. */
+jorge_status jorge_set_state(jorge_ctx* ctx, int32_t layer, int32_t kind, const float* src,
+                             int64_t ld_src);
+
+/* Lends the device pointer of one state tensor and its row stride in floats
+ * (factors are stored with rows padded to a multiple of 32, zero outside the
+ * valid block). Valid until jorge_destroy. */
+jorge_status jorge_state_ptr(jorge_ctx* ctx, int32_t layer, int32_t kind, float** dev_ptr,
+                             int64_t* ld);
+
+/* Step counter: the number of steps taken (0 after create). */
+jorge_status jorge_get_step(const jorge_ctx* ctx, int64_t* t);
+jorge_status jorge_set_step(jorge_ctx* ctx, int64_t t);            /* t >= 0 */
+
+/* Diagnostics of the last step for one layer: out[JORGE_DIAG_COUNT] on the
+ * host. Synchronises the context's stream. */
+jorge_status jorge_read_diag(jorge_ctx* ctx, int32_t layer, double* out);
+
+/* Changes the stream later calls queue on (NULL = the null stream). */
+jorge_status jorge_set_stream(jorge_ctx* ctx, void* hip_stream);
+
+/* Waits for all work queued by the context. */
+jorge_status jorge_synchronize(jorge_ctx* ctx);
+
+/* Device bytes the context holds (state plus workspace). */
+jorge_status jorge_device_bytes(const jorge_ctx* ctx, int64_t* bytes);
+
+/* Per-stage timing. When enabled, every kernel launch of a step is bracketed
+ * by HIP events on the context's stream. jorge_read_timing synchronises,
+ * adds the elapsed time of every bracket since the last read to per-stage
+ * totals, and copies min(n, jorge_num_stages()) totals (milliseconds) and
+ * launch counts into ms / launches (either may be NULL).
+ * jorge_reset_timing zeroes the totals. */
+jorge_status jorge_set_timing(jorge_ctx* ctx, int32_t enable);
+jorge_status jorge_read_timing(jorge_ctx* ctx, double* ms, int64_t* launches, int32_t n);
+jorge_status jorge_reset_timing(jorge_ctx* ctx);
+int32_t      jorge_num_stages(void);
+const char*  jorge_stage_name(int32_t stage);  /* NULL if out of range */
+
+/* Frees the context and all device memory it holds; NULL is ignored.
+ * Synchronises the context's stream first. */
+void jorge_destroy(jorge_ctx* ctx);
+
+/* Static description of a status code. */
+const char* jorge_status_string(jorge_status s);
+
+/* Detail of the last error on this context ("" if none). */
+const char* jorge_last_error(const jorge_ctx* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* JORGE_H */

@@ -1,0 +1,220 @@
+// Grouped fp32 MFMA GEMM for gfx950 with fused epilogues.
+//
+// One launch covers every tile of a list of independent products (all layers'
+// factors of one stage of the step). A workgroup of 256 threads computes one
+// 128 x 128 tile of C = A * B; its four waves each own a 64 x 64 sub-tile held
+// as 2 x 2 blocks of v_mfma_f32_32x32x2_f32 accumulators. K is consumed in
+// slabs of 32 staged through double-buffered LDS: while the waves run the
+// MFMAs of slab k, each thread holds slab k+1 in registers and writes it to
+// the other LDS buffer afterwards (one barrier per slab).
+//
+// Within a slab, lane l of a wave contributes k = 8*k8 + 4*(l/32) + s to the
+// MFMA of step s (s = 0..3): the half-waves take disjoint halves of each
+// 8-wide k group, so a K-contiguous operand is read from LDS as one 16-byte
+// load per lane per 8 k values. The same k map is used for A and B, so every
+// product A[i][k] * B[k][j] is formed exactly once.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "jorge_types.hpp"
+
+namespace jorge {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int kTile = 128;                    // tile rows = tile columns
+constexpr int kSlab = 32;                     // K per LDS stage
+constexpr int kGemmThreads = 256;
+constexpr int kLdsK = kSlab + 4;              // row stride of a K-contiguous operand in LDS
+constexpr int kLdsMN = kTile + 8;             // row stride of an M/N-contiguous operand in LDS
+constexpr int kLdsOperand = kTile * kLdsK;    // floats per operand per stage (>= kSlab * kLdsMN)
+static_assert(kLdsOperand >= kSlab * kLdsMN, "LDS operand buffer too small");
+
+// Workgroups are dispatched round-robin over the 8 XCDs. Remap the dispatch
+// index so each XCD walks a contiguous run of the tile list, keeping tiles
+// that share A rows and B columns in the same L2.
+__device__ __forceinline__ int xcd_remap(int bid, int n) {
+    const int q = n >> 3, r = n & 7;
+    const int x = bid & 7, i = bid >> 3;
+    return (x < r) ? x * (q + 1) + i : r * (q + 1) + (x - r) * q + i;
+}
+
+// Global -> registers: one 128 x 32 operand slab, four 16-byte loads per thread.
+// Rows (K-major) or columns (MN-major) past the extent `lim` are clamped to
+// the last valid one: they only feed outputs that the epilogue discards.
+template <bool KMAJ>
+__device__ __forceinline__ void load_slab(const float* __restrict__ base, int ld, int mn0, int lim,
+                                          int k0, f32x4 (&r)[4]) {
+    const int tid = threadIdx.x;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int u = tid + i * kGemmThreads;
+        if constexpr (KMAJ) {
+            const int row = min(mn0 + (u >> 3), lim - 1);
+            r[i] = *reinterpret_cast<const f32x4*>(base + (size_t)row * ld + k0 + (u & 7) * 4);
+        } else {
+            const int col = min(mn0 + (u & 31) * 4, lim - 4);
+            r[i] = *reinterpret_cast<const f32x4*>(base + (size_t)(k0 + (u >> 5)) * ld + col);
+        }
+    }
+}
+
+// Registers -> LDS, in the operand's own layout.
+template <bool KMAJ>
+__device__ __forceinline__ void store_slab(float* s, const f32x4 (&r)[4]) {
+    const int tid = threadIdx.x;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int u = tid + i * kGemmThreads;
+        if constexpr (KMAJ)
+            *reinterpret_cast<f32x4*>(s + (u >> 3) * kLdsK + (u & 7) * 4) = r[i];
+        else
+            *reinterpret_cast<f32x4*>(s + (u >> 5) * kLdsMN + (u & 31) * 4) = r[i];
+    }
+}
+
+// LDS -> MFMA operand registers: values for k = k .. k+3 at row/column mn.
+template <bool KMAJ>
+__device__ __forceinline__ void fragment(const float* s, int mn, int k, float (&f)[4]) {
+    if constexpr (KMAJ) {
+        const f32x4 v = *reinterpret_cast<const f32x4*>(s + mn * kLdsK + k);
+        f[0] = v[0]; f[1] = v[1]; f[2] = v[2]; f[3] = v[3];
+    } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) f[q] = s[(k + q) * kLdsMN + mn];
+    }
+}
+
+template <bool AK, bool BK>
+__device__ __forceinline__ void mma_slab(const float* sa, const float* sb, int wy, int wx, int lane,
+                                         f32x16 (&acc)[2][2]) {
+    const int r = lane & 31, h = lane >> 5;
+#pragma unroll
+    for (int k8 = 0; k8 < kSlab / 8; ++k8) {
+        float a[2][4], b[2][4];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            fragment<AK>(sa, wy * 64 + i * 32 + r, k8 * 8 + h * 4, a[i]);
+            fragment<BK>(sb, wx * 64 + i * 32 + r, k8 * 8 + h * 4, b[i]);
+        }
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][s], b[j][s], acc[i][j], 0, 0, 0);
+    }
+}
+
+// Sum of one double per thread over the workgroup, in a fixed order.
+__device__ __forceinline__ double block_sum_256(double v, double* red) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+    __syncthreads();
+    return (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+template <bool AK, bool BK, int EPI>
+__global__ __launch_bounds__(kGemmThreads, 2) void gemm_grouped(const GemmProblem* __restrict__ probs,
+                                                                const TileDesc* __restrict__ tiles,
+                                                                float beta1) {
+    __shared__ __attribute__((aligned(16))) float lds[2][2][kLdsOperand];
+    __shared__ double red[4];
+
+    const TileDesc td = tiles[xcd_remap(blockIdx.x, gridDim.x)];
+    const GemmProblem& p = probs[td.prob];
+    const int row0 = td.tm * kTile, col0 = td.tn * kTile;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wy = wave >> 1, wx = wave & 1;
+
+    f32x16 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+
+    f32x4 ra[4], rb[4];
+    const int nk = p.K / kSlab;
+    load_slab<AK>(p.A, p.lda, row0, p.M, 0, ra);
+    load_slab<BK>(p.B, p.ldb, col0, p.N, 0, rb);
+    store_slab<AK>(lds[0][0], ra);
+    store_slab<BK>(lds[0][1], rb);
+    __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+        const int cur = kt & 1;
+        const bool more = kt + 1 < nk;
+        if (more) {
+            load_slab<AK>(p.A, p.lda, row0, p.M, (kt + 1) * kSlab, ra);
+            load_slab<BK>(p.B, p.ldb, col0, p.N, (kt + 1) * kSlab, rb);
+        }
+        mma_slab<AK, BK>(lds[cur][0], lds[cur][1], wy, wx, lane, acc);
+        if (more) {
+            store_slab<AK>(lds[cur ^ 1][0], ra);
+            store_slab<BK>(lds[cur ^ 1][1], rb);
+        }
+        __syncthreads();
+    }
+
+    // Epilogue. Accumulator register e of block (i, j) holds
+    // C[row0 + wy*64 + i*32 + 8*(e/4) + 4*(lane/32) + e%4][col0 + wx*64 + j*32 + lane%32].
+    const int h = lane >> 5;
+    float a = 0.f, b = 0.f, sf = 0.f;
+    if constexpr (EPI == EPI_POLY) { a = p.sc->a; b = p.sc->b; }
+    if constexpr (EPI == EPI_SCALE) sf = p.sc->sf;
+    double part = 0.0;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int col = col0 + wx * 64 + j * 32 + (lane & 31);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int rowb = row0 + wy * 64 + i * 32 + q * 8 + h * 4;
+                if constexpr (EPI == EPI_SYM) {
+                    if (col < p.N && rowb < p.M && td.tm != td.tn) {
+                        f32x4 v;
+                        v[0] = acc[i][j][q * 4 + 0]; v[1] = acc[i][j][q * 4 + 1];
+                        v[2] = acc[i][j][q * 4 + 2]; v[3] = acc[i][j][q * 4 + 3];
+                        *reinterpret_cast<f32x4*>(p.C + (size_t)col * p.ldc + rowb) = v;
+                    }
+                }
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int row = rowb + e;
+                    const float v = acc[i][j][q * 4 + e];
+                    if constexpr (EPI == EPI_MOMENTUM) {
+                        if (row < p.valid_m && col < p.valid_n) {
+                            float* mp = p.mom + (size_t)row * p.ldmom + col;
+                            const float mn = beta1 * *mp + (1.0f - beta1) * v;
+                            *mp = mn;
+                            part += (double)mn * (double)mn;
+                        }
+                    } else {
+                        if (row < p.M && col < p.N) {
+                            float out = v;
+                            if constexpr (EPI == EPI_NORM) part += (double)v * (double)v;
+                            if constexpr (EPI == EPI_POLY) {
+                                const float x = p.X[(size_t)row * p.ldx + col];
+                                const float id = (row == col && row < p.valid_m) ? 1.0f : 0.0f;
+                                out = id - a * x + b * v;
+                            }
+                            if constexpr (EPI == EPI_SCALE) out = sf * v;
+                            p.C[(size_t)row * p.ldc + col] = out;
+                        }
+                    }
+                }
+            }
+        }
+    if constexpr (EPI == EPI_NORM || EPI == EPI_MOMENTUM) {
+        const double total = block_sum_256(part, red);
+        if (threadIdx.x == 0) p.partials[td.slot] = total;
+    }
+}
+
+}  // namespace jorge

@@ -1,0 +1,203 @@
+// Bandwidth-bound and scalar kernels of the Jorge step for gfx950.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "jorge_gemm.hpp"
+#include "jorge_types.hpp"
+
+namespace jorge {
+
+constexpr int kEwThreads = 256;
+
+// Sum of one double per lane over a 64-lane wave, in a fixed order.
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+    return v;
+}
+
+// Fixed-order sum of n doubles by one wave (every lane gets the total).
+__device__ __forceinline__ double wave_sum_array(const double* __restrict__ x, int n) {
+    double v = 0.0;
+    for (int i = threadIdx.x & 63; i < n; i += 64) v += x[i];
+    return wave_sum(v);
+}
+
+// A_hat = eps^(-1/4) I on the valid diagonal of every factor (the arena is zeroed before).
+__global__ void init_factors_kernel(const FactorDev* __restrict__ f, float l0) {
+    const FactorDev F = f[blockIdx.x];
+    for (int i = threadIdx.x; i < F.d; i += blockDim.x) F.A[(size_t)i * F.dp + i] = l0;
+}
+
+// Gradient stage-in: copies G (dense m x n, caller's buffer) into the padded
+// operand Gp, updates m_SGD = beta1 m_SGD + G (Algorithm 3) and writes the
+// chunk's sum of m_SGD^2.
+__global__ __launch_bounds__(kEwThreads) void stagein_kernel(const LayerDev* __restrict__ layers,
+                                                             const RowChunk* __restrict__ chunks,
+                                                             int layer_base, PtrBatch grads,
+                                                             float beta1) {
+    __shared__ double red[4];
+    const RowChunk ck = chunks[blockIdx.x];
+    const LayerDev& L = layers[ck.layer];
+    const float* __restrict__ G = grads.p[ck.layer - layer_base];
+    const int n = L.n;
+    double part = 0.0;
+    if ((n & 3) == 0 && (reinterpret_cast<uintptr_t>(G) & 15) == 0) {
+        const int n4 = n >> 2;
+        const int total = ck.nrows * n4;
+        for (int e = threadIdx.x; e < total; e += kEwThreads) {
+            const int r = ck.row0 + e / n4, c = (e % n4) * 4;
+            const f32x4 g = *reinterpret_cast<const f32x4*>(G + (size_t)r * n + c);
+            *reinterpret_cast<f32x4*>(L.Gp + (size_t)r * L.np + c) = g;
+            f32x4* ms = reinterpret_cast<f32x4*>(L.msgd + (size_t)r * n + c);
+            f32x4 v = *ms;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                v[q] = beta1 * v[q] + g[q];
+                part += (double)v[q] * (double)v[q];
+            }
+            *ms = v;
+        }
+    } else {
+        const int total = ck.nrows * n;
+        for (int e = threadIdx.x; e < total; e += kEwThreads) {
+            const int r = ck.row0 + e / n, c = e % n;
+            const float g = G[(size_t)r * n + c];
+            L.Gp[(size_t)r * L.np + c] = g;
+            float* ms = L.msgd + (size_t)r * n + c;
+            const float v = beta1 * *ms + g;
+            *ms = v;
+            part += (double)v * (double)v;
+        }
+    }
+    const double total = block_sum_256(part, red);
+    if (threadIdx.x == 0) L.part_sgd[ck.slot] = total;
+}
+
+// nu = ||X||_F from the per-tile partial sums, then (c, s) of the beta mode
+// (Algorithm 2; Appendix A.1, Eq. 8-9). One wave per factor.
+__global__ void factor_finalize_kernel(const FactorDev* __restrict__ f, double beta2, int mode) {
+    const FactorDev F = f[blockIdx.x];
+    const double nu = sqrt(wave_sum_array(F.partials, F.nparts));
+    if (threadIdx.x != 0) return;
+    bool dyn = false;
+    if (mode == 1) dyn = nu > 0.0;                           // DYNAMIC
+    else if (mode == 2) dyn = nu > beta2 / (1.0 - beta2);    // CLAMPED
+    double beta, c, s;
+    if (dyn) {
+        beta = nu / (nu + 1.0);
+        c = 1.0 / nu;
+        s = pow(1.0 + 1.0 / nu, 0.25);
+    } else {
+        beta = beta2;
+        c = (1.0 - beta2) / beta2;
+        s = pow(beta2, -0.25);
+    }
+    FactorScalars out;
+    out.nu = nu;
+    out.beta = beta;
+    out.c = c;
+    out.s = s;
+    out.a = (float)(0.25 * c);
+    out.b = (float)(0.15625 * c * c);
+    out.sf = (float)s;
+    out.pad = 0.f;
+    *F.sc = out;
+}
+
+// A_hat <- (Z + Z^T)/2 (or Z when not symmetrizing) for a pair of 64 x 64
+// tiles (ti, tj), (tj, ti). fp32 addition commutes, so the result is bitwise
+// symmetric.
+__global__ __launch_bounds__(kEwThreads) void symmetrize_kernel(const FactorDev* __restrict__ f,
+                                                                const SymTile* __restrict__ tiles,
+                                                                int symmetrize) {
+    __shared__ float za[64][65];
+    __shared__ float zb[64][65];
+    const SymTile st = tiles[blockIdx.x];
+    const FactorDev& F = f[st.factor];
+    const int dp = F.dp, i0 = st.ti * 64, j0 = st.tj * 64;
+    const int tid = threadIdx.x;
+    // 64 rows x 16 float4 per tile, 4 per thread.
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int u = tid + q * kEwThreads, r = u >> 4, c = (u & 15) * 4;
+        if (i0 + r < dp && j0 + c < dp) {
+            const f32x4 v = *reinterpret_cast<const f32x4*>(F.W0 + (size_t)(i0 + r) * dp + j0 + c);
+            za[r][c] = v[0]; za[r][c + 1] = v[1]; za[r][c + 2] = v[2]; za[r][c + 3] = v[3];
+        }
+        if (j0 + r < dp && i0 + c < dp) {
+            const f32x4 v = *reinterpret_cast<const f32x4*>(F.W0 + (size_t)(j0 + r) * dp + i0 + c);
+            zb[r][c] = v[0]; zb[r][c + 1] = v[1]; zb[r][c + 2] = v[2]; zb[r][c + 3] = v[3];
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int u = tid + q * kEwThreads, r = u >> 4, c = (u & 15) * 4;
+        if (i0 + r < dp && j0 + c < dp) {
+            f32x4 v;
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                v[e] = symmetrize ? 0.5f * (za[r][c + e] + zb[c + e][r]) : za[r][c + e];
+            *reinterpret_cast<f32x4*>(F.A + (size_t)(i0 + r) * dp + j0 + c) = v;
+        }
+        if (st.ti != st.tj && j0 + r < dp && i0 + c < dp) {
+            f32x4 v;
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                v[e] = symmetrize ? 0.5f * (zb[r][c + e] + za[c + e][r]) : zb[r][c + e];
+            *reinterpret_cast<f32x4*>(F.A + (size_t)(j0 + r) * dp + i0 + c) = v;
+        }
+    }
+}
+
+// Per-layer norms of m and m_SGD from their partial sums, and the grafted
+// step g (Algorithm 3) with the decoupled decay factor (Section 4). One wave
+// per layer.
+__global__ void layer_finalize_kernel(const LayerDev* __restrict__ layers, double lr, double wd,
+                                      int graft) {
+    const LayerDev L = layers[blockIdx.x];
+    const double nm = sqrt(wave_sum_array(L.part_m, L.n_part_m));
+    const double ns = sqrt(wave_sum_array(L.part_sgd, L.n_part_sgd));
+    if (threadIdx.x != 0) return;
+    double g = lr;
+    if (graft) g = nm > 0.0 ? lr * ns / nm : 0.0;
+    LayerScalars out;
+    out.norm_m = nm;
+    out.norm_sgd = ns;
+    out.g = g;
+    out.gf = (float)g;
+    out.decay = (float)(1.0 - lr * wd);
+    *L.ls = out;
+}
+
+// theta <- theta (1 - lr wd) - g m over a flat chunk of one layer.
+__global__ __launch_bounds__(kEwThreads) void weight_kernel(const LayerDev* __restrict__ layers,
+                                                            const FlatChunk* __restrict__ chunks,
+                                                            int layer_base, MutPtrBatch params) {
+    const FlatChunk ck = chunks[blockIdx.x];
+    const LayerDev& L = layers[ck.layer];
+    float* __restrict__ th = params.p[ck.layer - layer_base];
+    const float g = L.ls->gf, decay = L.ls->decay;
+    const float* __restrict__ m = L.mom;
+    if ((ck.count & 3) == 0 && (reinterpret_cast<uintptr_t>(th) & 15) == 0) {
+        const int n4 = ck.count >> 2;
+        f32x4* t4 = reinterpret_cast<f32x4*>(th + ck.start);
+        const f32x4* m4 = reinterpret_cast<const f32x4*>(m + ck.start);
+        for (int e = threadIdx.x; e < n4; e += kEwThreads) {
+            f32x4 t = t4[e];
+            const f32x4 mv = m4[e];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) t[q] = t[q] * decay - g * mv[q];
+            t4[e] = t;
+        }
+    } else {
+        for (int e = threadIdx.x; e < ck.count; e += kEwThreads) {
+            const int i = ck.start + e;
+            th[i] = th[i] * decay - g * m[i];
+        }
+    }
+}
+
+}  // namespace jorge

@@ -1,0 +1,235 @@
+"""ctypes binding of libjorge.so: argument marshalling only.
+
+Every step of the Jorge update runs in the HIP kernels behind the C ABI of
+include/jorge.h. torch is used only to own device tensors and to name the
+current HIP stream; there is no CPU fallback: if the library is missing or
+fails to load, construction raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libjorge.so")
+
+JORGE_OK = 0
+BETA_MODES = {"fixed": 0, "dynamic": 1, "clamped": 2}
+STATE_KINDS = {"L": 0, "R": 1, "mom": 2, "mom_sgd": 3}
+DIAG_NAMES = ("nu_L", "nu_R", "beta_L", "beta_R", "norm_m", "norm_sgd", "g")
+
+
+class JorgeError(RuntimeError):
+    def __init__(self, status: int, detail: str = ""):
+        self.status = status
+        super().__init__(f"jorge status {status}: {detail}")
+
+
+class Shape(ctypes.Structure):
+    _fields_ = [("rows", ctypes.c_int64), ("cols", ctypes.c_int64)]
+
+
+class HParams(ctypes.Structure):
+    _fields_ = [("eps", ctypes.c_double), ("precond_interval", ctypes.c_int32),
+                ("beta_mode", ctypes.c_int32), ("graft", ctypes.c_int32),
+                ("symmetrize", ctypes.c_int32)]
+
+
+_LIB = None
+
+# name -> (restype, argtypes); mirrors include/jorge.h
+_P = ctypes.c_void_p
+_SIGNATURES = {
+    "jorge_hparams_default": (ctypes.c_int32, [ctypes.POINTER(HParams)]),
+    "jorge_create": (ctypes.c_int32, [ctypes.POINTER(Shape), ctypes.c_int32, ctypes.POINTER(HParams), _P,
+                                      ctypes.POINTER(_P)]),
+    "jorge_step": (ctypes.c_int32, [_P, ctypes.POINTER(_P), ctypes.POINTER(_P), ctypes.c_double,
+                                    ctypes.c_double, ctypes.c_double, ctypes.c_double]),
+    "jorge_get_state": (ctypes.c_int32, [_P, ctypes.c_int32, ctypes.c_int32, _P, ctypes.c_int64]),
+    "jorge_set_state": (ctypes.c_int32, [_P, ctypes.c_int32, ctypes.c_int32, _P, ctypes.c_int64]),
+    "jorge_state_ptr": (ctypes.c_int32, [_P, ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(_P),
+                                         ctypes.POINTER(ctypes.c_int64)]),
+    "jorge_get_step": (ctypes.c_int32, [_P, ctypes.POINTER(ctypes.c_int64)]),
+    "jorge_set_step": (ctypes.c_int32, [_P, ctypes.c_int64]),
+    "jorge_read_diag": (ctypes.c_int32, [_P, ctypes.c_int32, ctypes.POINTER(ctypes.c_double)]),
+    "jorge_set_stream": (ctypes.c_int32, [_P, _P]),
+    "jorge_synchronize": (ctypes.c_int32, [_P]),
+    "jorge_device_bytes": (ctypes.c_int32, [_P, ctypes.POINTER(ctypes.c_int64)]),
+    "jorge_set_timing": (ctypes.c_int32, [_P, ctypes.c_int32]),
+    "jorge_read_timing": (ctypes.c_int32, [_P, ctypes.POINTER(ctypes.c_double),
+                                           ctypes.POINTER(ctypes.c_int64), ctypes.c_int32]),
+    "jorge_reset_timing": (ctypes.c_int32, [_P]),
+    "jorge_num_stages": (ctypes.c_int32, []),
+    "jorge_stage_name": (ctypes.c_char_p, [ctypes.c_int32]),
+    "jorge_destroy": (None, [_P]),
+    "jorge_status_string": (ctypes.c_char_p, [ctypes.c_int32]),
+    "jorge_last_error": (ctypes.c_char_p, [_P]),
+}
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Loads libjorge.so (built by paper_2310_12298_amd.build); raises if absent."""
+    global _LIB
+    if _LIB is not None:
+        return _LIB
+    if not os.path.exists(path):
+        raise FileNotFoundError(f"{path} is not built; run __graft_entry__.build() or "
+                                f"python -m paper_2310_12298_amd.build")
+    lib = ctypes.CDLL(path)
+    for name, (res, args) in _SIGNATURES.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _LIB = lib
+    return lib
+
+
+def _check(lib, status, ctx=None):
+    if status != JORGE_OK:
+        detail = lib.jorge_status_string(status).decode()
+        if ctx:
+            extra = lib.jorge_last_error(ctx).decode()
+            if extra:
+                detail += f" ({extra})"
+        raise JorgeError(status, detail)
+
+
+def _current_stream():
+    import torch
+    return torch.cuda.current_stream().cuda_stream
+
+
+class Jorge:
+    """A Jorge optimizer context over a fixed list of m x n layers.
+
+    shapes: list of (rows, cols). State lives on the current HIP device.
+    """
+
+    def __init__(self, shapes, eps=1e-6, precond_interval=1, beta_mode="clamped", graft=True,
+                 symmetrize=True, stream=None):
+        self.lib = load_library()
+        self.shapes = [(int(m), int(n)) for m, n in shapes]
+        hp = HParams()
+        _check(self.lib, self.lib.jorge_hparams_default(ctypes.byref(hp)))
+        hp.eps = float(eps)
+        hp.precond_interval = int(precond_interval)
+        hp.beta_mode = BETA_MODES[beta_mode] if isinstance(beta_mode, str) else int(beta_mode)
+        hp.graft = int(bool(graft))
+        hp.symmetrize = int(bool(symmetrize))
+        arr = (Shape * len(self.shapes))(*[Shape(m, n) for m, n in self.shapes])
+        ctx = _P()
+        s = _current_stream() if stream is None else int(stream)
+        _check(self.lib, self.lib.jorge_create(arr, len(self.shapes), ctypes.byref(hp), _P(s),
+                                               ctypes.byref(ctx)))
+        self.ctx = ctx
+
+    # -------------------------------------------------------------- stepping
+    def _ptrs(self, tensors, what):
+        import torch
+        if len(tensors) != len(self.shapes):
+            raise ValueError(f"{what}: expected {len(self.shapes)} tensors, got {len(tensors)}")
+        for t, (m, n) in zip(tensors, self.shapes):
+            if not (isinstance(t, torch.Tensor) and t.is_cuda and t.dtype == torch.float32
+                    and t.is_contiguous() and tuple(t.shape) == (m, n)):
+                raise ValueError(f"{what}: need contiguous fp32 cuda tensors of shape {(m, n)}")
+        return (_P * len(tensors))(*[t.data_ptr() for t in tensors])
+
+    def step(self, params, grads, lr, beta2=0.9, beta1=0.9, weight_decay=0.0):
+        """One Jorge step for all layers on the context's stream (params updated in place)."""
+        p = self._ptrs(params, "params")
+        g = self._ptrs(grads, "grads")
+        _check(self.lib, self.lib.jorge_step(self.ctx, p, g, float(lr), float(beta2), float(beta1),
+                                             float(weight_decay)), self.ctx)
+
+    def step_ptrs(self, param_ptrs, grad_ptrs, lr, beta2=0.9, beta1=0.9, weight_decay=0.0):
+        """Same as step, from prebuilt ctypes pointer arrays (no per-call checks)."""
+        _check(self.lib, self.lib.jorge_step(self.ctx, param_ptrs, grad_ptrs, float(lr), float(beta2),
+                                             float(beta1), float(weight_decay)), self.ctx)
+
+    @staticmethod
+    def pointer_array(tensors):
+        return (_P * len(tensors))(*[t.data_ptr() for t in tensors])
+
+    # -------------------------------------------------------------- state
+    def _dims(self, layer, kind):
+        m, n = self.shapes[layer]
+        return {0: (m, m), 1: (n, n), 2: (m, n), 3: (m, n)}[kind]
+
+    def get_state(self, layer, kind):
+        """Copy of one state tensor as a new fp32 device tensor (stream-ordered)."""
+        import torch
+        kind = STATE_KINDS[kind] if isinstance(kind, str) else int(kind)
+        r, c = self._dims(layer, kind)
+        out = torch.empty((r, c), dtype=torch.float32, device="cuda")
+        _check(self.lib, self.lib.jorge_get_state(self.ctx, layer, kind, _P(out.data_ptr()), c), self.ctx)
+        return out
+
+    def set_state(self, layer, kind, tensor):
+        import torch
+        kind = STATE_KINDS[kind] if isinstance(kind, str) else int(kind)
+        r, c = self._dims(layer, kind)
+        t = tensor.to(device="cuda", dtype=torch.float32).contiguous()
+        if tuple(t.shape) != (r, c):
+            raise ValueError(f"state shape {tuple(t.shape)} != {(r, c)}")
+        _check(self.lib, self.lib.jorge_set_state(self.ctx, layer, kind, _P(t.data_ptr()), c), self.ctx)
+        self.synchronize()            # t may be freed once this returns
+
+    def state_ptr(self, layer, kind):
+        kind = STATE_KINDS[kind] if isinstance(kind, str) else int(kind)
+        p, ld = _P(), ctypes.c_int64()
+        _check(self.lib, self.lib.jorge_state_ptr(self.ctx, layer, kind, ctypes.byref(p), ctypes.byref(ld)),
+               self.ctx)
+        return p.value, ld.value
+
+    @property
+    def t(self):
+        v = ctypes.c_int64()
+        _check(self.lib, self.lib.jorge_get_step(self.ctx, ctypes.byref(v)))
+        return v.value
+
+    @t.setter
+    def t(self, value):
+        _check(self.lib, self.lib.jorge_set_step(self.ctx, int(value)), self.ctx)
+
+    def read_diag(self, layer):
+        out = (ctypes.c_double * len(DIAG_NAMES))()
+        _check(self.lib, self.lib.jorge_read_diag(self.ctx, layer, out), self.ctx)
+        return dict(zip(DIAG_NAMES, list(out)))
+
+    def synchronize(self):
+        _check(self.lib, self.lib.jorge_synchronize(self.ctx), self.ctx)
+
+    def set_stream(self, stream):
+        _check(self.lib, self.lib.jorge_set_stream(self.ctx, _P(int(stream))), self.ctx)
+
+    def device_bytes(self):
+        v = ctypes.c_int64()
+        _check(self.lib, self.lib.jorge_device_bytes(self.ctx, ctypes.byref(v)))
+        return v.value
+
+    # -------------------------------------------------------------- timing
+    def set_timing(self, enable: bool):
+        _check(self.lib, self.lib.jorge_set_timing(self.ctx, int(bool(enable))), self.ctx)
+
+    def reset_timing(self):
+        _check(self.lib, self.lib.jorge_reset_timing(self.ctx), self.ctx)
+
+    def read_timing(self):
+        """{stage name: (total ms, launches)} accumulated since the last reset (synchronises)."""
+        n = self.lib.jorge_num_stages()
+        ms = (ctypes.c_double * n)()
+        cnt = (ctypes.c_int64 * n)()
+        _check(self.lib, self.lib.jorge_read_timing(self.ctx, ms, cnt, n), self.ctx)
+        return {self.lib.jorge_stage_name(i).decode(): (ms[i], cnt[i]) for i in range(n)}
+
+    # -------------------------------------------------------------- lifetime
+    def close(self):
+        if getattr(self, "ctx", None):
+            self.lib.jorge_destroy(self.ctx)
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -72,3 +72,26 @@ def initial_params(seed: int, layer: int, shape) -> np.ndarray:
 
 def param_count(shapes) -> int:
     return int(sum(m * n for m, n in shapes))
+
+
+def _stream_seed(seed: int, layer: int, t: int) -> int:
+    """64-bit seed of the (seed, layer, t) stream, from numpy's SeedSequence."""
+    return int(np.random.SeedSequence([seed, layer, t]).generate_state(1, np.uint64)[0] >> 1)
+
+
+def device_gradient(seed: int, layer: int, t: int, shape, sigma: float, device: str = "cuda"):
+    """G[layer, t] drawn on the device (torch's Philox generator), N(0, sigma^2) fp32.
+
+    A different stream from gradient(): used where host generation would take
+    longer than the measurement (pre-staging many full-size gradient sets).
+    """
+    import torch
+    gen = torch.Generator(device=device)
+    gen.manual_seed(_stream_seed(seed, layer, t))
+    return torch.randn(tuple(shape), generator=gen, device=device, dtype=torch.float32).mul_(sigma)
+
+
+def device_initial_params(seed: int, layer: int, shape, device: str = "cuda"):
+    """theta_0[layer] drawn on the device: N(0, 2/n) fp32."""
+    m, n = shape
+    return device_gradient(seed, layer, THETA_STREAM, shape, float(np.sqrt(2.0 / n)), device)

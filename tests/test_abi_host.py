@@ -1,0 +1,119 @@
+"""C-ABI checks that need no GPU: the library loads, exports every entry point
+that include/jorge.h declares, and rejects invalid arguments before any HIP
+call is made."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2310_12298_amd import jorge as J
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "jorge.h")
+
+ERR_INVALID, ERR_UNSUPPORTED = -1, -4
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return re.findall(r"\b(jorge_[a-z_]+)\s*\(", text)
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(J.LIB_PATH):
+        from paper_2310_12298_amd.build import build_library
+        build_library()
+    return J.load_library()
+
+
+def test_header_declares_expected_api():
+    names = set(declared_functions())
+    assert {"jorge_create", "jorge_step", "jorge_destroy", "jorge_get_state", "jorge_set_state"} <= names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = set(declared_functions())
+    missing = [n for n in names if not hasattr(lib, n)]
+    assert not missing, missing
+    # The binding marshals exactly the declared entry points.
+    assert names == set(J._SIGNATURES)
+
+
+def test_hparams_default(lib):
+    hp = J.HParams()
+    assert lib.jorge_hparams_default(ctypes.byref(hp)) == 0
+    assert (hp.eps, hp.precond_interval, hp.beta_mode, hp.graft, hp.symmetrize) == (1e-6, 1, 2, 1, 1)
+    assert lib.jorge_hparams_default(None) == ERR_INVALID
+
+
+def _create(lib, shapes, hp=None):
+    arr = (J.Shape * max(1, len(shapes)))(*[J.Shape(m, n) for m, n in shapes])
+    out = ctypes.c_void_p(12345)
+    st = lib.jorge_create(arr, len(shapes), ctypes.byref(hp) if hp else None, None, ctypes.byref(out))
+    return st, out.value
+
+
+@pytest.mark.parametrize("shapes", [[], [(0, 4)], [(4, 0)], [(-1, 3)], [(3, 4), (5, -2)]])
+def test_create_rejects_bad_shapes(lib, shapes):
+    st, out = _create(lib, shapes)
+    assert st == ERR_INVALID and out is None
+
+
+def test_create_rejects_oversize(lib):
+    st, out = _create(lib, [(4, 32769)])
+    assert st == ERR_UNSUPPORTED and out is None
+
+
+@pytest.mark.parametrize("field,value", [("eps", 0.0), ("eps", -1.0), ("eps", float("inf")),
+                                         ("eps", float("nan")), ("precond_interval", 0),
+                                         ("beta_mode", 3), ("beta_mode", -1), ("graft", 2),
+                                         ("symmetrize", -1)])
+def test_create_rejects_bad_hparams(lib, field, value):
+    hp = J.HParams()
+    lib.jorge_hparams_default(ctypes.byref(hp))
+    setattr(hp, field, value)
+    st, out = _create(lib, [(4, 4)], hp)
+    assert st == ERR_INVALID and out is None
+
+
+def test_null_arguments(lib):
+    shp = (J.Shape * 1)(J.Shape(2, 2))
+    assert lib.jorge_create(shp, 1, None, None, None) == ERR_INVALID
+    assert lib.jorge_create(None, 1, None, None, ctypes.byref(ctypes.c_void_p())) == ERR_INVALID
+    P = ctypes.c_void_p
+    arr = (P * 1)(P(0))
+    assert lib.jorge_step(None, arr, arr, 0.1, 0.9, 0.9, 0.0) == ERR_INVALID
+    assert lib.jorge_get_state(None, 0, 0, P(16), 4) == ERR_INVALID
+    assert lib.jorge_set_state(None, 0, 0, P(16), 4) == ERR_INVALID
+    assert lib.jorge_state_ptr(None, 0, 0, ctypes.byref(P()), ctypes.byref(ctypes.c_int64())) == ERR_INVALID
+    assert lib.jorge_get_step(None, ctypes.byref(ctypes.c_int64())) == ERR_INVALID
+    assert lib.jorge_set_step(None, 0) == ERR_INVALID
+    assert lib.jorge_read_diag(None, 0, (ctypes.c_double * 7)()) == ERR_INVALID
+    assert lib.jorge_set_stream(None, None) == ERR_INVALID
+    assert lib.jorge_synchronize(None) == ERR_INVALID
+    assert lib.jorge_device_bytes(None, ctypes.byref(ctypes.c_int64())) == ERR_INVALID
+    assert lib.jorge_set_timing(None, 1) == ERR_INVALID
+    assert lib.jorge_read_timing(None, None, None, 0) == ERR_INVALID
+    assert lib.jorge_reset_timing(None) == ERR_INVALID
+    lib.jorge_destroy(None)
+    assert lib.jorge_last_error(None) == b""
+
+
+def test_stage_names_and_status_strings(lib):
+    n = lib.jorge_num_stages()
+    names = [lib.jorge_stage_name(i).decode() for i in range(n)]
+    assert names[0] == "stage_in" and "xform" in names and names[-1] == "weight"
+    assert len(set(names)) == n
+    assert lib.jorge_stage_name(n) is None and lib.jorge_stage_name(-1) is None
+    assert lib.jorge_status_string(0) == b"ok"
+    assert lib.jorge_status_string(-1) == b"invalid argument"
+    assert lib.jorge_status_string(-99) == b"unknown status"
+
+
+def test_binding_fails_loudly_without_library(tmp_path, monkeypatch):
+    monkeypatch.setattr(J, "_LIB", None)
+    with pytest.raises(FileNotFoundError):
+        J.load_library(str(tmp_path / "missing.so"))
