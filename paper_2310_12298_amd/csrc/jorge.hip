@@ -149,11 +149,11 @@ struct TimedLaunch {
         if (!c->timing) return;
         start = take_event(c);
         stop = take_event(c);
-        if (start) hipEventRecord(start, c->stream);
+        if (start) (void)hipEventRecord(start, c->stream);
     }
     void finish() {
         if (!c->timing || !start || !stop) return;
-        hipEventRecord(stop, c->stream);
+        (void)hipEventRecord(stop, c->stream);
         c->pending.push_back({stage, start, stop});
     }
 };
@@ -174,6 +174,50 @@ void add_problem(GemmStage& st, const GemmProblem& p, bool upper_only) {
 }
 
 int tile_count(int M, int N) { return ((M + kTile - 1) / kTile) * ((N + kTile - 1) / kTile); }
+
+constexpr int kXcds = 8;  // workgroup b of a launch runs on XCD b % 8, in increasing b
+
+// Puts a stage's tiles in dispatch order. The tiles come in problem order
+// (largest first), each problem in bands of kGroupRows tile rows walked column
+// by column. Runs of consecutive tiles of one problem and one column (they
+// share the B panel and neighbouring A panels) are dealt, in that order, to
+// the XCD with the least accumulated work (K of the tile), so every XCD gets
+// a balanced, largest-first share whose tiles reuse panels in its own L2.
+// The shares are then interleaved so that XCD x's i-th tile sits at slot
+// kXcds * i + x; once a share is used up, its slots take the next tile of the
+// longest remaining share.
+void order_for_xcds(GemmStage& st) {
+    const size_t n = st.tiles.size();
+    if (n == 0) return;
+    std::vector<std::vector<TileDesc>> share(kXcds);
+    std::vector<int64_t> work(kXcds, 0);
+    for (size_t i = 0; i < n;) {
+        size_t j = i + 1;
+        while (j < n && st.tiles[j].prob == st.tiles[i].prob && st.tiles[j].tn == st.tiles[i].tn &&
+               st.tiles[j].tm / kGroupRows == st.tiles[i].tm / kGroupRows)
+            ++j;
+        const int x = (int)(std::min_element(work.begin(), work.end()) - work.begin());
+        for (size_t k = i; k < j; ++k) share[x].push_back(st.tiles[k]);
+        work[x] += (int64_t)(j - i) * st.probs[st.tiles[i].prob].K;
+        i = j;
+    }
+    std::vector<size_t> next(kXcds, 0);
+    std::vector<TileDesc> out;
+    out.reserve(n);
+    for (size_t b = 0; b < n; ++b) {
+        int x = (int)(b % kXcds);
+        if (next[x] == share[x].size()) {
+            size_t best = 0;
+            for (int y = 0; y < kXcds; ++y)
+                if (share[y].size() - next[y] > best) {
+                    best = share[y].size() - next[y];
+                    x = y;
+                }
+        }
+        out.push_back(share[x][next[x]++]);
+    }
+    st.tiles.swap(out);
+}
 
 template <bool AK, bool BK, int EPI>
 jorge_status launch_gemm(jorge_ctx* c, const GemmStage& st, int stage, float beta1) {
@@ -369,6 +413,7 @@ jorge_status upload(jorge_ctx* c, const std::vector<T>& v, T** dptr) {
 }
 
 jorge_status upload_stage(jorge_ctx* c, GemmStage& st) {
+    order_for_xcds(st);
     jorge_status s = upload(c, st.probs, &st.dprobs);
     if (s != JORGE_OK) return s;
     return upload(c, st.tiles, &st.dtiles);

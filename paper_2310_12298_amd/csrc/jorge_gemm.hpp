@@ -32,13 +32,14 @@ constexpr int kLdsMN = kTile + 8;             // row stride of an M/N-contiguous
 constexpr int kLdsOperand = kTile * kLdsK;    // floats per operand per stage (>= kSlab * kLdsMN)
 static_assert(kLdsOperand >= kSlab * kLdsMN, "LDS operand buffer too small");
 
-// Workgroups are dispatched round-robin over the 8 XCDs. Remap the dispatch
-// index so each XCD walks a contiguous run of the tile list, keeping tiles
-// that share A rows and B columns in the same L2.
-__device__ __forceinline__ int xcd_remap(int bid, int n) {
-    const int q = n >> 3, r = n & 7;
-    const int x = bid & 7, i = bid >> 3;
-    return (x < r) ? x * (q + 1) + i : r * (q + 1) + (x - r) * q + i;
+// Pointers into global memory (address space 1): loads through them compile
+// to global_load rather than flat_load, which would also count against the
+// LDS wait counter and make every LDS wait drain the in-flight prefetch.
+typedef __attribute__((address_space(1))) const f32x4 global_f32x4;
+typedef __attribute__((address_space(1))) const float global_f32;
+
+__device__ __forceinline__ f32x4 gload4(const float* p) {
+    return *(global_f32x4*)p;
 }
 
 // Global -> registers: one 128 x 32 operand slab, four 16-byte loads per thread.
@@ -53,10 +54,10 @@ __device__ __forceinline__ void load_slab(const float* __restrict__ base, int ld
         const int u = tid + i * kGemmThreads;
         if constexpr (KMAJ) {
             const int row = min(mn0 + (u >> 3), lim - 1);
-            r[i] = *reinterpret_cast<const f32x4*>(base + (size_t)row * ld + k0 + (u & 7) * 4);
+            r[i] = gload4(base + (size_t)row * ld + k0 + (u & 7) * 4);
         } else {
             const int col = min(mn0 + (u & 31) * 4, lim - 4);
-            r[i] = *reinterpret_cast<const f32x4*>(base + (size_t)(k0 + (u >> 5)) * ld + col);
+            r[i] = gload4(base + (size_t)(k0 + (u >> 5)) * ld + col);
         }
     }
 }
@@ -87,17 +88,27 @@ __device__ __forceinline__ void fragment(const float* s, int mn, int k, float (&
     }
 }
 
+// The MFMAs of one LDS slab. Fragments of the next 8-wide k group are read
+// from LDS while the MFMAs of the current group run.
 template <bool AK, bool BK>
 __device__ __forceinline__ void mma_slab(const float* sa, const float* sb, int wy, int wx, int lane,
                                          f32x16 (&acc)[2][2]) {
     const int r = lane & 31, h = lane >> 5;
+    float a[2][2][4], b[2][2][4];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        fragment<AK>(sa, wy * 64 + i * 32 + r, h * 4, a[0][i]);
+        fragment<BK>(sb, wx * 64 + i * 32 + r, h * 4, b[0][i]);
+    }
 #pragma unroll
     for (int k8 = 0; k8 < kSlab / 8; ++k8) {
-        float a[2][4], b[2][4];
+        const int cur = k8 & 1;
+        if (k8 + 1 < kSlab / 8) {
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            fragment<AK>(sa, wy * 64 + i * 32 + r, k8 * 8 + h * 4, a[i]);
-            fragment<BK>(sb, wx * 64 + i * 32 + r, k8 * 8 + h * 4, b[i]);
+            for (int i = 0; i < 2; ++i) {
+                fragment<AK>(sa, wy * 64 + i * 32 + r, (k8 + 1) * 8 + h * 4, a[cur ^ 1][i]);
+                fragment<BK>(sb, wx * 64 + i * 32 + r, (k8 + 1) * 8 + h * 4, b[cur ^ 1][i]);
+            }
         }
 #pragma unroll
         for (int s = 0; s < 4; ++s)
@@ -105,7 +116,8 @@ __device__ __forceinline__ void mma_slab(const float* sa, const float* sb, int w
             for (int i = 0; i < 2; ++i)
 #pragma unroll
                 for (int j = 0; j < 2; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][s], b[j][s], acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[cur][i][s], b[cur][j][s], acc[i][j],
+                                                                     0, 0, 0);
     }
 }
 
@@ -125,8 +137,11 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_grouped(const GemmProble
     __shared__ __attribute__((aligned(16))) float lds[2][2][kLdsOperand];
     __shared__ double red[4];
 
-    const TileDesc td = tiles[xcd_remap(blockIdx.x, gridDim.x)];
-    const GemmProblem& p = probs[td.prob];
+    // The tile list is in dispatch order: consecutive workgroups go round-robin
+    // to the 8 XCDs, and the host arranged the list so each XCD's share is
+    // balanced and reuses operand panels in its own L2.
+    const TileDesc td = tiles[blockIdx.x];
+    const GemmProblem p = probs[td.prob];
     const int row0 = td.tm * kTile, col0 = td.tn * kTile;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int wy = wave >> 1, wx = wave & 1;
@@ -200,7 +215,7 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_grouped(const GemmProble
                             float out = v;
                             if constexpr (EPI == EPI_NORM) part += (double)v * (double)v;
                             if constexpr (EPI == EPI_POLY) {
-                                const float x = p.X[(size_t)row * p.ldx + col];
+                                const float x = *(global_f32*)(p.X + (size_t)row * p.ldx + col);
                                 const float id = (row == col && row < p.valid_m) ? 1.0f : 0.0f;
                                 out = id - a * x + b * v;
                             }
