@@ -30,11 +30,9 @@ WORKLOAD_NAMES = {
 
 def stage_flops(shapes):
     """Algorithmic flops of one update step per GEMM stage (symmetric products count half)."""
-    f = {k: 0 for k in ("gram_L", "gram_R", "pow2", "pow4", "xform", "poly", "update", "precond_L",
-                        "precond_R")}
+    f = {k: 0 for k in ("gram", "pow2", "pow4", "xform", "poly", "update", "precond_L", "precond_R")}
     for m, n in shapes:
-        f["gram_L"] += m * m * n
-        f["gram_R"] += n * n * m
+        f["gram"] += m * m * n + n * n * m
         for d in (m, n):
             f["pow2"] += d ** 3
             f["pow4"] += d ** 3
@@ -154,6 +152,8 @@ def main():
 
     updates = sum(1 for i in range(args.warmup, args.warmup + steps) if i % args.interval == 0)
     flops = stage_flops(shapes)
+    if timing["pow2"][1] == 0:          # A^2 shares the gram launch when factors are symmetric
+        flops["gram"] += flops.pop("pow2")
     per_stage = {k: {"ms_per_launch": (v[0] / v[1]) if v[1] else 0.0, "launches": v[1]}
                  for k, v in timing.items()}
     gemm_ms = sum(timing[k][0] for k in flops)
@@ -164,7 +164,7 @@ def main():
     hbm = stage_bytes(shapes)
     w_ms = timing["weight"][0] / max(1, timing["weight"][1])
     for k, v in per_stage.items():
-        if k in flops:
+        if k in flops and v["launches"]:
             v["tflops"] = flops[k] / (v["ms_per_launch"] * 1e-3) / 1e12 if v["ms_per_launch"] else 0.0
     out = {
         "metric": METRIC,

@@ -8,9 +8,9 @@
 // step is a fixed sequence of launches on one stream with no host sync.
 //
 // Update step (Algorithm 2, Appendix A.1, Algorithm 3, Section 4):
-//   stage-in   Gp <- G, m_SGD <- beta1 m_SGD + G, partial sums of m_SGD^2
-//   gram       M_L = G G^T, M_R = G^T G                 (symmetric tiles only)
-//   pow2/pow4  A^2 = A A, A^4 = A^2 A^2                 (symmetric tiles only)
+//   stage-in   Gp <- G, Gpt <- G^T, m_SGD <- beta1 m_SGD + G, partial sums of m_SGD^2
+//   gram       M_L = G G^T, M_R = G^T G and A^2 = A A     (one launch, symmetric tiles only)
+//   pow4       A^4 = A^2 A^2                              (symmetric tiles only)
 //   xform      X = A^4 M, partial sums of X^2
 //   ffinal     nu = ||X||_F, beta, c, s per factor
 //   poly       P = I - (c/4) X + (5c^2/32) X X
@@ -39,16 +39,17 @@ using namespace jorge;
 
 namespace {
 
+// Timed stages. With symmetric factors the Gram products and A^2 share the
+// "gram" launch and "pow2" has none; the literal mode launches pow2 apart.
 enum Stage : int {
-    ST_STAGEIN = 0, ST_GRAM_L, ST_GRAM_R, ST_POW2, ST_POW4, ST_XFORM, ST_FFINAL, ST_POLY,
-    ST_UPDATE, ST_SYMM, ST_PRECOND_L, ST_PRECOND_R, ST_LFINAL, ST_WEIGHT, ST_COUNT
+    ST_STAGEIN = 0, ST_GRAM, ST_POW2, ST_POW4, ST_XFORM, ST_FFINAL, ST_POLY, ST_UPDATE, ST_SYMM,
+    ST_PRECOND_L, ST_PRECOND_R, ST_LFINAL, ST_WEIGHT, ST_COUNT
 };
 const char* const kStageNames[ST_COUNT] = {
-    "stage_in", "gram_L", "gram_R", "pow2", "pow4", "xform", "factor_finalize", "poly",
-    "update", "symmetrize", "precond_L", "precond_R", "layer_finalize", "weight"};
+    "stage_in", "gram", "pow2", "pow4", "xform", "factor_finalize", "poly", "update", "symmetrize",
+    "precond_L", "precond_R", "layer_finalize", "weight"};
 
 constexpr size_t kAlign = 256;
-constexpr int kRowChunkElems = 16384;
 constexpr int kFlatChunkElems = 16384;
 constexpr int kGroupRows = 8;  // tile rows per group in the tile ordering
 
@@ -64,7 +65,7 @@ struct GemmStage {
 
 struct LayerHost {
     int m, n, mp, np;
-    size_t off_Gp, off_T, off_mom, off_msgd, off_part_m, off_part_sgd, off_ls;
+    size_t off_Gp, off_Gpt, off_T, off_mom, off_msgd, off_part_m, off_part_sgd, off_ls;
     int n_part_m = 0, n_part_sgd = 0;
     int fL, fR;
 };
@@ -94,14 +95,14 @@ struct jorge_ctx {
     // device tables
     LayerDev* dlayers = nullptr;
     FactorDev* dfactors = nullptr;
-    RowChunk* drow = nullptr;
+    StageTile* dstage = nullptr;
     FlatChunk* dflat = nullptr;
     SymTile* dsym = nullptr;
-    std::vector<RowChunk> row_chunks;
+    std::vector<StageTile> stage_tiles;
     std::vector<FlatChunk> flat_chunks;
-    std::vector<int> row_batch_start, flat_batch_start;  // chunk index of each layer batch
+    std::vector<int> stage_batch_start, flat_batch_start;  // first block of each layer batch
     std::vector<SymTile> sym_tiles;
-    GemmStage gram_l, gram_r, pow2, pow4, xform, poly, update, pre_l, pre_r;
+    GemmStage gram, pow2, pow4, xform, poly, update, pre_l, pre_r;
     // timing
     bool timing = false;
     std::vector<hipEvent_t> free_events;
@@ -177,9 +178,9 @@ int tile_count(int M, int N) { return ((M + kTile - 1) / kTile) * ((N + kTile - 
 
 constexpr int kXcds = 8;  // workgroup b of a launch runs on XCD b % 8, in increasing b
 
-// Puts a stage's tiles in dispatch order. The tiles come in problem order
-// (largest first), each problem in bands of kGroupRows tile rows walked column
-// by column. Runs of consecutive tiles of one problem and one column (they
+// Puts a stage's tiles in dispatch order. The tiles are sorted by K, longest
+// first; each problem's tiles stay in bands of kGroupRows tile rows walked
+// column by column. Runs of consecutive tiles of one problem and one column (they
 // share the B panel and neighbouring A panels) are dealt, in that order, to
 // the XCD with the least accumulated work (K of the tile), so every XCD gets
 // a balanced, largest-first share whose tiles reuse panels in its own L2.
@@ -189,6 +190,10 @@ constexpr int kXcds = 8;  // workgroup b of a launch runs on XCD b % 8, in incre
 void order_for_xcds(GemmStage& st) {
     const size_t n = st.tiles.size();
     if (n == 0) return;
+    // Longest K first (stable: each problem's tiles stay together and in order).
+    std::stable_sort(st.tiles.begin(), st.tiles.end(), [&](const TileDesc& a, const TileDesc& b) {
+        return st.probs[a.prob].K > st.probs[b.prob].K;
+    });
     std::vector<std::vector<TileDesc>> share(kXcds);
     std::vector<int64_t> work(kXcds, 0);
     for (size_t i = 0; i < n;) {
@@ -271,13 +276,13 @@ size_t plan(jorge_ctx* c) {
         const size_t padded = (size_t)L.mp * L.np * sizeof(float);
         const size_t dense = (size_t)L.m * L.n * sizeof(float);
         L.off_Gp = take(padded);
+        L.off_Gpt = take(padded);
         L.off_T = take(padded);
         L.off_mom = take(dense);
         L.off_msgd = take(dense);
         L.n_part_m = tile_count(L.mp, L.np);
         L.off_part_m = take((size_t)L.n_part_m * sizeof(double));
-        const int rows_per_chunk = std::max(1, std::min(L.m, kRowChunkElems / std::max(L.n, 1)));
-        L.n_part_sgd = (L.m + rows_per_chunk - 1) / rows_per_chunk;
+        L.n_part_sgd = ((L.m + 63) / 64) * ((L.n + 63) / 64);
         L.off_part_sgd = take((size_t)L.n_part_sgd * sizeof(double));
         L.off_ls = take(sizeof(LayerScalars));
     }
@@ -307,6 +312,7 @@ void build_tables(jorge_ctx* c, std::vector<LayerDev>& ld, std::vector<FactorDev
         auto& L = c->layers[li];
         LayerDev d{};
         d.Gp = at<float>(c, L.off_Gp);
+        d.Gpt = at<float>(c, L.off_Gpt);
         d.T = at<float>(c, L.off_T);
         d.mom = at<float>(c, L.off_mom);
         d.msgd = at<float>(c, L.off_msgd);
@@ -318,21 +324,21 @@ void build_tables(jorge_ctx* c, std::vector<LayerDev>& ld, std::vector<FactorDev
         d.n_part_sgd = L.n_part_sgd;
         ld.push_back(d);
     }
-    // Per-layer chunk lists, batched by kPtrBatch layers (user pointers go in kernel arguments).
+    // Per-layer block lists, batched by kPtrBatch layers (user pointers go in kernel arguments).
     for (int li = 0; li < nl; ++li) {
         if (li % kPtrBatch == 0) {
-            c->row_batch_start.push_back((int)c->row_chunks.size());
+            c->stage_batch_start.push_back((int)c->stage_tiles.size());
             c->flat_batch_start.push_back((int)c->flat_chunks.size());
         }
         const auto& L = c->layers[li];
-        const int rpc = std::max(1, std::min(L.m, kRowChunkElems / std::max(L.n, 1)));
-        for (int r = 0, s = 0; r < L.m; r += rpc, ++s)
-            c->row_chunks.push_back({li, r, std::min(rpc, L.m - r), s});
+        int slot = 0;
+        for (int r = 0; r < L.m; r += 64)
+            for (int q = 0; q < L.n; q += 64) c->stage_tiles.push_back({li, r, q, slot++});
         const int64_t total = (int64_t)L.m * L.n;
         for (int64_t st = 0; st < total; st += kFlatChunkElems)
             c->flat_chunks.push_back({li, (int)st, (int)std::min<int64_t>(kFlatChunkElems, total - st), 0});
     }
-    c->row_batch_start.push_back((int)c->row_chunks.size());
+    c->stage_batch_start.push_back((int)c->stage_tiles.size());
     c->flat_batch_start.push_back((int)c->flat_chunks.size());
 
     // Factors in decreasing size, so large tiles are dispatched first.
@@ -349,20 +355,14 @@ void build_tables(jorge_ctx* c, std::vector<LayerDev>& ld, std::vector<FactorDev
         g.M = g.N = g.K = F.dp;
         g.lda = g.ldb = g.ldc = g.ldx = F.dp;
         g.valid_m = g.valid_n = F.d;
-        // Gram statistic into W0.
+        // Gram statistic into W0: G G^T = Gp Gp^T (K = np) and G^T G = Gpt Gpt^T (K = mp),
+        // both with K-contiguous operands.
         GemmProblem s = g;
         s.C = d.W0;
-        if (F.side == 0) {  // G G^T: A = Gp (K-major), B^T = Gp (K-major), K = np
-            s.A = s.B = l.Gp;
-            s.K = L.np;
-            s.lda = s.ldb = L.np;
-            add_problem(c->gram_l, s, true);
-        } else {            // G^T G: A = Gp^T (M-major), B = Gp (N-major), K = mp
-            s.A = s.B = l.Gp;
-            s.K = L.mp;
-            s.lda = s.ldb = L.np;
-            add_problem(c->gram_r, s, true);
-        }
+        s.A = s.B = F.side == 0 ? l.Gp : l.Gpt;
+        s.K = F.side == 0 ? L.np : L.mp;
+        s.lda = s.ldb = s.K;
+        add_problem(c->gram, s, true);
         // With symmetric factors A^2 and A^4 are symmetric products (upper tiles, mirrored);
         // the literal mode keeps non-symmetric factors and needs the general product.
         const bool sym = c->hp.symmetrize != 0;
@@ -387,10 +387,10 @@ void build_tables(jorge_ctx* c, std::vector<LayerDev>& ld, std::vector<FactorDev
     for (int li : lorder) {
         const auto& L = c->layers[li];
         const LayerDev& l = ld[li];
-        GemmProblem a{};  // T = L_hat Gp: A = L_hat (K-major), B = Gp (N-major)
-        a.A = fd[L.fL].A; a.B = l.Gp; a.C = l.T;
+        GemmProblem a{};  // T = L_hat G: A = L_hat, B^T = Gpt (both K-major)
+        a.A = fd[L.fL].A; a.B = l.Gpt; a.C = l.T;
         a.M = L.mp; a.N = L.np; a.K = L.mp;
-        a.lda = L.mp; a.ldb = L.np; a.ldc = L.np;
+        a.lda = L.mp; a.ldb = L.mp; a.ldc = L.np;
         a.valid_m = L.m; a.valid_n = L.n;
         add_problem(c->pre_l, a, false);
         GemmProblem b{};  // G~ = T R_hat: A = T (K-major), B = R_hat (K-major when symmetric)
@@ -412,6 +412,19 @@ jorge_status upload(jorge_ctx* c, const std::vector<T>& v, T** dptr) {
     return JORGE_OK;
 }
 
+// Moves every problem and tile of `from` into `into` (same kernel instantiation),
+// so independent products share one launch.
+void merge_stage(GemmStage& into, GemmStage& from) {
+    const int base = (int)into.probs.size();
+    into.probs.insert(into.probs.end(), from.probs.begin(), from.probs.end());
+    for (TileDesc t : from.tiles) {
+        t.prob += base;
+        into.tiles.push_back(t);
+    }
+    from.probs.clear();
+    from.tiles.clear();
+}
+
 jorge_status upload_stage(jorge_ctx* c, GemmStage& st) {
     order_for_xcds(st);
     jorge_status s = upload(c, st.probs, &st.dprobs);
@@ -421,14 +434,14 @@ jorge_status upload_stage(jorge_ctx* c, GemmStage& st) {
 
 void free_ctx(jorge_ctx* c) {
     if (!c) return;
-    for (GemmStage* st : {&c->gram_l, &c->gram_r, &c->pow2, &c->pow4, &c->xform, &c->poly, &c->update,
-                          &c->pre_l, &c->pre_r}) {
+    for (GemmStage* st : {&c->gram, &c->pow2, &c->pow4, &c->xform, &c->poly, &c->update, &c->pre_l,
+                          &c->pre_r}) {
         if (st->dprobs) (void)hipFree(st->dprobs);
         if (st->dtiles) (void)hipFree(st->dtiles);
     }
     if (c->dlayers) (void)hipFree(c->dlayers);
     if (c->dfactors) (void)hipFree(c->dfactors);
-    if (c->drow) (void)hipFree(c->drow);
+    if (c->dstage) (void)hipFree(c->dstage);
     if (c->dflat) (void)hipFree(c->dflat);
     if (c->dsym) (void)hipFree(c->dsym);
     if (c->arena) (void)hipFree(c->arena);
@@ -442,10 +455,8 @@ void free_ctx(jorge_ctx* c) {
 
 jorge_status run_update(jorge_ctx* c, double beta2) {
     jorge_status s;
-    if ((s = launch_gemm<true, true, EPI_SYM>(c, c->gram_l, ST_GRAM_L, 0.f)) != JORGE_OK) return s;
-    if ((s = launch_gemm<false, false, EPI_SYM>(c, c->gram_r, ST_GRAM_R, 0.f)) != JORGE_OK) return s;
-    if (c->hp.symmetrize) {
-        if ((s = launch_gemm<true, true, EPI_SYM>(c, c->pow2, ST_POW2, 0.f)) != JORGE_OK) return s;
+    if ((s = launch_gemm<true, true, EPI_SYM>(c, c->gram, ST_GRAM, 0.f)) != JORGE_OK) return s;
+    if (c->hp.symmetrize) {  // A^2 ran inside the gram launch
         if ((s = launch_gemm<true, true, EPI_SYM>(c, c->pow4, ST_POW4, 0.f)) != JORGE_OK) return s;
     } else {
         if ((s = launch_gemm<true, false, EPI_STORE>(c, c->pow2, ST_POW2, 0.f)) != JORGE_OK) return s;
@@ -557,11 +568,12 @@ jorge_status jorge_create(const jorge_shape* shapes, int32_t num_layers, const j
     }
     if ((st = upload(c, ld, &c->dlayers)) != JORGE_OK) return bail(st);
     if ((st = upload(c, fd, &c->dfactors)) != JORGE_OK) return bail(st);
-    if ((st = upload(c, c->row_chunks, &c->drow)) != JORGE_OK) return bail(st);
+    if ((st = upload(c, c->stage_tiles, &c->dstage)) != JORGE_OK) return bail(st);
     if ((st = upload(c, c->flat_chunks, &c->dflat)) != JORGE_OK) return bail(st);
     if ((st = upload(c, c->sym_tiles, &c->dsym)) != JORGE_OK) return bail(st);
-    for (GemmStage* s : {&c->gram_l, &c->gram_r, &c->pow2, &c->pow4, &c->xform, &c->poly, &c->update,
-                         &c->pre_l, &c->pre_r})
+    if (c->hp.symmetrize) merge_stage(c->gram, c->pow2);
+    for (GemmStage* s : {&c->gram, &c->pow2, &c->pow4, &c->xform, &c->poly, &c->update, &c->pre_l,
+                         &c->pre_r})
         if ((st = upload_stage(c, *s)) != JORGE_OK) return bail(st);
     hipLaunchKernelGGL(init_factors_kernel, dim3((unsigned)c->factors.size()), dim3(256), 0, c->stream,
                        c->dfactors, (float)std::pow(h.eps, -0.25));
@@ -586,16 +598,16 @@ jorge_status jorge_step(jorge_ctx* c, float* const* params, const float* const* 
     for (int b = 0; b < nbatch; ++b) {
         PtrBatch pb{};
         for (int i = b * kPtrBatch; i < std::min(nl, (b + 1) * kPtrBatch); ++i) pb.p[i - b * kPtrBatch] = grads[i];
-        const int c0 = c->row_batch_start[b], c1 = c->row_batch_start[b + 1];
+        const int c0 = c->stage_batch_start[b], c1 = c->stage_batch_start[b + 1];
         TimedLaunch tl(c, ST_STAGEIN);
         hipLaunchKernelGGL(stagein_kernel, dim3(c1 - c0), dim3(kEwThreads), 0, c->stream, c->dlayers,
-                           c->drow + c0, b * kPtrBatch, pb, (float)beta1);
+                           c->dstage + c0, b * kPtrBatch, pb, (float)beta1);
         tl.finish();
         JORGE_HIP(c, hipGetLastError());
     }
     jorge_status s;
     if (update && (s = run_update(c, beta2)) != JORGE_OK) return s;
-    if ((s = launch_gemm<true, false, EPI_STORE>(c, c->pre_l, ST_PRECOND_L, 0.f)) != JORGE_OK) return s;
+    if ((s = launch_gemm<true, true, EPI_STORE>(c, c->pre_l, ST_PRECOND_L, 0.f)) != JORGE_OK) return s;
     s = c->hp.symmetrize ? launch_gemm<true, true, EPI_MOMENTUM>(c, c->pre_r, ST_PRECOND_R, (float)beta1)
                          : launch_gemm<true, false, EPI_MOMENTUM>(c, c->pre_r, ST_PRECOND_R, (float)beta1);
     if (s != JORGE_OK) return s;

@@ -168,7 +168,11 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_grouped(const GemmProble
             load_slab<AK>(p.A, p.lda, row0, p.M, (kt + 1) * kSlab, ra);
             load_slab<BK>(p.B, p.ldb, col0, p.N, (kt + 1) * kSlab, rb);
         }
+        // Raised issue priority while this wave runs its MFMAs: the two waves
+        // sharing a SIMD then alternate between MFMA and memory phases.
+        __builtin_amdgcn_s_setprio(1);
         mma_slab<AK, BK>(lds[cur][0], lds[cur][1], wy, wx, lane, acc);
+        __builtin_amdgcn_s_setprio(0);
         if (more) {
             store_slab<AK>(lds[cur ^ 1][0], ra);
             store_slab<BK>(lds[cur ^ 1][1], rb);

@@ -30,49 +30,41 @@ __global__ void init_factors_kernel(const FactorDev* __restrict__ f, float l0) {
     for (int i = threadIdx.x; i < F.d; i += blockDim.x) F.A[(size_t)i * F.dp + i] = l0;
 }
 
-// Gradient stage-in: copies G (dense m x n, caller's buffer) into the padded
-// operand Gp, updates m_SGD = beta1 m_SGD + G (Algorithm 3) and writes the
-// chunk's sum of m_SGD^2.
+// Gradient stage-in over 64 x 64 blocks: copies G (dense m x n, caller's
+// buffer) into the padded operand Gp and its transpose Gpt, updates
+// m_SGD = beta1 m_SGD + G (Algorithm 3) and writes the block's sum of m_SGD^2.
+// Both the row-major reads and the transposed writes are coalesced; the
+// transpose goes through LDS.
 __global__ __launch_bounds__(kEwThreads) void stagein_kernel(const LayerDev* __restrict__ layers,
-                                                             const RowChunk* __restrict__ chunks,
+                                                             const StageTile* __restrict__ tiles,
                                                              int layer_base, PtrBatch grads,
                                                              float beta1) {
+    __shared__ float blk[64][65];
     __shared__ double red[4];
-    const RowChunk ck = chunks[blockIdx.x];
-    const LayerDev& L = layers[ck.layer];
-    const float* __restrict__ G = grads.p[ck.layer - layer_base];
-    const int n = L.n;
+    const StageTile st = tiles[blockIdx.x];
+    const LayerDev& L = layers[st.layer];
+    const float* __restrict__ G = grads.p[st.layer - layer_base];
+    const int m = L.m, n = L.n;
     double part = 0.0;
-    if ((n & 3) == 0 && (reinterpret_cast<uintptr_t>(G) & 15) == 0) {
-        const int n4 = n >> 2;
-        const int total = ck.nrows * n4;
-        for (int e = threadIdx.x; e < total; e += kEwThreads) {
-            const int r = ck.row0 + e / n4, c = (e % n4) * 4;
-            const f32x4 g = *reinterpret_cast<const f32x4*>(G + (size_t)r * n + c);
-            *reinterpret_cast<f32x4*>(L.Gp + (size_t)r * L.np + c) = g;
-            f32x4* ms = reinterpret_cast<f32x4*>(L.msgd + (size_t)r * n + c);
-            f32x4 v = *ms;
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                v[q] = beta1 * v[q] + g[q];
-                part += (double)v[q] * (double)v[q];
-            }
-            *ms = v;
-        }
-    } else {
-        const int total = ck.nrows * n;
-        for (int e = threadIdx.x; e < total; e += kEwThreads) {
-            const int r = ck.row0 + e / n, c = e % n;
-            const float g = G[(size_t)r * n + c];
-            L.Gp[(size_t)r * L.np + c] = g;
-            float* ms = L.msgd + (size_t)r * n + c;
+    for (int e = threadIdx.x; e < 64 * 64; e += kEwThreads) {
+        const int r = e >> 6, c = e & 63, gr = st.r0 + r, gc = st.c0 + c;
+        if (gr < m && gc < n) {
+            const float g = G[(size_t)gr * n + gc];
+            L.Gp[(size_t)gr * L.np + gc] = g;
+            float* ms = L.msgd + (size_t)gr * n + gc;
             const float v = beta1 * *ms + g;
             *ms = v;
             part += (double)v * (double)v;
+            blk[r][c] = g;
         }
     }
+    __syncthreads();
+    for (int e = threadIdx.x; e < 64 * 64; e += kEwThreads) {
+        const int c = e >> 6, r = e & 63, gr = st.r0 + r, gc = st.c0 + c;
+        if (gr < m && gc < n) L.Gpt[(size_t)gc * L.mp + gr] = blk[r][c];
+    }
     const double total = block_sum_256(part, red);
-    if (threadIdx.x == 0) L.part_sgd[ck.slot] = total;
+    if (threadIdx.x == 0) L.part_sgd[st.slot] = total;
 }
 
 // nu = ||X||_F from the per-tile partial sums, then (c, s) of the beta mode

@@ -77,21 +77,22 @@ struct FactorDev {
 // Device view of a layer.
 struct LayerDev {
     float* Gp;             // padded copy of G, mp x np, ld = np, zero padding
+    float* Gpt;            // its transpose, np x mp, ld = mp
     float* T;              // L_hat G, mp x np
     float* mom;            // m_t, dense m x n
     float* msgd;           // m_SGD, dense m x n
     double* part_m;        // per-tile sums of m_ij^2
-    double* part_sgd;      // per-chunk sums of m_SGD,ij^2
+    double* part_sgd;      // per-block sums of m_SGD,ij^2
     LayerScalars* ls;
     int m, n, mp, np;
     int n_part_m, n_part_sgd;
 };
 
-// A block of rows of one layer for the gradient stage-in kernel.
-struct RowChunk {
+// A 64 x 64 block of one layer's gradient for the stage-in kernel.
+struct StageTile {
     int layer;
-    int row0;
-    int nrows;
+    int r0;
+    int c0;
     int slot;
 };
 

@@ -290,8 +290,13 @@ def test_stage_timing_reports_every_update_stage():
     opt.set_timing(True)
     opt.step(p, g, 0.1)
     tm = opt.read_timing()
-    for name in ("stage_in", "gram_L", "gram_R", "pow2", "pow4", "xform", "factor_finalize", "poly",
-                 "update", "symmetrize", "precond_L", "precond_R", "layer_finalize", "weight"):
+    for name in ("stage_in", "gram", "pow4", "xform", "factor_finalize", "poly", "update", "symmetrize",
+                 "precond_L", "precond_R", "layer_finalize", "weight"):
         assert tm[name][1] == 1 and tm[name][0] > 0, name
+    assert tm["pow2"] == (0.0, 0)          # A^2 shares the gram launch
+    lit = Jorge([(256, 512)], symmetrize=False)
+    lit.set_timing(True)
+    lit.step([torch.zeros((256, 512), device="cuda")], g, 0.1)
+    assert lit.read_timing()["pow2"][1] == 1
     opt.reset_timing()
     assert all(v == (0.0, 0) for v in opt.read_timing().values())
