@@ -81,6 +81,11 @@ typedef struct jorge_hparams {
     int32_t graft;            /* 1: SGD grafting (Algorithm 3); 0: theta -= lr * m_t. Default 1. */
     int32_t symmetrize;       /* 1: each updated factor is replaced by (Z + Z^T)/2, Z being
                                  Algorithm 2's product; 0: Z itself. Default 1. */
+    int32_t small_factor_max; /* factors whose padded size (rounded up to 32) is at most this
+                                 are updated whole by one workgroup each, on a second stream,
+                                 concurrently with the grouped launches of the larger factors;
+                                 0 sends every factor through the grouped launches. The result
+                                 is bitwise the same either way. In [0, 4096]. Default 0. */
 } jorge_hparams;
 
 /* Largest rows or cols of a layer the library accepts. */

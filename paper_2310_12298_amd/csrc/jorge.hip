@@ -20,6 +20,10 @@
 //   lfinal     ||m||, ||m_SGD||, grafted step g
 //   weight     theta <- theta (1 - lr wd) - g m
 // Non-update steps run stage-in, precond, lfinal and weight only.
+//
+// Factors no larger than hp.small_factor_max skip the grouped launches: one
+// workgroup per factor runs its whole update (chain_kernel) on a second
+// stream, forked after stage-in and joined before preconditioning.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -43,11 +47,11 @@ namespace {
 // "gram" launch and "pow2" has none; the literal mode launches pow2 apart.
 enum Stage : int {
     ST_STAGEIN = 0, ST_GRAM, ST_POW2, ST_POW4, ST_XFORM, ST_FFINAL, ST_POLY, ST_UPDATE, ST_SYMM,
-    ST_PRECOND_L, ST_PRECOND_R, ST_LFINAL, ST_WEIGHT, ST_COUNT
+    ST_CHAIN, ST_PRECOND_L, ST_PRECOND_R, ST_LFINAL, ST_WEIGHT, ST_COUNT
 };
 const char* const kStageNames[ST_COUNT] = {
     "stage_in", "gram", "pow2", "pow4", "xform", "factor_finalize", "poly", "update", "symmetrize",
-    "precond_L", "precond_R", "layer_finalize", "weight"};
+    "small_chain", "precond_L", "precond_R", "layer_finalize", "weight"};
 
 constexpr size_t kAlign = 256;
 constexpr int kFlatChunkElems = 16384;
@@ -72,6 +76,7 @@ struct LayerHost {
 
 struct FactorHost {
     int layer, side, d, dp;
+    bool small = false;  // updated by chain_kernel rather than the grouped launches
     size_t off_A, off_W0, off_W1, off_W2, off_part, off_sc;
     int nparts = 0;
 };
@@ -98,6 +103,11 @@ struct jorge_ctx {
     StageTile* dstage = nullptr;
     FlatChunk* dflat = nullptr;
     SymTile* dsym = nullptr;
+    int* dbig = nullptr;     // indices of the factors in the grouped launches
+    int* dsmall = nullptr;   // indices of the factors updated by chain_kernel, costliest first
+    std::vector<int> big, small;
+    hipStream_t side = nullptr;                   // stream of chain_kernel
+    hipEvent_t ev_fork = nullptr, ev_join = nullptr;
     std::vector<StageTile> stage_tiles;
     std::vector<FlatChunk> flat_chunks;
     std::vector<int> stage_batch_start, flat_batch_start;  // first block of each layer batch
@@ -145,16 +155,18 @@ hipEvent_t take_event(jorge_ctx* c) {
 struct TimedLaunch {
     jorge_ctx* c;
     int stage;
+    hipStream_t stream;
     hipEvent_t start = nullptr, stop = nullptr;
-    TimedLaunch(jorge_ctx* ctx, int st) : c(ctx), stage(st) {
+    TimedLaunch(jorge_ctx* ctx, int st) : TimedLaunch(ctx, st, ctx->stream) {}
+    TimedLaunch(jorge_ctx* ctx, int st, hipStream_t s) : c(ctx), stage(st), stream(s) {
         if (!c->timing) return;
         start = take_event(c);
         stop = take_event(c);
-        if (start) (void)hipEventRecord(start, c->stream);
+        if (start) (void)hipEventRecord(start, stream);
     }
     void finish() {
         if (!c->timing || !start || !stop) return;
-        (void)hipEventRecord(stop, c->stream);
+        (void)hipEventRecord(stop, stream);
         c->pending.push_back({stage, start, stop});
     }
 };
@@ -244,6 +256,7 @@ jorge_status validate_hparams(const jorge_hparams* hp) {
         return JORGE_ERR_INVALID_ARGUMENT;
     if ((hp->graft != 0 && hp->graft != 1) || (hp->symmetrize != 0 && hp->symmetrize != 1))
         return JORGE_ERR_INVALID_ARGUMENT;
+    if (hp->small_factor_max < 0 || hp->small_factor_max > 4096) return JORGE_ERR_INVALID_ARGUMENT;
     return JORGE_OK;
 }
 
@@ -270,6 +283,7 @@ size_t plan(jorge_ctx* c) {
             F.nparts = tile_count(F.dp, F.dp);
             F.off_part = take((size_t)F.nparts * sizeof(double));
             F.off_sc = take(sizeof(FactorScalars));
+            F.small = F.dp <= c->hp.small_factor_max;
             (side == 0 ? L.fL : L.fR) = (int)c->factors.size();
             c->factors.push_back(F);
         }
@@ -306,6 +320,9 @@ void build_tables(jorge_ctx* c, std::vector<LayerDev>& ld, std::vector<FactorDev
         d.d = F.d;
         d.dp = F.dp;
         d.nparts = F.nparts;
+        const auto& L = c->layers[F.layer];
+        d.gop = at<float>(c, F.side == 0 ? L.off_Gp : L.off_Gpt);
+        d.gk = F.side == 0 ? L.np : L.mp;
         fd.push_back(d);
     }
     for (int li = 0; li < nl; ++li) {
@@ -348,6 +365,8 @@ void build_tables(jorge_ctx* c, std::vector<LayerDev>& ld, std::vector<FactorDev
                      [&](int a, int b) { return c->factors[a].dp > c->factors[b].dp; });
     for (int fi : order) {
         const auto& F = c->factors[fi];
+        if (F.small) continue;
+        c->big.push_back(fi);
         const FactorDev& d = fd[fi];
         const auto& L = c->layers[F.layer];
         const LayerDev& l = ld[F.layer];
@@ -377,6 +396,16 @@ void build_tables(jorge_ctx* c, std::vector<LayerDev>& ld, std::vector<FactorDev
         for (int ti = 0; ti * 64 < F.dp; ++ti)
             for (int tj = ti; tj * 64 < F.dp; ++tj) c->sym_tiles.push_back({fi, ti, tj, 0});
     }
+    // Small factors, costliest first (tile-K products of the Gram and the chain).
+    std::vector<std::pair<int64_t, int>> sc;
+    for (size_t fi = 0; fi < c->factors.size(); ++fi) {
+        const auto& F = c->factors[fi];
+        if (!F.small) continue;
+        const int64_t nt = (F.dp + kTile - 1) / kTile, sym = nt * (nt + 1) / 2;
+        sc.push_back({sym * fd[fi].gk + (2 * sym + 3 * nt * nt) * F.dp, (int)fi});
+    }
+    std::stable_sort(sc.begin(), sc.end(), [](const auto& a, const auto& b) { return a.first > b.first; });
+    for (const auto& e : sc) c->small.push_back(e.second);
     // Preconditioning, largest layers first.
     std::vector<int> lorder(nl);
     for (int i = 0; i < nl; ++i) lorder[i] = i;
@@ -444,6 +473,11 @@ void free_ctx(jorge_ctx* c) {
     if (c->dstage) (void)hipFree(c->dstage);
     if (c->dflat) (void)hipFree(c->dflat);
     if (c->dsym) (void)hipFree(c->dsym);
+    if (c->dbig) (void)hipFree(c->dbig);
+    if (c->dsmall) (void)hipFree(c->dsmall);
+    if (c->ev_fork) (void)hipEventDestroy(c->ev_fork);
+    if (c->ev_join) (void)hipEventDestroy(c->ev_join);
+    if (c->side) (void)hipStreamDestroy(c->side);
     if (c->arena) (void)hipFree(c->arena);
     for (auto& l : c->pending) {
         (void)hipEventDestroy(l.start);
@@ -463,22 +497,46 @@ jorge_status run_update(jorge_ctx* c, double beta2) {
         if ((s = launch_gemm<true, false, EPI_STORE>(c, c->pow4, ST_POW4, 0.f)) != JORGE_OK) return s;
     }
     if ((s = launch_gemm<true, true, EPI_NORM>(c, c->xform, ST_XFORM, 0.f)) != JORGE_OK) return s;
-    {
+    if (!c->big.empty()) {
         TimedLaunch tl(c, ST_FFINAL);
-        hipLaunchKernelGGL(factor_finalize_kernel, dim3((unsigned)c->factors.size()), dim3(64), 0,
-                           c->stream, c->dfactors, beta2, (int)c->hp.beta_mode);
+        hipLaunchKernelGGL(factor_finalize_kernel, dim3((unsigned)c->big.size()), dim3(64), 0, c->stream,
+                           c->dfactors, c->dbig, beta2, (int)c->hp.beta_mode);
         tl.finish();
         JORGE_HIP(c, hipGetLastError());
     }
     if ((s = launch_gemm<true, false, EPI_POLY>(c, c->poly, ST_POLY, 0.f)) != JORGE_OK) return s;
     if ((s = launch_gemm<true, false, EPI_SCALE>(c, c->update, ST_UPDATE, 0.f)) != JORGE_OK) return s;
-    {
+    if (!c->sym_tiles.empty()) {
         TimedLaunch tl(c, ST_SYMM);
         hipLaunchKernelGGL(symmetrize_kernel, dim3((unsigned)c->sym_tiles.size()), dim3(kEwThreads), 0,
                            c->stream, c->dfactors, c->dsym, (int)c->hp.symmetrize);
         tl.finish();
         JORGE_HIP(c, hipGetLastError());
     }
+    return JORGE_OK;
+}
+
+// Small factors: fork the side stream after stage-in, one chain_kernel launch.
+jorge_status fork_small(jorge_ctx* c, double beta2) {
+    if (c->small.empty()) return JORGE_OK;
+    JORGE_HIP(c, hipEventRecord(c->ev_fork, c->stream));
+    JORGE_HIP(c, hipStreamWaitEvent(c->side, c->ev_fork, 0));
+    TimedLaunch tl(c, ST_CHAIN, c->side);
+    if (c->hp.symmetrize)
+        hipLaunchKernelGGL(chain_kernel<1>, dim3((unsigned)c->small.size()), dim3(kGemmThreads), 0, c->side,
+                           c->dfactors, c->dsmall, beta2, (int)c->hp.beta_mode);
+    else
+        hipLaunchKernelGGL(chain_kernel<0>, dim3((unsigned)c->small.size()), dim3(kGemmThreads), 0, c->side,
+                           c->dfactors, c->dsmall, beta2, (int)c->hp.beta_mode);
+    tl.finish();
+    JORGE_HIP(c, hipGetLastError());
+    JORGE_HIP(c, hipEventRecord(c->ev_join, c->side));
+    return JORGE_OK;
+}
+
+jorge_status join_small(jorge_ctx* c) {
+    if (c->small.empty()) return JORGE_OK;
+    JORGE_HIP(c, hipStreamWaitEvent(c->stream, c->ev_join, 0));
     return JORGE_OK;
 }
 
@@ -515,6 +573,7 @@ jorge_status jorge_hparams_default(jorge_hparams* hp) {
     hp->beta_mode = JORGE_BETA_CLAMPED;
     hp->graft = 1;
     hp->symmetrize = 1;
+    hp->small_factor_max = 0;
     return JORGE_OK;
 }
 
@@ -571,6 +630,14 @@ jorge_status jorge_create(const jorge_shape* shapes, int32_t num_layers, const j
     if ((st = upload(c, c->stage_tiles, &c->dstage)) != JORGE_OK) return bail(st);
     if ((st = upload(c, c->flat_chunks, &c->dflat)) != JORGE_OK) return bail(st);
     if ((st = upload(c, c->sym_tiles, &c->dsym)) != JORGE_OK) return bail(st);
+    if ((st = upload(c, c->big, &c->dbig)) != JORGE_OK) return bail(st);
+    if ((st = upload(c, c->small, &c->dsmall)) != JORGE_OK) return bail(st);
+    if (!c->small.empty()) {
+        if (hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking) != hipSuccess ||
+            hipEventCreateWithFlags(&c->ev_fork, hipEventDisableTiming) != hipSuccess ||
+            hipEventCreateWithFlags(&c->ev_join, hipEventDisableTiming) != hipSuccess)
+            return bail(JORGE_ERR_HIP);
+    }
     if (c->hp.symmetrize) merge_stage(c->gram, c->pow2);
     for (GemmStage* s : {&c->gram, &c->pow2, &c->pow4, &c->xform, &c->poly, &c->update, &c->pre_l,
                          &c->pre_r})
@@ -606,7 +673,11 @@ jorge_status jorge_step(jorge_ctx* c, float* const* params, const float* const* 
         JORGE_HIP(c, hipGetLastError());
     }
     jorge_status s;
-    if (update && (s = run_update(c, beta2)) != JORGE_OK) return s;
+    if (update) {
+        if ((s = fork_small(c, beta2)) != JORGE_OK) return s;
+        if ((s = run_update(c, beta2)) != JORGE_OK) return s;
+        if ((s = join_small(c)) != JORGE_OK) return s;
+    }
     if ((s = launch_gemm<true, true, EPI_STORE>(c, c->pre_l, ST_PRECOND_L, 0.f)) != JORGE_OK) return s;
     s = c->hp.symmetrize ? launch_gemm<true, true, EPI_MOMENTUM>(c, c->pre_r, ST_PRECOND_R, (float)beta1)
                          : launch_gemm<true, false, EPI_MOMENTUM>(c, c->pre_r, ST_PRECOND_R, (float)beta1);

@@ -130,19 +130,19 @@ __device__ __forceinline__ double block_sum_256(double v, double* red) {
     return (red[0] + red[1]) + (red[2] + red[3]);
 }
 
-template <bool AK, bool BK, int EPI>
-__global__ __launch_bounds__(kGemmThreads, 2) void gemm_grouped(const GemmProblem* __restrict__ probs,
-                                                                const TileDesc* __restrict__ tiles,
-                                                                float beta1) {
-    __shared__ __attribute__((aligned(16))) float lds[2][2][kLdsOperand];
-    __shared__ double red[4];
+// LDS of one workgroup of the GEMM: two stages of the A and B operand slabs.
+struct GemmLds {
+    float op[2][2][kLdsOperand];
+};
 
-    // The tile list is in dispatch order: consecutive workgroups go round-robin
-    // to the 8 XCDs, and the host arranged the list so each XCD's share is
-    // balanced and reuses operand panels in its own L2.
-    const TileDesc td = tiles[blockIdx.x];
-    const GemmProblem p = probs[td.prob];
-    const int row0 = td.tm * kTile, col0 = td.tn * kTile;
+// One 128 x 128 tile (tm, tn) of problem p computed by the whole workgroup,
+// followed by the epilogue EPI. a, b, sf are the polynomial coefficients and
+// the scale of EPI_POLY / EPI_SCALE; beta1 is the momentum of EPI_MOMENTUM.
+// Every thread of the workgroup must call it; it leaves LDS free for reuse.
+template <bool AK, bool BK, int EPI>
+__device__ __forceinline__ void gemm_tile(const GemmProblem& p, int tm, int tn, int slot, float beta1,
+                                          float a, float b, float sf, GemmLds& sm, double* red) {
+    const int row0 = tm * kTile, col0 = tn * kTile;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int wy = wave >> 1, wx = wave & 1;
 
@@ -158,8 +158,8 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_grouped(const GemmProble
     const int nk = p.K / kSlab;
     load_slab<AK>(p.A, p.lda, row0, p.M, 0, ra);
     load_slab<BK>(p.B, p.ldb, col0, p.N, 0, rb);
-    store_slab<AK>(lds[0][0], ra);
-    store_slab<BK>(lds[0][1], rb);
+    store_slab<AK>(sm.op[0][0], ra);
+    store_slab<BK>(sm.op[0][1], rb);
     __syncthreads();
     for (int kt = 0; kt < nk; ++kt) {
         const int cur = kt & 1;
@@ -171,11 +171,11 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_grouped(const GemmProble
         // Raised issue priority while this wave runs its MFMAs: the two waves
         // sharing a SIMD then alternate between MFMA and memory phases.
         __builtin_amdgcn_s_setprio(1);
-        mma_slab<AK, BK>(lds[cur][0], lds[cur][1], wy, wx, lane, acc);
+        mma_slab<AK, BK>(sm.op[cur][0], sm.op[cur][1], wy, wx, lane, acc);
         __builtin_amdgcn_s_setprio(0);
         if (more) {
-            store_slab<AK>(lds[cur ^ 1][0], ra);
-            store_slab<BK>(lds[cur ^ 1][1], rb);
+            store_slab<AK>(sm.op[cur ^ 1][0], ra);
+            store_slab<BK>(sm.op[cur ^ 1][1], rb);
         }
         __syncthreads();
     }
@@ -183,9 +183,6 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_grouped(const GemmProble
     // Epilogue. Accumulator register e of block (i, j) holds
     // C[row0 + wy*64 + i*32 + 8*(e/4) + 4*(lane/32) + e%4][col0 + wx*64 + j*32 + lane%32].
     const int h = lane >> 5;
-    float a = 0.f, b = 0.f, sf = 0.f;
-    if constexpr (EPI == EPI_POLY) { a = p.sc->a; b = p.sc->b; }
-    if constexpr (EPI == EPI_SCALE) sf = p.sc->sf;
     double part = 0.0;
 #pragma unroll
     for (int i = 0; i < 2; ++i)
@@ -196,7 +193,7 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_grouped(const GemmProble
             for (int q = 0; q < 4; ++q) {
                 const int rowb = row0 + wy * 64 + i * 32 + q * 8 + h * 4;
                 if constexpr (EPI == EPI_SYM) {
-                    if (col < p.N && rowb < p.M && td.tm != td.tn) {
+                    if (col < p.N && rowb < p.M && tm != tn) {
                         f32x4 v;
                         v[0] = acc[i][j][q * 4 + 0]; v[1] = acc[i][j][q * 4 + 1];
                         v[2] = acc[i][j][q * 4 + 2]; v[3] = acc[i][j][q * 4 + 3];
@@ -232,8 +229,26 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_grouped(const GemmProble
         }
     if constexpr (EPI == EPI_NORM || EPI == EPI_MOMENTUM) {
         const double total = block_sum_256(part, red);
-        if (threadIdx.x == 0) p.partials[td.slot] = total;
+        if (threadIdx.x == 0) p.partials[slot] = total;
     }
+}
+
+// Grouped launch: one workgroup per tile of the list. The tile list is in
+// dispatch order: consecutive workgroups go round-robin to the 8 XCDs, and the
+// host arranged the list so each XCD's share is balanced and reuses operand
+// panels in its own L2.
+template <bool AK, bool BK, int EPI>
+__global__ __launch_bounds__(kGemmThreads, 2) void gemm_grouped(const GemmProblem* __restrict__ probs,
+                                                                const TileDesc* __restrict__ tiles,
+                                                                float beta1) {
+    __shared__ __attribute__((aligned(16))) GemmLds sm;
+    __shared__ double red[4];
+    const TileDesc td = tiles[blockIdx.x];
+    const GemmProblem p = probs[td.prob];
+    float a = 0.f, b = 0.f, sf = 0.f;
+    if constexpr (EPI == EPI_POLY) { a = p.sc->a; b = p.sc->b; }
+    if constexpr (EPI == EPI_SCALE) sf = p.sc->sf;
+    gemm_tile<AK, BK, EPI>(p, td.tm, td.tn, td.slot, beta1, a, b, sf, sm, red);
 }
 
 }  // namespace jorge

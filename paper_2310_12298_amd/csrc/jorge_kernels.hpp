@@ -67,48 +67,47 @@ __global__ __launch_bounds__(kEwThreads) void stagein_kernel(const LayerDev* __r
     if (threadIdx.x == 0) L.part_sgd[st.slot] = total;
 }
 
-// nu = ||X||_F from the per-tile partial sums, then (c, s) of the beta mode
-// (Algorithm 2; Appendix A.1, Eq. 8-9). One wave per factor.
-__global__ void factor_finalize_kernel(const FactorDev* __restrict__ f, double beta2, int mode) {
-    const FactorDev F = f[blockIdx.x];
-    const double nu = sqrt(wave_sum_array(F.partials, F.nparts));
-    if (threadIdx.x != 0) return;
+// (beta, c, s) of one factor update from nu = ||X||_F (Algorithm 2; Appendix
+// A.1, Eq. 8-9). The dynamic branch forms c = 1/nu and s = (1 + 1/nu)^(1/4)
+// directly, never 1 - beta.
+__device__ __forceinline__ FactorScalars factor_scalars(double nu, double beta2, int mode) {
     bool dyn = false;
     if (mode == 1) dyn = nu > 0.0;                           // DYNAMIC
-    else if (mode == 2) dyn = nu > beta2 / (1.0 - beta2);    // CLAMPED
-    double beta, c, s;
-    if (dyn) {
-        beta = nu / (nu + 1.0);
-        c = 1.0 / nu;
-        s = pow(1.0 + 1.0 / nu, 0.25);
-    } else {
-        beta = beta2;
-        c = (1.0 - beta2) / beta2;
-        s = pow(beta2, -0.25);
-    }
+    else if (mode == 2) dyn = nu > beta2 / (1.0 - beta2);    // CLAMPED: nu/(nu+1) > beta2
     FactorScalars out;
+    if (dyn) {
+        out.beta = nu / (nu + 1.0);
+        out.c = 1.0 / nu;
+        out.s = pow(1.0 + 1.0 / nu, 0.25);
+    } else {
+        out.beta = beta2;
+        out.c = (1.0 - beta2) / beta2;
+        out.s = pow(beta2, -0.25);
+    }
     out.nu = nu;
-    out.beta = beta;
-    out.c = c;
-    out.s = s;
-    out.a = (float)(0.25 * c);
-    out.b = (float)(0.15625 * c * c);
-    out.sf = (float)s;
+    out.a = (float)(0.25 * out.c);
+    out.b = (float)(0.15625 * out.c * out.c);
+    out.sf = (float)out.s;
     out.pad = 0.f;
-    *F.sc = out;
+    return out;
 }
 
-// A_hat <- (Z + Z^T)/2 (or Z when not symmetrizing) for a pair of 64 x 64
-// tiles (ti, tj), (tj, ti). fp32 addition commutes, so the result is bitwise
-// symmetric.
-__global__ __launch_bounds__(kEwThreads) void symmetrize_kernel(const FactorDev* __restrict__ f,
-                                                                const SymTile* __restrict__ tiles,
-                                                                int symmetrize) {
-    __shared__ float za[64][65];
-    __shared__ float zb[64][65];
-    const SymTile st = tiles[blockIdx.x];
-    const FactorDev& F = f[st.factor];
-    const int dp = F.dp, i0 = st.ti * 64, j0 = st.tj * 64;
+// nu = ||X||_F from the per-tile partial sums, then the factor's scalars.
+// One wave per factor of the list.
+__global__ void factor_finalize_kernel(const FactorDev* __restrict__ f, const int* __restrict__ list,
+                                       double beta2, int mode) {
+    const FactorDev F = f[list[blockIdx.x]];
+    const double nu = sqrt(wave_sum_array(F.partials, F.nparts));
+    if (threadIdx.x == 0) *F.sc = factor_scalars(nu, beta2, mode);
+}
+
+// A_hat <- (Z + Z^T)/2 (or Z when not symmetrizing) for the pair of 64 x 64
+// tiles (ti, tj), (tj, ti), Z being in W0. fp32 addition commutes, so the
+// result is bitwise symmetric. za, zb: 64 x 65 floats of LDS each. All threads
+// of the workgroup call it; it ends with a barrier so the LDS can be reused.
+__device__ __forceinline__ void symmetrize_pair(const FactorDev& F, int ti, int tj, int symmetrize,
+                                                float (*za)[65], float (*zb)[65]) {
+    const int dp = F.dp, i0 = ti * 64, j0 = tj * 64;
     const int tid = threadIdx.x;
     // 64 rows x 16 float4 per tile, 4 per thread.
 #pragma unroll
@@ -134,7 +133,7 @@ __global__ __launch_bounds__(kEwThreads) void symmetrize_kernel(const FactorDev*
                 v[e] = symmetrize ? 0.5f * (za[r][c + e] + zb[c + e][r]) : za[r][c + e];
             *reinterpret_cast<f32x4*>(F.A + (size_t)(i0 + r) * dp + j0 + c) = v;
         }
-        if (st.ti != st.tj && j0 + r < dp && i0 + c < dp) {
+        if (ti != tj && j0 + r < dp && i0 + c < dp) {
             f32x4 v;
 #pragma unroll
             for (int e = 0; e < 4; ++e)
@@ -142,6 +141,104 @@ __global__ __launch_bounds__(kEwThreads) void symmetrize_kernel(const FactorDev*
             *reinterpret_cast<f32x4*>(F.A + (size_t)(j0 + r) * dp + i0 + c) = v;
         }
     }
+    __syncthreads();
+}
+
+__global__ __launch_bounds__(kEwThreads) void symmetrize_kernel(const FactorDev* __restrict__ f,
+                                                                const SymTile* __restrict__ tiles,
+                                                                int symmetrize) {
+    __shared__ float za[64][65];
+    __shared__ float zb[64][65];
+    const SymTile st = tiles[blockIdx.x];
+    symmetrize_pair(f[st.factor], st.ti, st.tj, symmetrize, za, zb);
+}
+
+// The whole update of one small factor by one workgroup (Algorithm 2 with
+// Appendix A.1): Gram statistic, A^2, A^4, X = A^4 M with ||X||_F, (c, s),
+// P = I - (c/4) X + (5c^2/32) X X, Z = s A P, and A <- (Z + Z^T)/2. The stages
+// are separated by workgroup barriers instead of kernel launches. Each product
+// uses the grouped launches' tile routine, tile decomposition, K order and
+// partial-sum slots, so a factor gets bitwise the same result on either path.
+// Intermediates live in the factor's workspace, which stays in L2.
+template <int SYMM>
+__global__ __launch_bounds__(kGemmThreads, 2) void chain_kernel(const FactorDev* __restrict__ f,
+                                                                const int* __restrict__ list,
+                                                                double beta2, int mode) {
+    __shared__ __attribute__((aligned(16))) GemmLds sm;
+    __shared__ double red[4];
+    __shared__ float scal[3];
+    const FactorDev F = f[list[blockIdx.x]];
+    const int dp = F.dp, nt = (dp + kTile - 1) / kTile;
+    GemmProblem g{};
+    g.M = g.N = g.K = dp;
+    g.lda = g.ldb = g.ldc = g.ldx = dp;
+    g.valid_m = g.valid_n = F.d;
+
+    GemmProblem s = g;                                   // Gram statistic -> W0
+    s.A = s.B = F.gop;
+    s.K = s.lda = s.ldb = F.gk;
+    s.C = F.W0;
+    for (int tm = 0; tm < nt; ++tm)
+        for (int tn = tm; tn < nt; ++tn) gemm_tile<true, true, EPI_SYM>(s, tm, tn, 0, 0.f, 0.f, 0.f, 0.f, sm, red);
+    __syncthreads();
+    GemmProblem p2 = g;                                  // A^2 -> W1
+    p2.A = p2.B = F.A;
+    p2.C = F.W1;
+    GemmProblem p4 = g;                                  // A^4 -> W2
+    p4.A = p4.B = F.W1;
+    p4.C = F.W2;
+    if constexpr (SYMM) {
+        for (int tm = 0; tm < nt; ++tm)
+            for (int tn = tm; tn < nt; ++tn) gemm_tile<true, true, EPI_SYM>(p2, tm, tn, 0, 0.f, 0.f, 0.f, 0.f, sm, red);
+        __syncthreads();
+        for (int tm = 0; tm < nt; ++tm)
+            for (int tn = tm; tn < nt; ++tn) gemm_tile<true, true, EPI_SYM>(p4, tm, tn, 0, 0.f, 0.f, 0.f, 0.f, sm, red);
+    } else {
+        for (int tn = 0; tn < nt; ++tn)
+            for (int tm = 0; tm < nt; ++tm) gemm_tile<true, false, EPI_STORE>(p2, tm, tn, 0, 0.f, 0.f, 0.f, 0.f, sm, red);
+        __syncthreads();
+        for (int tn = 0; tn < nt; ++tn)
+            for (int tm = 0; tm < nt; ++tm) gemm_tile<true, false, EPI_STORE>(p4, tm, tn, 0, 0.f, 0.f, 0.f, 0.f, sm, red);
+    }
+    __syncthreads();
+    GemmProblem px = g;                                  // X = A^4 M -> W1, ||X||^2 partials
+    px.A = F.W2;
+    px.B = F.W0;
+    px.C = F.W1;
+    px.partials = F.partials;
+    // Slots follow the grouped tile order (column by column within bands of 8 tile rows).
+    for (int tn = 0, slot = 0; tn < nt; ++tn)
+        for (int tm = 0; tm < nt; ++tm, ++slot)
+            gemm_tile<true, true, EPI_NORM>(px, tm, tn, slot, 0.f, 0.f, 0.f, 0.f, sm, red);
+    __syncthreads();
+    if (threadIdx.x < 64) {
+        const double nu = sqrt(wave_sum_array(F.partials, F.nparts));
+        if (threadIdx.x == 0) {
+            const FactorScalars fs = factor_scalars(nu, beta2, mode);
+            *F.sc = fs;
+            scal[0] = fs.a;
+            scal[1] = fs.b;
+            scal[2] = fs.sf;
+        }
+    }
+    __syncthreads();
+    GemmProblem pp = g;                                  // P = I - a X + b X X -> W2
+    pp.A = pp.B = pp.X = F.W1;
+    pp.C = F.W2;
+    for (int tn = 0; tn < nt; ++tn)
+        for (int tm = 0; tm < nt; ++tm) gemm_tile<true, false, EPI_POLY>(pp, tm, tn, 0, 0.f, scal[0], scal[1], 0.f, sm, red);
+    __syncthreads();
+    GemmProblem pu = g;                                  // Z = s A P -> W0
+    pu.A = F.A;
+    pu.B = F.W2;
+    pu.C = F.W0;
+    for (int tn = 0; tn < nt; ++tn)
+        for (int tm = 0; tm < nt; ++tm) gemm_tile<true, false, EPI_SCALE>(pu, tm, tn, 0, 0.f, 0.f, 0.f, scal[2], sm, red);
+    __syncthreads();
+    float (*za)[65] = reinterpret_cast<float (*)[65]>(&sm.op[0][0][0]);
+    float (*zb)[65] = za + 64;
+    for (int ti = 0; ti * 64 < dp; ++ti)
+        for (int tj = ti; tj * 64 < dp; ++tj) symmetrize_pair(F, ti, tj, SYMM, za, zb);
 }
 
 // Per-layer norms of m and m_SGD from their partial sums, and the grafted

@@ -69,9 +69,10 @@ struct FactorDev {
     float* W2;             // workspace: A^4, later P
     FactorScalars* sc;
     double* partials;      // per-tile sums of X_ij^2
+    const float* gop;      // Gram operand with K contiguous: Gp (L side) or Gpt (R side)
+    int gk;                // its K (np or mp), also its row stride
     int d, dp;
     int nparts;
-    int pad0;
 };
 
 // Device view of a layer.

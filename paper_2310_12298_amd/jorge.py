@@ -32,7 +32,7 @@ class Shape(ctypes.Structure):
 class HParams(ctypes.Structure):
     _fields_ = [("eps", ctypes.c_double), ("precond_interval", ctypes.c_int32),
                 ("beta_mode", ctypes.c_int32), ("graft", ctypes.c_int32),
-                ("symmetrize", ctypes.c_int32)]
+                ("symmetrize", ctypes.c_int32), ("small_factor_max", ctypes.c_int32)]
 
 
 _LIB = None
@@ -106,7 +106,7 @@ class Jorge:
     """
 
     def __init__(self, shapes, eps=1e-6, precond_interval=1, beta_mode="clamped", graft=True,
-                 symmetrize=True, stream=None):
+                 symmetrize=True, small_factor_max=None, stream=None):
         self.lib = load_library()
         self.shapes = [(int(m), int(n)) for m, n in shapes]
         hp = HParams()
@@ -116,6 +116,8 @@ class Jorge:
         hp.beta_mode = BETA_MODES[beta_mode] if isinstance(beta_mode, str) else int(beta_mode)
         hp.graft = int(bool(graft))
         hp.symmetrize = int(bool(symmetrize))
+        if small_factor_max is not None:
+            hp.small_factor_max = int(small_factor_max)
         arr = (Shape * len(self.shapes))(*[Shape(m, n) for m, n in self.shapes])
         ctx = _P()
         s = _current_stream() if stream is None else int(stream)

@@ -45,7 +45,8 @@ def test_every_declared_symbol_is_exported(lib):
 def test_hparams_default(lib):
     hp = J.HParams()
     assert lib.jorge_hparams_default(ctypes.byref(hp)) == 0
-    assert (hp.eps, hp.precond_interval, hp.beta_mode, hp.graft, hp.symmetrize) == (1e-6, 1, 2, 1, 1)
+    assert (hp.eps, hp.precond_interval, hp.beta_mode, hp.graft, hp.symmetrize,
+            hp.small_factor_max) == (1e-6, 1, 2, 1, 1, 0)
     assert lib.jorge_hparams_default(None) == ERR_INVALID
 
 
@@ -70,7 +71,8 @@ def test_create_rejects_oversize(lib):
 @pytest.mark.parametrize("field,value", [("eps", 0.0), ("eps", -1.0), ("eps", float("inf")),
                                          ("eps", float("nan")), ("precond_interval", 0),
                                          ("beta_mode", 3), ("beta_mode", -1), ("graft", 2),
-                                         ("symmetrize", -1)])
+                                         ("symmetrize", -1), ("small_factor_max", -1),
+                                         ("small_factor_max", 4097)])
 def test_create_rejects_bad_hparams(lib, field, value):
     hp = J.HParams()
     lib.jorge_hparams_default(ctypes.byref(hp))

@@ -300,3 +300,23 @@ def test_stage_timing_reports_every_update_stage():
     assert lit.read_timing()["pow2"][1] == 1
     opt.reset_timing()
     assert all(v == (0.0, 0) for v in opt.read_timing().values())
+
+
+@pytest.mark.parametrize("symmetrize", [True, False])
+def test_small_factor_chain_matches_grouped_bitwise(symmetrize):
+    """One workgroup per small factor (second stream) gives the grouped launches' bits."""
+    shapes = [(64, 576), (32, 256), (64, 147), (200, 100), (256, 512)]
+    say("chain vs grouped, symmetrize", symmetrize)
+    chain = Jorge(shapes, symmetrize=symmetrize, small_factor_max=256)
+    grouped = Jorge(shapes, symmetrize=symmetrize, small_factor_max=0)
+    pa = [to_dev(initial_params(0, l, s)) for l, s in enumerate(shapes)]
+    pb = [p.clone() for p in pa]
+    for t in range(1, 4):
+        G = [to_dev(gradient(0, l, t, s, 1e-2)) for l, s in enumerate(shapes)]
+        chain.step(pa, G, **HP)
+        grouped.step(pb, G, **HP)
+    for l in range(len(shapes)):
+        for k in KINDS:
+            assert torch.equal(chain.get_state(l, k), grouped.get_state(l, k)), (l, k)
+        assert torch.equal(pa[l], pb[l])
+        assert chain.read_diag(l) == grouped.read_diag(l)
