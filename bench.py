@@ -28,33 +28,12 @@ WORKLOAD_NAMES = {
 }
 
 
-def pad32(d):
-    return (d + 31) // 32 * 32
+def falg_paper(m, n):
+    """Flops of one factor-updating step of an m x n layer in the paper's explicit order.
 
-
-def stage_flops(shapes, small_max):
-    """Algorithmic flops of one update step per timed stage (symmetric products count half).
-
-    Factors whose padded size is at most small_max run their whole chain,
-    Gram statistic included, inside the small_chain stage.
+    Per factor of size d with statistic rank k: A^2 and A^4 (symmetric, d^3 each),
+    X, X X and A P (2 d^3 each), the Gram product (d^2 k); plus L_hat G R_hat.
     """
-    f = {k: 0 for k in ("gram", "pow2", "pow4", "xform", "poly", "update", "small_chain", "precond_L",
-                        "precond_R")}
-    for m, n in shapes:
-        for d, k in ((m, n), (n, m)):
-            chain = {"gram": d * d * k, "pow2": d ** 3, "pow4": d ** 3, "xform": 2 * d ** 3,
-                     "poly": 2 * d ** 3, "update": 2 * d ** 3}
-            if pad32(d) <= small_max:
-                f["small_chain"] += sum(chain.values())
-            else:
-                for key, v in chain.items():
-                    f[key] += v
-        f["precond_L"] += 2 * m * m * n
-        f["precond_R"] += 2 * m * n * n
-    return f
-
-
-def falg(m, n):
     return 8 * m ** 3 + 8 * n ** 3 + 3 * m * m * n + 3 * m * n * n
 
 
@@ -63,6 +42,9 @@ def stage_bytes(shapes):
     mn = sum(m * n for m, n in shapes)
     return {"weight": 12 * mn,       # read theta and m, write theta
             "stage_in": 16 * mn}     # read G, write the padded copy, read and write m_SGD
+
+
+GEMM_STAGES = ("gram", "pow4", "xform", "chain4", "chain5", "poly", "update", "precond_L", "precond_R")
 
 
 def cpu_baseline(shapes, sigma, seed, budget_s):
@@ -77,7 +59,7 @@ def cpu_baseline(shapes, sigma, seed, budget_s):
     from oracle import JorgeOracle
     from paper_2310_12298_amd.workloads import gradient, initial_params
 
-    total_f = sum(falg(m, n) for m, n in shapes)
+    total_f = sum(falg_paper(m, n) for m, n in shapes)
     done_f, spent, used = 0, 0.0, 0
     for l, s in enumerate(shapes):
         G = [gradient(seed, l, 1, s, sigma)]
@@ -86,7 +68,7 @@ def cpu_baseline(shapes, sigma, seed, budget_s):
         t0 = time.perf_counter()
         orc.step(P, G, 0.1, 0.9, 0.9, 5e-5)
         spent += time.perf_counter() - t0
-        done_f += falg(*s)
+        done_f += falg_paper(*s)
         used += 1
         if spent >= budget_s:
             break
@@ -104,8 +86,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="resnet50", choices=sorted(WORKLOAD_NAMES))
     ap.add_argument("--interval", type=int, default=1, help="preconditioner update interval k")
-    ap.add_argument("--small-max", type=int, default=0,
-                    help="factors of padded size <= this run as one workgroup chain each (0 = none)")
+    ap.add_argument("--form", default="auto", choices=("auto", "explicit", "factored"),
+                    help="evaluation order of the factor updates")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time (0 = skip)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -126,7 +108,7 @@ def main():
     shapes, sigma, run_steps = CONFIGS[args.config]
     steps = args.steps if args.steps is not None else run_steps
     hp = DEFAULT_HPARAMS
-    opt = Jorge(shapes, eps=hp["eps"], precond_interval=args.interval, small_factor_max=args.small_max)
+    opt = Jorge(shapes, eps=hp["eps"], precond_interval=args.interval, factor_form=args.form)
     params = [device_initial_params(args.seed, l, s) for l, s in enumerate(shapes)]
     grads = [[device_gradient(args.seed, l, t, s, sigma) for l, s in enumerate(shapes)]
              for t in range(1, args.warmup + steps + 1)]
@@ -165,22 +147,27 @@ def main():
     updates = sum(1 for i in range(args.warmup, args.warmup + steps) if i % args.interval == 0)
     if updates == 0:
         raise SystemExit("no factor update in the timed steps; use more steps or a smaller interval")
-    flops = stage_flops(shapes, args.small_max)
-    if timing["pow2"][1] == 0:          # A^2 shares the gram launch when factors are symmetric
-        flops["gram"] += flops.pop("pow2")
-    per_stage = {k: {"ms_per_launch": (v[0] / v[1]) if v[1] else 0.0, "launches": v[1]}
-                 for k, v in timing.items()}
-    for k, v in per_stage.items():
-        if k in flops and v["launches"]:
-            v["tflops"] = flops[k] / (v["ms_per_launch"] * 1e-3) / 1e12 if v["ms_per_launch"] else 0.0
-    # Dominant kernel: the GEMM-engine stage (grouped launch or small-factor chain) with the most time.
-    dom = max((k for k in flops if timing[k][1]), key=lambda k: timing[k][0])
-    dom_ms = timing[dom][0] / timing[dom][1]
-    achieved = flops[dom] / (dom_ms * 1e-3) / 1e12
-    f_step = sum(falg(m, n) for m, n in shapes) * updates / steps
+    # Algorithmic flops of each stage in one factor-updating step, from the library's launch tables.
+    flops = opt.stage_flops()
+    ran = {k: (updates if k not in ("precond_L", "precond_R") else steps) for k in GEMM_STAGES}
+    per_stage = {}
+    for k, (ms, n) in timing.items():
+        e = {"ms_per_launch": ms / n if n else 0.0, "launches": n}
+        if k in GEMM_STAGES and ms > 0:
+            e["tflops"] = flops[k] * ran[k] / (ms * 1e-3) / 1e12
+        per_stage[k] = e
+    # Dominant kernel: the grouped NT GEMM; every GEMM stage of the step is a launch of it.
+    g_flops = sum(flops[k] * ran[k] for k in GEMM_STAGES)
+    g_ms = sum(timing[k][0] for k in GEMM_STAGES)
+    g_launches = sum(timing[k][1] for k in GEMM_STAGES)
+    achieved = g_flops / (g_ms * 1e-3) / 1e12
+    f_paper = sum(falg_paper(m, n) for m, n in shapes) * updates / steps
     hbm = stage_bytes(shapes)
     w_ms = timing["weight"][0] / max(1, timing["weight"][1])
-    kernel = "chain_kernel (small_chain stage)" if dom == "small_chain" else f"gemm_grouped ({dom} stage)"
+    forms = {"explicit": 0, "factored": 0}
+    for l in range(len(shapes)):
+        for side in (0, 1):
+            forms[opt.factor_form(l, side)] += 1
     out = {
         "metric": METRIC,
         "value": steps / (total_ms * 1e-3),
@@ -196,12 +183,16 @@ def main():
         "data": "synthetic",
         "config": {"workload": WORKLOAD_NAMES[args.config], "name": args.config, "layers": len(shapes),
                    "params": sum(m * n for m, n in shapes), "precond_interval": args.interval,
-                   "factor_updates": updates, "small_factor_max": args.small_max, "seed": args.seed},
-        "roofline": {"bound": "mfma", "kernel": kernel, "achieved": achieved,
-                     "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s", "frac": achieved / PEAK_FP32_MFMA_TFLOPS,
-                     "traffic": None},
-        # whole step: algorithmic flops / (step time x fp32 MFMA peak)
-        "mfma_util_pct": 100.0 * f_step / (total_ms / steps * 1e-3) / (PEAK_FP32_MFMA_TFLOPS * 1e12),
+                   "factor_updates": updates, "factor_form": args.form, "factors": forms, "seed": args.seed},
+        "roofline": {"bound": "mfma", "kernel": "gemm_grouped<true, true> (every GEMM stage of the step)",
+                     "achieved": achieved, "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s",
+                     "frac": achieved / PEAK_FP32_MFMA_TFLOPS, "traffic": None,
+                     "launches": g_launches, "ms_per_launch": g_ms / max(1, g_launches),
+                     "gflop_per_launch": g_flops / max(1, g_launches) / 1e9},
+        # executed algorithmic flops of the whole step / (step time x fp32 MFMA peak)
+        "mfma_util_pct": 100.0 * g_flops / steps / (total_ms / steps * 1e-3) / (PEAK_FP32_MFMA_TFLOPS * 1e12),
+        # the same step's flops counted in the paper's explicit order, per second of step time
+        "paper_order_tflops": f_paper / (total_ms / steps * 1e-3) / 1e12,
         "hbm": {"kernel": "weight", "achieved": hbm["weight"] / (w_ms * 1e-3) / 1e9 if w_ms else 0.0,
                 "peak": PEAK_HBM_GBS, "unit": "GB/s"},
         "stages": per_stage,

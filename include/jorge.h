@@ -48,6 +48,20 @@ typedef int32_t jorge_status;
 #define JORGE_BETA_DYNAMIC 1
 #define JORGE_BETA_CLAMPED 2
 
+/* Evaluation order of a factor update. Both compute the same factor (up to
+ * fp32 rounding); they differ in cost. A (d x d) is updated from the
+ * statistic M = H H^T with H = G (d = rows, k = cols) for L_hat and H = G^T
+ * for R_hat, so M has rank at most k.
+ * EXPLICIT: the paper's order (Algorithm 2): A^2, A^4, X = A^4 M, X X, A P;
+ *           about 8 d^3 + d^2 k flops.
+ * FACTORED: through H: U = A^4 H, X = U H^T, X X = U (H^T U) H^T,
+ *           A P = A - A^5 H (a I - b H^T U) H^T, ||X||_F^2 = <U^T U, H^T H>;
+ *           about 12 d^2 k + 5 d k^2 flops, far less when k << d.
+ * AUTO:     per factor, whichever order has less tile work. */
+#define JORGE_FORM_AUTO     0
+#define JORGE_FORM_EXPLICIT 1
+#define JORGE_FORM_FACTORED 2
+
 /* State tensors of one layer (Algorithm 2 and Algorithm 3). */
 #define JORGE_STATE_L       0 /* L_hat, rows x rows, fp32, symmetric        */
 #define JORGE_STATE_R       1 /* R_hat, cols x cols, fp32, symmetric        */
@@ -81,11 +95,8 @@ typedef struct jorge_hparams {
     int32_t graft;            /* 1: SGD grafting (Algorithm 3); 0: theta -= lr * m_t. Default 1. */
     int32_t symmetrize;       /* 1: each updated factor is replaced by (Z + Z^T)/2, Z being
                                  Algorithm 2's product; 0: Z itself. Default 1. */
-    int32_t small_factor_max; /* factors whose padded size (rounded up to 32) is at most this
-                                 are updated whole by one workgroup each, on a second stream,
-                                 concurrently with the grouped launches of the larger factors;
-                                 0 sends every factor through the grouped launches. The result
-                                 is bitwise the same either way. In [0, 4096]. Default 0. */
+    int32_t factor_form;      /* JORGE_FORM_*: evaluation order of each factor update.
+                                 Default JORGE_FORM_AUTO. */
 } jorge_hparams;
 
 /* Largest rows or cols of a layer the library accepts. */
@@ -108,6 +119,16 @@ jorge_status jorge_hparams_default(jorge_hparams* hp);
  * set to NULL and nothing stays allocated. */
 jorge_status jorge_create(const jorge_shape* shapes, int32_t num_layers,
                           const jorge_hparams* hp, void* hip_stream, jorge_ctx** out);
+
+/* Plans a context without a GPU: lays out the device arena and builds and
+ * checks every launch table on the host (each access of each grouped launch
+ * inside its buffer, alignment and extents as the kernels assume), exactly as
+ * jorge_create does, then frees everything. Makes no HIP call.
+ * *arena_bytes receives the size of the device allocation jorge_create would
+ * make. Same argument rules and errors as jorge_create; a table that fails
+ * the check returns JORGE_ERR_HIP (an internal error). */
+jorge_status jorge_plan(const jorge_shape* shapes, int32_t num_layers, const jorge_hparams* hp,
+                        int64_t* arena_bytes);
 
 /* One Jorge step for every layer (Algorithm 2 with Algorithm 3 and decoupled
  * weight decay). With t the new step number (1 for the first call):
@@ -170,7 +191,15 @@ jorge_status jorge_set_timing(jorge_ctx* ctx, int32_t enable);
 jorge_status jorge_read_timing(jorge_ctx* ctx, double* ms, int64_t* launches, int32_t n);
 jorge_status jorge_reset_timing(jorge_ctx* ctx);
 int32_t      jorge_num_stages(void);
+/* Algorithmic flops of each stage in one step that updates the factors
+ * (symmetric products counted once per stored pair), for
+ * min(n, jorge_num_stages()) stages; flops: host array. */
+jorge_status jorge_stage_flops(const jorge_ctx* ctx, double* flops, int32_t n);
 const char*  jorge_stage_name(int32_t stage);  /* NULL if out of range */
+
+/* The evaluation order chosen for one factor: side 0 = L_hat, 1 = R_hat;
+ * *form receives JORGE_FORM_EXPLICIT or JORGE_FORM_FACTORED. */
+jorge_status jorge_factor_form(const jorge_ctx* ctx, int32_t layer, int32_t side, int32_t* form);
 
 /* Frees the context and all device memory it holds; NULL is ignored.
  * Synchronises the context's stream first. */

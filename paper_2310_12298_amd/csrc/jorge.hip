@@ -1,29 +1,43 @@
 // Host runtime and C ABI of the Jorge optimizer step on gfx950.
 //
 // A context owns one device arena holding, per layer, the factors L_hat and
-// R_hat (padded to multiples of 32, zero outside the valid block), three
-// workspace matrices per factor, the padded gradient, the intermediate
-// L_hat G, both momenta and the partial-sum slots; and the device tables that
-// describe every grouped launch. Tables are built once at creation, so a
-// step is a fixed sequence of launches on one stream with no host sync.
+// R_hat (padded to multiples of 32, zero outside the valid block), the
+// workspace of each factor's update, the padded gradient and its transpose,
+// the intermediate L_hat G, both momenta and the partial-sum slots; and the
+// device tables that describe every grouped launch. Tables are built once at
+// creation, so a step is a fixed sequence of launches on one stream with no
+// host sync.
 //
-// Update step (Algorithm 2, Appendix A.1, Algorithm 3, Section 4):
-//   stage-in   Gp <- G, Gpt <- G^T, m_SGD <- beta1 m_SGD + G, partial sums of m_SGD^2
-//   gram       M_L = G G^T, M_R = G^T G and A^2 = A A     (one launch, symmetric tiles only)
-//   pow4       A^4 = A^2 A^2                              (symmetric tiles only)
-//   xform      X = A^4 M, partial sums of X^2
-//   ffinal     nu = ||X||_F, beta, c, s per factor
-//   poly       P = I - (c/4) X + (5c^2/32) X X
-//   update     Z = s A P
-//   symm       A <- (Z + Z^T)/2
-//   precond    T = L_hat G, then G~ = T R_hat fused with m <- beta1 m + (1-beta1) G~
-//   lfinal     ||m||, ||m_SGD||, grafted step g
-//   weight     theta <- theta (1 - lr wd) - g m
+// Each factor A (d x d) is updated from the statistic M = H H^T, where H is
+// G (L side, d = m, k = n) or G^T (R side, d = n, k = m) (Algorithm 2,
+// Appendix A.1). Two evaluation orders give the same factor:
+//
+//   explicit (the paper's order):  A^2, A^4, X = A^4 M, nu = ||X||_F,
+//     P = I - (c/4) X + (5c^2/32) X X, Z = s A P, A <- (Z + Z^T)/2.
+//   factored, through H (rank of M is at most k):  with U = A^4 H,
+//     X = U H^T, X X = U S H^T with S = H^T U (k x k), so
+//     P = I - U (aI - bS) H^T and A P = A - W H^T with W = A^5 H (aI - bS);
+//     nu^2 = ||U H^T||_F^2 = <U^T U, H^T H>; the symmetrized factor is
+//     s A - (s/2)(W H^T + H W^T). It costs about 12 d^2 k + 5 d k^2 flops
+//     against 8 d^3 + d^2 k, and is chosen per factor by the tile work of
+//     both orders (hp.factor_form can force either).
+//
+// Update step, as dependency levels (every GEMM of a level is one grouped
+// launch; "Yt_j" is (A^j H)^T, k x d):
+//   stage-in  Gp <- G, Gpt <- G^T, m_SGD <- beta1 m_SGD + G, partial sums of m_SGD^2
+//   gram      explicit: M = H H^T, A^2      factored: Q = H^T H, Yt_1 = H^T A^T
+//   pow4      explicit: A^4                 factored: Yt_2
+//   xform     explicit: X, X^T, ||X||^2     factored: Yt_3, S = Yt_2 Yt_2^T
+//   chain4                                  factored: Yt_4
+//   chain5                                  factored: A^5 H (stored d x k), <U^T U, Q>
+//   ffinal    nu = ||X||_F, beta, c, s per factor
+//   poly      explicit: P^T                 factored: W = a A^5 H - b A^5 H S
+//   update    explicit: Z = s A P           factored: A <- s A - (s/2)(W H^T + H W^T)
+//   symm      explicit: A <- (Z + Z^T)/2
+//   precond   T = L_hat G, then G~ = T R_hat fused with m <- beta1 m + (1-beta1) G~
+//   lfinal    ||m||, ||m_SGD||, grafted step g
+//   weight    theta <- theta (1 - lr wd) - g m
 // Non-update steps run stage-in, precond, lfinal and weight only.
-//
-// Factors no larger than hp.small_factor_max skip the grouped launches: one
-// workgroup per factor runs its whole update (chain_kernel) on a second
-// stream, forked after stage-in and joined before preconditioning.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -43,25 +57,28 @@ using namespace jorge;
 
 namespace {
 
-// Timed stages. With symmetric factors the Gram products and A^2 share the
-// "gram" launch and "pow2" has none; the literal mode launches pow2 apart.
+// Timed stages: one per dependency level of the update (see above).
 enum Stage : int {
-    ST_STAGEIN = 0, ST_GRAM, ST_POW2, ST_POW4, ST_XFORM, ST_FFINAL, ST_POLY, ST_UPDATE, ST_SYMM,
-    ST_CHAIN, ST_PRECOND_L, ST_PRECOND_R, ST_LFINAL, ST_WEIGHT, ST_COUNT
+    ST_STAGEIN = 0, ST_GRAM, ST_POW4, ST_XFORM, ST_CHAIN4, ST_CHAIN5, ST_FFINAL, ST_POLY, ST_UPDATE,
+    ST_SYMM, ST_PRECOND_L, ST_PRECOND_R, ST_LFINAL, ST_WEIGHT, ST_COUNT
 };
 const char* const kStageNames[ST_COUNT] = {
-    "stage_in", "gram", "pow2", "pow4", "xform", "factor_finalize", "poly", "update", "symmetrize",
-    "small_chain", "precond_L", "precond_R", "layer_finalize", "weight"};
+    "stage_in", "gram", "pow4", "xform", "chain4", "chain5", "factor_finalize", "poly", "update",
+    "symmetrize", "precond_L", "precond_R", "layer_finalize", "weight"};
+// The GEMM levels of an update step, in launch order.
+constexpr int kLevels[] = {ST_GRAM, ST_POW4, ST_XFORM, ST_CHAIN4, ST_CHAIN5, ST_POLY, ST_UPDATE};
 
 constexpr size_t kAlign = 256;
 constexpr int kFlatChunkElems = 16384;
 constexpr int kGroupRows = 8;  // tile rows per group in the tile ordering
 
 inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+inline int64_t tiles_of(int64_t x) { return (x + kTile - 1) / kTile; }
 
 struct GemmStage {
     std::vector<GemmProblem> probs;
     std::vector<TileDesc> tiles;
+    double flops = 0.0;  // algorithmic flops of all its products
     GemmProblem* dprobs = nullptr;
     TileDesc* dtiles = nullptr;
     int ntiles() const { return (int)tiles.size(); }
@@ -74,10 +91,14 @@ struct LayerHost {
     int fL, fR;
 };
 
+// One factor: A (d x d) with statistic H H^T, H being d x k.
+//   explicit workspace: w[0] M then P^T, w[1] A^2 then X, w[2] A^4 then Z, w[3] X^T (dp x dp each)
+//   factored workspace: w[0], w[1] kp x dp (Yt_j, A^5 H, W), w[2] Q = H^T H, w[3] S (kp x kp)
 struct FactorHost {
-    int layer, side, d, dp;
-    bool small = false;  // updated by chain_kernel rather than the grouped launches
-    size_t off_A, off_W0, off_W1, off_W2, off_part, off_sc;
+    int layer, side, d, dp, k, kp;
+    bool expl = true;
+    size_t off_A, off_part, off_sc;
+    size_t off_w[4];
     int nparts = 0;
 };
 
@@ -97,22 +118,20 @@ struct jorge_ctx {
     std::vector<FactorHost> factors;
     char* arena = nullptr;
     size_t arena_bytes = 0;
+    std::vector<std::pair<size_t, size_t>> regions;  // (offset, bytes) of every arena buffer
     // device tables
     LayerDev* dlayers = nullptr;
     FactorDev* dfactors = nullptr;
     StageTile* dstage = nullptr;
     FlatChunk* dflat = nullptr;
     SymTile* dsym = nullptr;
-    int* dbig = nullptr;     // indices of the factors in the grouped launches
-    int* dsmall = nullptr;   // indices of the factors updated by chain_kernel, costliest first
-    std::vector<int> big, small;
-    hipStream_t side = nullptr;                   // stream of chain_kernel
-    hipEvent_t ev_fork = nullptr, ev_join = nullptr;
     std::vector<StageTile> stage_tiles;
     std::vector<FlatChunk> flat_chunks;
     std::vector<int> stage_batch_start, flat_batch_start;  // first block of each layer batch
     std::vector<SymTile> sym_tiles;
-    GemmStage gram, pow2, pow4, xform, poly, update, pre_l, pre_r;
+    // Per stage: products with both operands K-major, and (literal mode only)
+    // powers of non-symmetric factors, which need an MN-major B.
+    GemmStage nt[ST_COUNT], nn[ST_COUNT];
     // timing
     bool timing = false;
     std::vector<hipEvent_t> free_events;
@@ -155,38 +174,51 @@ hipEvent_t take_event(jorge_ctx* c) {
 struct TimedLaunch {
     jorge_ctx* c;
     int stage;
-    hipStream_t stream;
     hipEvent_t start = nullptr, stop = nullptr;
-    TimedLaunch(jorge_ctx* ctx, int st) : TimedLaunch(ctx, st, ctx->stream) {}
-    TimedLaunch(jorge_ctx* ctx, int st, hipStream_t s) : c(ctx), stage(st), stream(s) {
+    TimedLaunch(jorge_ctx* ctx, int st) : c(ctx), stage(st) {
         if (!c->timing) return;
         start = take_event(c);
         stop = take_event(c);
-        if (start) (void)hipEventRecord(start, stream);
+        if (start) (void)hipEventRecord(start, c->stream);
     }
     void finish() {
         if (!c->timing || !start || !stop) return;
-        (void)hipEventRecord(stop, stream);
+        (void)hipEventRecord(stop, c->stream);
         c->pending.push_back({stage, start, stop});
     }
 };
 
+// A product for add_problem: C = A B^T (NT) or A B (NN) with the given
+// padded extents; everything else of the problem is zero until set.
+GemmProblem product(const float* A, int lda, const float* B, int ldb, int M, int N, int K) {
+    GemmProblem p{};
+    p.A = A; p.lda = lda;
+    p.B = B; p.ldb = ldb;
+    p.M = M; p.N = N; p.K = K; p.K1 = K;
+    p.coef = CO_ONE;
+    return p;
+}
+
 // Adds a product's tiles in grouped order: bands of kGroupRows tile rows,
 // walked column by column, so concurrently running workgroups share panels.
-void add_problem(GemmStage& st, const GemmProblem& p, bool upper_only) {
+// flops: the product's algorithmic flops. Returns the number of partial-sum
+// slots (one per tile).
+int add_problem(GemmStage& st, const GemmProblem& p, double flops) {
     const int idx = (int)st.probs.size();
     st.probs.push_back(p);
-    const int tm_n = (p.M + kTile - 1) / kTile, tn_n = (p.N + kTile - 1) / kTile;
+    st.flops += flops;
+    const int tm_n = (int)tiles_of(p.M), tn_n = (int)tiles_of(p.N);
     int slot = 0;
     for (int g = 0; g < tm_n; g += kGroupRows)
         for (int tn = 0; tn < tn_n; ++tn)
             for (int tm = g; tm < std::min(g + kGroupRows, tm_n); ++tm) {
-                if (upper_only && tm > tn) continue;
+                if (p.upper && tm > tn) continue;
                 st.tiles.push_back({idx, tm, tn, slot++});
             }
+    return slot;
 }
 
-int tile_count(int M, int N) { return ((M + kTile - 1) / kTile) * ((N + kTile - 1) / kTile); }
+int tile_count(int M, int N) { return (int)(tiles_of(M) * tiles_of(N)); }
 
 constexpr int kXcds = 8;  // workgroup b of a launch runs on XCD b % 8, in increasing b
 
@@ -236,11 +268,11 @@ void order_for_xcds(GemmStage& st) {
     st.tiles.swap(out);
 }
 
-template <bool AK, bool BK, int EPI>
+template <bool AK, bool BK>
 jorge_status launch_gemm(jorge_ctx* c, const GemmStage& st, int stage, float beta1) {
     if (st.ntiles() == 0) return JORGE_OK;
     TimedLaunch tl(c, stage);
-    hipLaunchKernelGGL((gemm_grouped<AK, BK, EPI>), dim3(st.ntiles()), dim3(kGemmThreads), 0, c->stream,
+    hipLaunchKernelGGL((gemm_grouped<AK, BK>), dim3(st.ntiles()), dim3(kGemmThreads), 0, c->stream,
                        st.dprobs, st.dtiles, beta1);
     tl.finish();
     JORGE_HIP(c, hipGetLastError());
@@ -256,18 +288,39 @@ jorge_status validate_hparams(const jorge_hparams* hp) {
         return JORGE_ERR_INVALID_ARGUMENT;
     if ((hp->graft != 0 && hp->graft != 1) || (hp->symmetrize != 0 && hp->symmetrize != 1))
         return JORGE_ERR_INVALID_ARGUMENT;
-    if (hp->small_factor_max < 0 || hp->small_factor_max > 4096) return JORGE_ERR_INVALID_ARGUMENT;
+    if (hp->factor_form < JORGE_FORM_AUTO || hp->factor_form > JORGE_FORM_FACTORED)
+        return JORGE_ERR_INVALID_ARGUMENT;
     return JORGE_OK;
 }
 
-// Builds every offset and launch table; returns the arena size in bytes.
+// Tile work (128 x 128 tiles times K) of one product, as the grouped launch runs it.
+int64_t tile_work(int64_t M, int64_t N, int64_t K, bool upper) {
+    const int64_t tm = tiles_of(M), tn = tiles_of(N);
+    return (upper ? tm * (tm + 1) / 2 : tm * tn) * K;
+}
+
+// Whether a factor of padded size dp with statistic rank kp is cheaper in the
+// explicit order than in the factored one (same product list as build_tables).
+bool explicit_is_cheaper(int64_t dp, int64_t kp, bool sym) {
+    const int64_t e = tile_work(dp, dp, kp, true) + 2 * tile_work(dp, dp, dp, sym) +
+                      3 * tile_work(dp, dp, dp, false);
+    const int64_t f = tile_work(kp, kp, dp, true) + 5 * tile_work(kp, dp, dp, false) +
+                      tile_work(kp, kp, dp, sym) + tile_work(kp, kp, dp, true) +
+                      tile_work(dp, kp, kp, false) + (sym ? tile_work(dp, dp, 2 * kp, true)
+                                                          : tile_work(dp, dp, kp, false));
+    return e <= f;
+}
+
+// Builds every offset; returns the arena size in bytes.
 size_t plan(jorge_ctx* c) {
     size_t off = 0;
     auto take = [&](size_t bytes) {
         const size_t o = off;
+        c->regions.push_back({o, bytes});
         off = (size_t)round_up((int64_t)(off + bytes), kAlign);
         return o;
     };
+    const bool sym = c->hp.symmetrize != 0;
     for (auto& L : c->layers) {
         for (int side = 0; side < 2; ++side) {
             FactorHost F{};
@@ -275,15 +328,26 @@ size_t plan(jorge_ctx* c) {
             F.side = side;
             F.d = side == 0 ? L.m : L.n;
             F.dp = side == 0 ? L.mp : L.np;
-            const size_t mat = (size_t)F.dp * F.dp * sizeof(float);
-            F.off_A = take(mat);
-            F.off_W0 = take(mat);
-            F.off_W1 = take(mat);
-            F.off_W2 = take(mat);
-            F.nparts = tile_count(F.dp, F.dp);
+            F.k = side == 0 ? L.n : L.m;
+            F.kp = side == 0 ? L.np : L.mp;
+            if (c->hp.factor_form == JORGE_FORM_EXPLICIT) F.expl = true;
+            else if (c->hp.factor_form == JORGE_FORM_FACTORED) F.expl = false;
+            else F.expl = explicit_is_cheaper(F.dp, F.kp, sym);
+            const size_t dd = (size_t)F.dp * F.dp * sizeof(float);
+            F.off_A = take(dd);
+            if (F.expl) {
+                for (int w = 0; w < 4; ++w) F.off_w[w] = take(dd);
+                F.nparts = tile_count(F.dp, F.dp);
+            } else {
+                const size_t kd = (size_t)F.kp * F.dp * sizeof(float), kk = (size_t)F.kp * F.kp * sizeof(float);
+                F.off_w[0] = take(kd);
+                F.off_w[1] = take(kd);
+                F.off_w[2] = take(kk);
+                F.off_w[3] = take(kk);
+                F.nparts = tile_count(F.kp, F.kp);
+            }
             F.off_part = take((size_t)F.nparts * sizeof(double));
             F.off_sc = take(sizeof(FactorScalars));
-            F.small = F.dp <= c->hp.small_factor_max;
             (side == 0 ? L.fL : L.fR) = (int)c->factors.size();
             c->factors.push_back(F);
         }
@@ -306,23 +370,124 @@ size_t plan(jorge_ctx* c) {
 template <typename T>
 T* at(jorge_ctx* c, size_t off) { return reinterpret_cast<T*>(c->arena + off); }
 
+// The products of one factor's update in the explicit order.
+void add_explicit(jorge_ctx* c, const FactorHost& F, const FactorDev& fd, const float* Hr) {
+    const bool sym = c->hp.symmetrize != 0;
+    const int dp = F.dp, kp = F.kp;
+    const double d = F.d, k = F.k;
+    float* A = fd.A;
+    float* W0 = at<float>(c, F.off_w[0]);
+    float* W1 = at<float>(c, F.off_w[1]);
+    float* W2 = at<float>(c, F.off_w[2]);
+    float* W3 = at<float>(c, F.off_w[3]);
+    // M = H H^T
+    GemmProblem m = product(Hr, kp, Hr, kp, dp, dp, kp);
+    m.C = W0; m.ldc = dp; m.flags = EF_STORE; m.upper = 1;
+    add_problem(c->nt[ST_GRAM], m, d * d * k);
+    // A^2 and A^4: symmetric products of symmetric factors; general in the literal mode.
+    GemmProblem p2 = product(A, dp, A, dp, dp, dp, dp);
+    p2.C = W1; p2.ldc = dp; p2.flags = EF_STORE; p2.upper = sym;
+    add_problem(sym ? c->nt[ST_GRAM] : c->nn[ST_GRAM], p2, (sym ? 1 : 2) * d * d * d);
+    GemmProblem p4 = product(W1, dp, W1, dp, dp, dp, dp);
+    p4.C = W2; p4.ldc = dp; p4.flags = EF_STORE; p4.upper = sym;
+    add_problem(sym ? c->nt[ST_POW4] : c->nn[ST_POW4], p4, (sym ? 1 : 2) * d * d * d);
+    // X = A^4 M (M symmetric, so it is its own K-major B), stored with its transpose.
+    GemmProblem x = product(W2, dp, W0, dp, dp, dp, dp);
+    x.C = W1; x.ldc = dp; x.C2 = W3; x.ldc2 = dp;
+    x.flags = EF_STORE | EF_STORE_T | EF_NORM; x.partials = fd.partials;
+    add_problem(c->nt[ST_XFORM], x, 2 * d * d * d);
+    // P = I - a X + b X X, stored transposed (the K-major B of the next product).
+    GemmProblem p = product(W1, dp, W3, dp, dp, dp, dp);
+    p.C2 = W0; p.ldc2 = dp; p.X = W1; p.ldx = dp; p.sc = fd.sc;
+    p.flags = EF_STORE_T | EF_READX; p.coef = CO_POLY; p.valid_m = p.valid_n = F.d;
+    add_problem(c->nt[ST_POLY], p, 2 * d * d * d);
+    // Z = s A P
+    GemmProblem z = product(A, dp, W0, dp, dp, dp, dp);
+    z.C = W2; z.ldc = dp; z.sc = fd.sc; z.flags = EF_STORE; z.coef = CO_SCALE;
+    add_problem(c->nt[ST_UPDATE], z, 2 * d * d * d);
+    const int fi = (int)(&F - &c->factors[0]);
+    for (int ti = 0; ti * 64 < dp; ++ti)
+        for (int tj = ti; tj * 64 < dp; ++tj) c->sym_tiles.push_back({fi, ti, tj, 0});
+}
+
+// The products of one factor's update in the factored order (through H).
+// Hr: H row-major (dp x kp, ld kp); Ht: H^T row-major (kp x dp, ld dp).
+int add_factored(jorge_ctx* c, const FactorHost& F, const FactorDev& fd, const float* Hr, const float* Ht) {
+    const bool sym = c->hp.symmetrize != 0;
+    const int dp = F.dp, kp = F.kp;
+    const double d = F.d, k = F.k;
+    float* A = fd.A;
+    float* P0 = at<float>(c, F.off_w[0]);
+    float* P1 = at<float>(c, F.off_w[1]);
+    float* Q = at<float>(c, F.off_w[2]);
+    float* S = at<float>(c, F.off_w[3]);
+    // Q = H^T H
+    GemmProblem q = product(Ht, dp, Ht, dp, kp, kp, dp);
+    q.C = Q; q.ldc = kp; q.flags = EF_STORE; q.upper = 1;
+    add_problem(c->nt[ST_GRAM], q, k * k * d);
+    // Yt_{j+1} = Yt_j A^T, starting from Yt_0 = H^T: P0, P1, P0, P1.
+    const float* src = Ht;
+    float* dst[4] = {P0, P1, P0, P1};
+    const int lvl[4] = {ST_GRAM, ST_POW4, ST_XFORM, ST_CHAIN4};
+    for (int j = 0; j < 4; ++j) {
+        GemmProblem y = product(src, dp, A, dp, kp, dp, dp);
+        y.C = dst[j]; y.ldc = dp; y.flags = EF_STORE;
+        add_problem(c->nt[lvl[j]], y, 2 * k * d * d);
+        src = dst[j];
+    }
+    // S = H^T A^4 H: Yt_2 Yt_2^T for symmetric factors (read from P1 while Yt_3 goes to P0).
+    if (sym) {
+        GemmProblem s = product(P1, dp, P1, dp, kp, kp, dp);
+        s.C = S; s.ldc = kp; s.flags = EF_STORE; s.upper = 1;
+        add_problem(c->nt[ST_XFORM], s, k * k * d);
+    }
+    // A^5 H = (Yt_4 A^T)^T, stored d x k in P0; ||X||^2 = <Yt_4 Yt_4^T, Q>.
+    GemmProblem y5 = product(P1, dp, A, dp, kp, dp, dp);
+    y5.C2 = P0; y5.ldc2 = kp; y5.flags = EF_STORE_T;
+    add_problem(c->nt[ST_CHAIN5], y5, 2 * k * d * d);
+    GemmProblem nu = product(P1, dp, P1, dp, kp, kp, dp);
+    nu.X = Q; nu.ldx = kp; nu.flags = EF_DOT; nu.upper = 1; nu.partials = fd.partials;
+    const int slots = add_problem(c->nt[ST_CHAIN5], nu, k * k * d);
+    // Literal mode: S^T = U^T H = Yt_4 H (general).
+    if (!sym) {
+        GemmProblem s = product(P1, dp, Ht, dp, kp, kp, dp);
+        s.C = S; s.ldc = kp; s.flags = EF_STORE;
+        add_problem(c->nt[ST_CHAIN5], s, 2 * k * k * d);
+    }
+    // W = a A^5 H - b A^5 H S (B = S^T row-major), into P1.
+    GemmProblem w = product(P0, kp, S, kp, dp, kp, kp);
+    w.C = P1; w.ldc = kp; w.X = P0; w.ldx = kp; w.sc = fd.sc;
+    w.flags = EF_STORE | EF_READX; w.coef = CO_WMIX;
+    add_problem(c->nt[ST_POLY], w, 2 * d * k * k);
+    // A <- s A - (s/2)(W H^T + H W^T) (symmetric, in place) or s A - s W H^T.
+    GemmProblem u = product(P1, kp, Hr, kp, dp, dp, kp);
+    u.C = A; u.ldc = dp; u.X = A; u.ldx = dp; u.sc = fd.sc; u.flags = EF_STORE | EF_READX;
+    if (sym) {
+        u.A2 = Hr; u.lda2 = kp; u.B2 = P1; u.ldb2 = kp;
+        u.K = 2 * kp;
+        u.coef = CO_SYR2K;
+        u.upper = 1;
+        add_problem(c->nt[ST_UPDATE], u, d * d * 2 * k);
+    } else {
+        u.coef = CO_LITUPD;
+        add_problem(c->nt[ST_UPDATE], u, 2 * d * d * k);
+    }
+    return slots;
+}
+
 // Fills the host-side launch tables (device pointers already known).
 void build_tables(jorge_ctx* c, std::vector<LayerDev>& ld, std::vector<FactorDev>& fd) {
     const int nl = (int)c->layers.size();
     for (auto& F : c->factors) {
         FactorDev d{};
         d.A = at<float>(c, F.off_A);
-        d.W0 = at<float>(c, F.off_W0);
-        d.W1 = at<float>(c, F.off_W1);
-        d.W2 = at<float>(c, F.off_W2);
         d.sc = at<FactorScalars>(c, F.off_sc);
         d.partials = at<double>(c, F.off_part);
+        d.Z = F.expl ? at<float>(c, F.off_w[2]) : nullptr;
         d.d = F.d;
         d.dp = F.dp;
         d.nparts = F.nparts;
-        const auto& L = c->layers[F.layer];
-        d.gop = at<float>(c, F.side == 0 ? L.off_Gp : L.off_Gpt);
-        d.gk = F.side == 0 ? L.np : L.mp;
+        d.explicit_form = F.expl ? 1 : 0;
         fd.push_back(d);
     }
     for (int li = 0; li < nl; ++li) {
@@ -358,55 +523,26 @@ void build_tables(jorge_ctx* c, std::vector<LayerDev>& ld, std::vector<FactorDev
     c->stage_batch_start.push_back((int)c->stage_tiles.size());
     c->flat_batch_start.push_back((int)c->flat_chunks.size());
 
-    // Factors in decreasing size, so large tiles are dispatched first.
+    // Factors in decreasing size, so large tiles come first within a stage.
     std::vector<int> order(c->factors.size());
     for (size_t i = 0; i < order.size(); ++i) order[i] = (int)i;
     std::stable_sort(order.begin(), order.end(),
                      [&](int a, int b) { return c->factors[a].dp > c->factors[b].dp; });
     for (int fi : order) {
-        const auto& F = c->factors[fi];
-        if (F.small) continue;
-        c->big.push_back(fi);
-        const FactorDev& d = fd[fi];
-        const auto& L = c->layers[F.layer];
+        FactorHost& F = c->factors[fi];
         const LayerDev& l = ld[F.layer];
-        GemmProblem g{};
-        g.M = g.N = g.K = F.dp;
-        g.lda = g.ldb = g.ldc = g.ldx = F.dp;
-        g.valid_m = g.valid_n = F.d;
-        // Gram statistic into W0: G G^T = Gp Gp^T (K = np) and G^T G = Gpt Gpt^T (K = mp),
-        // both with K-contiguous operands.
-        GemmProblem s = g;
-        s.C = d.W0;
-        s.A = s.B = F.side == 0 ? l.Gp : l.Gpt;
-        s.K = F.side == 0 ? L.np : L.mp;
-        s.lda = s.ldb = s.K;
-        add_problem(c->gram, s, true);
-        // With symmetric factors A^2 and A^4 are symmetric products (upper tiles, mirrored);
-        // the literal mode keeps non-symmetric factors and needs the general product.
-        const bool sym = c->hp.symmetrize != 0;
-        GemmProblem p2 = g; p2.A = p2.B = d.A; p2.C = d.W1; add_problem(c->pow2, p2, sym);
-        GemmProblem p4 = g; p4.A = p4.B = d.W1; p4.C = d.W2; add_problem(c->pow4, p4, sym);
-        GemmProblem px = g; px.A = d.W2; px.B = d.W0; px.C = d.W1; px.partials = d.partials;
-        add_problem(c->xform, px, false);
-        GemmProblem pp = g; pp.A = pp.B = pp.X = d.W1; pp.C = d.W2; pp.sc = d.sc;
-        add_problem(c->poly, pp, false);
-        GemmProblem pu = g; pu.A = d.A; pu.B = d.W2; pu.C = d.W0; pu.sc = d.sc;
-        add_problem(c->update, pu, false);
-        for (int ti = 0; ti * 64 < F.dp; ++ti)
-            for (int tj = ti; tj * 64 < F.dp; ++tj) c->sym_tiles.push_back({fi, ti, tj, 0});
+        // H row-major (d x k) and H^T row-major (k x d): G and G^T for L, the reverse for R.
+        const float* Hr = F.side == 0 ? l.Gp : l.Gpt;
+        const float* Ht = F.side == 0 ? l.Gpt : l.Gp;
+        if (F.expl) {
+            add_explicit(c, F, fd[fi], Hr);
+        } else {
+            F.nparts = add_factored(c, F, fd[fi], Hr, Ht);
+            fd[fi].nparts = F.nparts;
+        }
     }
-    // Small factors, costliest first (tile-K products of the Gram and the chain).
-    std::vector<std::pair<int64_t, int>> sc;
-    for (size_t fi = 0; fi < c->factors.size(); ++fi) {
-        const auto& F = c->factors[fi];
-        if (!F.small) continue;
-        const int64_t nt = (F.dp + kTile - 1) / kTile, sym = nt * (nt + 1) / 2;
-        sc.push_back({sym * fd[fi].gk + (2 * sym + 3 * nt * nt) * F.dp, (int)fi});
-    }
-    std::stable_sort(sc.begin(), sc.end(), [](const auto& a, const auto& b) { return a.first > b.first; });
-    for (const auto& e : sc) c->small.push_back(e.second);
     // Preconditioning, largest layers first.
+    const bool sym = c->hp.symmetrize != 0;
     std::vector<int> lorder(nl);
     for (int i = 0; i < nl; ++i) lorder[i] = i;
     std::stable_sort(lorder.begin(), lorder.end(), [&](int a, int b) {
@@ -416,20 +552,147 @@ void build_tables(jorge_ctx* c, std::vector<LayerDev>& ld, std::vector<FactorDev
     for (int li : lorder) {
         const auto& L = c->layers[li];
         const LayerDev& l = ld[li];
-        GemmProblem a{};  // T = L_hat G: A = L_hat, B^T = Gpt (both K-major)
-        a.A = fd[L.fL].A; a.B = l.Gpt; a.C = l.T;
-        a.M = L.mp; a.N = L.np; a.K = L.mp;
-        a.lda = L.mp; a.ldb = L.mp; a.ldc = L.np;
-        a.valid_m = L.m; a.valid_n = L.n;
-        add_problem(c->pre_l, a, false);
-        GemmProblem b{};  // G~ = T R_hat: A = T (K-major), B = R_hat (K-major when symmetric)
-        b.A = l.T; b.B = fd[L.fR].A;
-        b.M = L.mp; b.N = L.np; b.K = L.np;
-        b.lda = L.np; b.ldb = L.np;
+        const double m = L.m, n = L.n;
+        // T = L_hat G: B^T = Gpt (both K-major)
+        GemmProblem a = product(fd[L.fL].A, L.mp, l.Gpt, L.mp, L.mp, L.np, L.mp);
+        a.C = l.T; a.ldc = L.np; a.flags = EF_STORE;
+        add_problem(c->nt[ST_PRECOND_L], a, 2 * m * m * n);
+        // G~ = T R_hat fused with the momentum: R_hat is its own K-major B when symmetric.
+        GemmProblem b = product(l.T, L.np, fd[L.fR].A, L.np, L.mp, L.np, L.np);
         b.mom = l.mom; b.ldmom = L.n; b.partials = l.part_m;
-        b.valid_m = L.m; b.valid_n = L.n;
-        add_problem(c->pre_r, b, false);
+        b.valid_m = L.m; b.valid_n = L.n; b.flags = EF_MOMENTUM;
+        add_problem(sym ? c->nt[ST_PRECOND_R] : c->nn[ST_PRECOND_R], b, 2 * m * n * n);
     }
+}
+
+// Whether [p, p + bytes) lies inside one arena buffer.
+bool in_buffer(const jorge_ctx* c, const void* p, int64_t bytes) {
+    const char* q = static_cast<const char*>(p);
+    if (bytes <= 0 || q < c->arena || q + bytes > c->arena + c->arena_bytes) return false;
+    const size_t off = (size_t)(q - c->arena);
+    auto it = std::upper_bound(c->regions.begin(), c->regions.end(), std::make_pair(off, SIZE_MAX));
+    if (it == c->regions.begin()) return false;
+    --it;
+    return off + (size_t)bytes <= it->first + it->second;
+}
+
+bool aligned16(const void* p, int ld) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0 && ld % 4 == 0; }
+
+// Checks, on the host, that every access a grouped launch makes stays inside
+// the buffer its pointer starts in and meets the kernel's alignment and
+// extent assumptions (the tile loads and the vector stores of the epilogue).
+// Returns an empty string, or a description of the first violation.
+std::string check_stage(const jorge_ctx* c, const GemmStage& st, bool bk, const char* name) {
+    auto fl = [](int64_t last) { return (last + 1) * (int64_t)sizeof(float); };
+    for (size_t i = 0; i < st.probs.size(); ++i) {
+        const GemmProblem& p = st.probs[i];
+        const std::string where = std::string(name) + " problem " + std::to_string(i) + ": ";
+        if (p.M <= 0 || p.N <= 0 || p.K <= 0 || p.M % 32 || p.N % 32 || p.K % kSlab || p.K1 % kSlab ||
+            p.K1 <= 0 || p.K1 > p.K)
+            return where + "extents";
+        const int k1 = p.K1, k2 = p.K - p.K1;
+        if (!aligned16(p.A, p.lda) || !in_buffer(c, p.A, fl((int64_t)(p.M - 1) * p.lda + k1 - 1)))
+            return where + "A";
+        const int64_t blast = bk ? (int64_t)(p.N - 1) * p.ldb + k1 - 1 : (int64_t)(k1 - 1) * p.ldb + p.N - 1;
+        if (!aligned16(p.B, p.ldb) || !in_buffer(c, p.B, fl(blast))) return where + "B";
+        if (k2 > 0) {
+            if (!aligned16(p.A2, p.lda2) || !in_buffer(c, p.A2, fl((int64_t)(p.M - 1) * p.lda2 + k2 - 1)))
+                return where + "A2";
+            const int64_t b2 = bk ? (int64_t)(p.N - 1) * p.ldb2 + k2 - 1 : (int64_t)(k2 - 1) * p.ldb2 + p.N - 1;
+            if (!aligned16(p.B2, p.ldb2) || !in_buffer(c, p.B2, fl(b2))) return where + "B2";
+        }
+        if (p.flags & EF_STORE) {
+            int64_t last = (int64_t)(p.M - 1) * p.ldc + p.N - 1;
+            if (p.upper) last = std::max(last, (int64_t)(p.N - 1) * p.ldc + p.M - 1);
+            if ((p.upper && (p.M != p.N || !aligned16(p.C, p.ldc))) || !in_buffer(c, p.C, fl(last)))
+                return where + "C";
+        }
+        if ((p.flags & EF_STORE_T) && (!aligned16(p.C2, p.ldc2) ||
+                                       !in_buffer(c, p.C2, fl((int64_t)(p.N - 1) * p.ldc2 + p.M - 1))))
+            return where + "C2";
+        if ((p.flags & (EF_READX | EF_DOT)) && !in_buffer(c, p.X, fl((int64_t)(p.M - 1) * p.ldx + p.N - 1)))
+            return where + "X";
+        if ((p.flags & EF_READX) && p.coef == CO_POLY && (p.valid_m > p.M || p.valid_m > p.N))
+            return where + "identity extent";
+        if ((p.flags & EF_MOMENTUM) &&
+            (p.valid_m > p.M || p.valid_n > p.N ||
+             !in_buffer(c, p.mom, fl((int64_t)(p.valid_m - 1) * p.ldmom + p.valid_n - 1))))
+            return where + "momentum";
+        if (p.coef != CO_ONE && !in_buffer(c, p.sc, (int64_t)sizeof(FactorScalars))) return where + "scalars";
+    }
+    for (const TileDesc& t : st.tiles) {
+        if (t.prob < 0 || t.prob >= (int)st.probs.size()) return std::string(name) + ": tile problem";
+        const GemmProblem& p = st.probs[t.prob];
+        if (t.tm < 0 || t.tn < 0 || t.tm >= tiles_of(p.M) || t.tn >= tiles_of(p.N) || (p.upper && t.tm > t.tn))
+            return std::string(name) + ": tile index";
+        if ((p.flags & (EF_NORM | EF_DOT | EF_MOMENTUM)) &&
+            (t.slot < 0 || !in_buffer(c, p.partials, (int64_t)(t.slot + 1) * (int64_t)sizeof(double))))
+            return std::string(name) + ": partial slot";
+    }
+    return "";
+}
+
+std::string check_tables(const jorge_ctx* c, const std::vector<FactorDev>& fd) {
+    for (int i = 0; i < ST_COUNT; ++i) {
+        std::string e = check_stage(c, c->nt[i], true, kStageNames[i]);
+        if (e.empty()) e = check_stage(c, c->nn[i], false, kStageNames[i]);
+        if (!e.empty()) return e;
+    }
+    for (const SymTile& t : c->sym_tiles) {
+        const FactorDev& F = fd[t.factor];
+        const int64_t dd = (int64_t)F.dp * F.dp * (int64_t)sizeof(float);
+        if (!F.Z || t.ti < 0 || t.ti > t.tj || t.tj * 64 >= F.dp || F.dp % 4 || !in_buffer(c, F.Z, dd) ||
+            !in_buffer(c, F.A, dd))
+            return "symmetrize tile";
+    }
+    for (const FactorDev& F : fd)
+        if (!in_buffer(c, F.partials, (int64_t)F.nparts * (int64_t)sizeof(double)) || F.nparts < 1)
+            return "factor partials";
+    return "";
+}
+
+// Layer list and arena offsets of a context (no device work).
+jorge_status layout_context(jorge_ctx* c, const jorge_shape* shapes, int32_t num_layers) {
+    try {
+        c->layers.resize(num_layers);
+        for (int32_t i = 0; i < num_layers; ++i) {
+            LayerHost& L = c->layers[i];
+            L.m = (int)shapes[i].rows;
+            L.n = (int)shapes[i].cols;
+            L.mp = (int)round_up(L.m, 32);
+            L.np = (int)round_up(L.n, 32);
+        }
+        c->arena_bytes = plan(c);
+    } catch (const std::bad_alloc&) {
+        return JORGE_ERR_OUT_OF_MEMORY;
+    }
+    return JORGE_OK;
+}
+
+// Launch tables for the arena at c->arena, checked on the host.
+jorge_status tables_context(jorge_ctx* c, std::vector<LayerDev>& ld, std::vector<FactorDev>& fd) {
+    try {
+        build_tables(c, ld, fd);
+        const std::string e = check_tables(c, fd);
+        if (!e.empty()) return fail(c, JORGE_ERR_HIP, "launch table check failed: " + e);
+    } catch (const std::bad_alloc&) {
+        return JORGE_ERR_OUT_OF_MEMORY;
+    }
+    return JORGE_OK;
+}
+
+jorge_status validate_args(const jorge_shape* shapes, int32_t num_layers, const jorge_hparams* hp,
+                           jorge_hparams* h) {
+    if (!shapes || num_layers <= 0) return JORGE_ERR_INVALID_ARGUMENT;
+    if (num_layers > JORGE_MAX_LAYERS) return JORGE_ERR_UNSUPPORTED;
+    jorge_hparams_default(h);
+    if (hp) *h = *hp;
+    if (validate_hparams(h) != JORGE_OK) return JORGE_ERR_INVALID_ARGUMENT;
+    for (int32_t i = 0; i < num_layers; ++i) {
+        if (shapes[i].rows <= 0 || shapes[i].cols <= 0) return JORGE_ERR_INVALID_ARGUMENT;
+        if (shapes[i].rows > JORGE_MAX_DIM || shapes[i].cols > JORGE_MAX_DIM) return JORGE_ERR_UNSUPPORTED;
+    }
+    return JORGE_OK;
 }
 
 template <typename T>
@@ -441,19 +704,6 @@ jorge_status upload(jorge_ctx* c, const std::vector<T>& v, T** dptr) {
     return JORGE_OK;
 }
 
-// Moves every problem and tile of `from` into `into` (same kernel instantiation),
-// so independent products share one launch.
-void merge_stage(GemmStage& into, GemmStage& from) {
-    const int base = (int)into.probs.size();
-    into.probs.insert(into.probs.end(), from.probs.begin(), from.probs.end());
-    for (TileDesc t : from.tiles) {
-        t.prob += base;
-        into.tiles.push_back(t);
-    }
-    from.probs.clear();
-    from.tiles.clear();
-}
-
 jorge_status upload_stage(jorge_ctx* c, GemmStage& st) {
     order_for_xcds(st);
     jorge_status s = upload(c, st.probs, &st.dprobs);
@@ -463,21 +713,16 @@ jorge_status upload_stage(jorge_ctx* c, GemmStage& st) {
 
 void free_ctx(jorge_ctx* c) {
     if (!c) return;
-    for (GemmStage* st : {&c->gram, &c->pow2, &c->pow4, &c->xform, &c->poly, &c->update, &c->pre_l,
-                          &c->pre_r}) {
-        if (st->dprobs) (void)hipFree(st->dprobs);
-        if (st->dtiles) (void)hipFree(st->dtiles);
-    }
+    for (int i = 0; i < ST_COUNT; ++i)
+        for (GemmStage* st : {&c->nt[i], &c->nn[i]}) {
+            if (st->dprobs) (void)hipFree(st->dprobs);
+            if (st->dtiles) (void)hipFree(st->dtiles);
+        }
     if (c->dlayers) (void)hipFree(c->dlayers);
     if (c->dfactors) (void)hipFree(c->dfactors);
     if (c->dstage) (void)hipFree(c->dstage);
     if (c->dflat) (void)hipFree(c->dflat);
     if (c->dsym) (void)hipFree(c->dsym);
-    if (c->dbig) (void)hipFree(c->dbig);
-    if (c->dsmall) (void)hipFree(c->dsmall);
-    if (c->ev_fork) (void)hipEventDestroy(c->ev_fork);
-    if (c->ev_join) (void)hipEventDestroy(c->ev_join);
-    if (c->side) (void)hipStreamDestroy(c->side);
     if (c->arena) (void)hipFree(c->arena);
     for (auto& l : c->pending) {
         (void)hipEventDestroy(l.start);
@@ -487,25 +732,24 @@ void free_ctx(jorge_ctx* c) {
     delete c;
 }
 
+jorge_status launch_stage(jorge_ctx* c, int stage, float beta1) {
+    jorge_status s = launch_gemm<true, true>(c, c->nt[stage], stage, beta1);
+    if (s != JORGE_OK) return s;
+    return launch_gemm<true, false>(c, c->nn[stage], stage, beta1);
+}
+
 jorge_status run_update(jorge_ctx* c, double beta2) {
     jorge_status s;
-    if ((s = launch_gemm<true, true, EPI_SYM>(c, c->gram, ST_GRAM, 0.f)) != JORGE_OK) return s;
-    if (c->hp.symmetrize) {  // A^2 ran inside the gram launch
-        if ((s = launch_gemm<true, true, EPI_SYM>(c, c->pow4, ST_POW4, 0.f)) != JORGE_OK) return s;
-    } else {
-        if ((s = launch_gemm<true, false, EPI_STORE>(c, c->pow2, ST_POW2, 0.f)) != JORGE_OK) return s;
-        if ((s = launch_gemm<true, false, EPI_STORE>(c, c->pow4, ST_POW4, 0.f)) != JORGE_OK) return s;
+    for (int lv : kLevels) {
+        if (lv == ST_POLY) {  // every factor's nu is complete after chain5
+            TimedLaunch tl(c, ST_FFINAL);
+            hipLaunchKernelGGL(factor_finalize_kernel, dim3((unsigned)c->factors.size()), dim3(64), 0,
+                               c->stream, c->dfactors, beta2, (int)c->hp.beta_mode);
+            tl.finish();
+            JORGE_HIP(c, hipGetLastError());
+        }
+        if ((s = launch_stage(c, lv, 0.f)) != JORGE_OK) return s;
     }
-    if ((s = launch_gemm<true, true, EPI_NORM>(c, c->xform, ST_XFORM, 0.f)) != JORGE_OK) return s;
-    if (!c->big.empty()) {
-        TimedLaunch tl(c, ST_FFINAL);
-        hipLaunchKernelGGL(factor_finalize_kernel, dim3((unsigned)c->big.size()), dim3(64), 0, c->stream,
-                           c->dfactors, c->dbig, beta2, (int)c->hp.beta_mode);
-        tl.finish();
-        JORGE_HIP(c, hipGetLastError());
-    }
-    if ((s = launch_gemm<true, false, EPI_POLY>(c, c->poly, ST_POLY, 0.f)) != JORGE_OK) return s;
-    if ((s = launch_gemm<true, false, EPI_SCALE>(c, c->update, ST_UPDATE, 0.f)) != JORGE_OK) return s;
     if (!c->sym_tiles.empty()) {
         TimedLaunch tl(c, ST_SYMM);
         hipLaunchKernelGGL(symmetrize_kernel, dim3((unsigned)c->sym_tiles.size()), dim3(kEwThreads), 0,
@@ -513,30 +757,6 @@ jorge_status run_update(jorge_ctx* c, double beta2) {
         tl.finish();
         JORGE_HIP(c, hipGetLastError());
     }
-    return JORGE_OK;
-}
-
-// Small factors: fork the side stream after stage-in, one chain_kernel launch.
-jorge_status fork_small(jorge_ctx* c, double beta2) {
-    if (c->small.empty()) return JORGE_OK;
-    JORGE_HIP(c, hipEventRecord(c->ev_fork, c->stream));
-    JORGE_HIP(c, hipStreamWaitEvent(c->side, c->ev_fork, 0));
-    TimedLaunch tl(c, ST_CHAIN, c->side);
-    if (c->hp.symmetrize)
-        hipLaunchKernelGGL(chain_kernel<1>, dim3((unsigned)c->small.size()), dim3(kGemmThreads), 0, c->side,
-                           c->dfactors, c->dsmall, beta2, (int)c->hp.beta_mode);
-    else
-        hipLaunchKernelGGL(chain_kernel<0>, dim3((unsigned)c->small.size()), dim3(kGemmThreads), 0, c->side,
-                           c->dfactors, c->dsmall, beta2, (int)c->hp.beta_mode);
-    tl.finish();
-    JORGE_HIP(c, hipGetLastError());
-    JORGE_HIP(c, hipEventRecord(c->ev_join, c->side));
-    return JORGE_OK;
-}
-
-jorge_status join_small(jorge_ctx* c) {
-    if (c->small.empty()) return JORGE_OK;
-    JORGE_HIP(c, hipStreamWaitEvent(c->stream, c->ev_join, 0));
     return JORGE_OK;
 }
 
@@ -573,7 +793,7 @@ jorge_status jorge_hparams_default(jorge_hparams* hp) {
     hp->beta_mode = JORGE_BETA_CLAMPED;
     hp->graft = 1;
     hp->symmetrize = 1;
-    hp->small_factor_max = 0;
+    hp->factor_form = JORGE_FORM_AUTO;
     return JORGE_OK;
 }
 
@@ -581,73 +801,61 @@ jorge_status jorge_create(const jorge_shape* shapes, int32_t num_layers, const j
                           void* hip_stream, jorge_ctx** out) {
     if (!out) return JORGE_ERR_INVALID_ARGUMENT;
     *out = nullptr;
-    if (!shapes || num_layers <= 0) return JORGE_ERR_INVALID_ARGUMENT;
-    if (num_layers > JORGE_MAX_LAYERS) return JORGE_ERR_UNSUPPORTED;
     jorge_hparams h;
-    jorge_hparams_default(&h);
-    if (hp) h = *hp;
-    if (validate_hparams(&h) != JORGE_OK) return JORGE_ERR_INVALID_ARGUMENT;
-    for (int32_t i = 0; i < num_layers; ++i) {
-        if (shapes[i].rows <= 0 || shapes[i].cols <= 0) return JORGE_ERR_INVALID_ARGUMENT;
-        if (shapes[i].rows > JORGE_MAX_DIM || shapes[i].cols > JORGE_MAX_DIM) return JORGE_ERR_UNSUPPORTED;
-    }
+    jorge_status st = validate_args(shapes, num_layers, hp, &h);
+    if (st != JORGE_OK) return st;
     jorge_ctx* c = new (std::nothrow) jorge_ctx();
     if (!c) return JORGE_ERR_OUT_OF_MEMORY;
     c->hp = h;
     c->stream = reinterpret_cast<hipStream_t>(hip_stream);
-    try {
-        c->layers.resize(num_layers);
-        for (int32_t i = 0; i < num_layers; ++i) {
-            LayerHost& L = c->layers[i];
-            L.m = (int)shapes[i].rows;
-            L.n = (int)shapes[i].cols;
-            L.mp = (int)round_up(L.m, 32);
-            L.np = (int)round_up(L.n, 32);
-        }
-        c->arena_bytes = plan(c);
-    } catch (const std::bad_alloc&) {
-        free_ctx(c);
-        return JORGE_ERR_OUT_OF_MEMORY;
-    }
-    jorge_status st = JORGE_OK;
     auto bail = [&](jorge_status s) {
         free_ctx(c);
         return s;
     };
+    if ((st = layout_context(c, shapes, num_layers)) != JORGE_OK) return bail(st);
     if (hipGetDevice(&c->device) != hipSuccess) return bail(JORGE_ERR_HIP);
     hipError_t e = hipMalloc(reinterpret_cast<void**>(&c->arena), c->arena_bytes);
     if (e != hipSuccess) return bail(e == hipErrorOutOfMemory ? JORGE_ERR_OUT_OF_MEMORY : JORGE_ERR_HIP);
     if (hipMemsetAsync(c->arena, 0, c->arena_bytes, c->stream) != hipSuccess) return bail(JORGE_ERR_HIP);
     std::vector<LayerDev> ld;
     std::vector<FactorDev> fd;
-    try {
-        build_tables(c, ld, fd);
-    } catch (const std::bad_alloc&) {
-        return bail(JORGE_ERR_OUT_OF_MEMORY);
-    }
+    if ((st = tables_context(c, ld, fd)) != JORGE_OK) return bail(st);
     if ((st = upload(c, ld, &c->dlayers)) != JORGE_OK) return bail(st);
     if ((st = upload(c, fd, &c->dfactors)) != JORGE_OK) return bail(st);
     if ((st = upload(c, c->stage_tiles, &c->dstage)) != JORGE_OK) return bail(st);
     if ((st = upload(c, c->flat_chunks, &c->dflat)) != JORGE_OK) return bail(st);
     if ((st = upload(c, c->sym_tiles, &c->dsym)) != JORGE_OK) return bail(st);
-    if ((st = upload(c, c->big, &c->dbig)) != JORGE_OK) return bail(st);
-    if ((st = upload(c, c->small, &c->dsmall)) != JORGE_OK) return bail(st);
-    if (!c->small.empty()) {
-        if (hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking) != hipSuccess ||
-            hipEventCreateWithFlags(&c->ev_fork, hipEventDisableTiming) != hipSuccess ||
-            hipEventCreateWithFlags(&c->ev_join, hipEventDisableTiming) != hipSuccess)
-            return bail(JORGE_ERR_HIP);
-    }
-    if (c->hp.symmetrize) merge_stage(c->gram, c->pow2);
-    for (GemmStage* s : {&c->gram, &c->pow2, &c->pow4, &c->xform, &c->poly, &c->update, &c->pre_l,
-                         &c->pre_r})
-        if ((st = upload_stage(c, *s)) != JORGE_OK) return bail(st);
+    for (int i = 0; i < ST_COUNT; ++i)
+        for (GemmStage* s : {&c->nt[i], &c->nn[i]})
+            if ((st = upload_stage(c, *s)) != JORGE_OK) return bail(st);
     hipLaunchKernelGGL(init_factors_kernel, dim3((unsigned)c->factors.size()), dim3(256), 0, c->stream,
                        c->dfactors, (float)std::pow(h.eps, -0.25));
     if (hipGetLastError() != hipSuccess) return bail(JORGE_ERR_HIP);
     if (hipStreamSynchronize(c->stream) != hipSuccess) return bail(JORGE_ERR_HIP);
     *out = c;
     return JORGE_OK;
+}
+
+jorge_status jorge_plan(const jorge_shape* shapes, int32_t num_layers, const jorge_hparams* hp,
+                        int64_t* arena_bytes) {
+    if (!arena_bytes) return JORGE_ERR_INVALID_ARGUMENT;
+    jorge_hparams h;
+    jorge_status st = validate_args(shapes, num_layers, hp, &h);
+    if (st != JORGE_OK) return st;
+    jorge_ctx* c = new (std::nothrow) jorge_ctx();
+    if (!c) return JORGE_ERR_OUT_OF_MEMORY;
+    c->hp = h;
+    std::vector<LayerDev> ld;
+    std::vector<FactorDev> fd;
+    if ((st = layout_context(c, shapes, num_layers)) == JORGE_OK) {
+        // Tables against a stand-in base address: pointers are only compared, never used.
+        c->arena = reinterpret_cast<char*>(uintptr_t(1) << 44);
+        st = tables_context(c, ld, fd);
+        c->arena = nullptr;
+    }
+    if (st == JORGE_OK) *arena_bytes = (int64_t)c->arena_bytes;
+    delete c;
+    return st;
 }
 
 jorge_status jorge_step(jorge_ctx* c, float* const* params, const float* const* grads, double lr,
@@ -673,15 +881,9 @@ jorge_status jorge_step(jorge_ctx* c, float* const* params, const float* const* 
         JORGE_HIP(c, hipGetLastError());
     }
     jorge_status s;
-    if (update) {
-        if ((s = fork_small(c, beta2)) != JORGE_OK) return s;
-        if ((s = run_update(c, beta2)) != JORGE_OK) return s;
-        if ((s = join_small(c)) != JORGE_OK) return s;
-    }
-    if ((s = launch_gemm<true, true, EPI_STORE>(c, c->pre_l, ST_PRECOND_L, 0.f)) != JORGE_OK) return s;
-    s = c->hp.symmetrize ? launch_gemm<true, true, EPI_MOMENTUM>(c, c->pre_r, ST_PRECOND_R, (float)beta1)
-                         : launch_gemm<true, false, EPI_MOMENTUM>(c, c->pre_r, ST_PRECOND_R, (float)beta1);
-    if (s != JORGE_OK) return s;
+    if (update && (s = run_update(c, beta2)) != JORGE_OK) return s;
+    if ((s = launch_stage(c, ST_PRECOND_L, 0.f)) != JORGE_OK) return s;
+    if ((s = launch_stage(c, ST_PRECOND_R, (float)beta1)) != JORGE_OK) return s;
     {
         TimedLaunch tl(c, ST_LFINAL);
         hipLaunchKernelGGL(layer_finalize_kernel, dim3(nl), dim3(64), 0, c->stream, c->dlayers, lr,
@@ -820,6 +1022,20 @@ jorge_status jorge_reset_timing(jorge_ctx* c) {
 }
 
 int32_t jorge_num_stages(void) { return ST_COUNT; }
+
+jorge_status jorge_stage_flops(const jorge_ctx* c, double* flops, int32_t n) {
+    if (!c || !flops || n < 0) return JORGE_ERR_INVALID_ARGUMENT;
+    for (int i = 0; i < std::min<int>(n, ST_COUNT); ++i) flops[i] = c->nt[i].flops + c->nn[i].flops;
+    return JORGE_OK;
+}
+
+jorge_status jorge_factor_form(const jorge_ctx* c, int32_t layer, int32_t side, int32_t* form) {
+    if (!c || !form || layer < 0 || layer >= (int32_t)c->layers.size() || (side != 0 && side != 1))
+        return JORGE_ERR_INVALID_ARGUMENT;
+    const auto& L = c->layers[layer];
+    *form = c->factors[side == 0 ? L.fL : L.fR].expl ? JORGE_FORM_EXPLICIT : JORGE_FORM_FACTORED;
+    return JORGE_OK;
+}
 
 const char* jorge_stage_name(int32_t stage) {
     return (stage >= 0 && stage < ST_COUNT) ? kStageNames[stage] : nullptr;

@@ -1,7 +1,9 @@
 // Grouped fp32 MFMA GEMM for gfx950 with fused epilogues.
 //
-// One launch covers every tile of a list of independent products (all layers'
-// factors of one stage of the step). A workgroup of 256 threads computes one
+// One launch covers every tile of a list of independent products (all
+// factors' products of one dependency level of the step). Each product
+// carries its own epilogue (flags and coefficient set, decided at run time
+// per problem), so products with different epilogues share a launch. A workgroup of 256 threads computes one
 // 128 x 128 tile of C = A * B; its four waves each own a 64 x 64 sub-tile held
 // as 2 x 2 blocks of v_mfma_f32_32x32x2_f32 accumulators. K is consumed in
 // slabs of 32 staged through double-buffered LDS: while the waves run the
@@ -135,13 +137,32 @@ struct GemmLds {
     float op[2][2][kLdsOperand];
 };
 
+// Operand base pointer, leading dimension and local k of one slab: the
+// second K segment (k >= K1) reads A2 / B2.
+struct SlabSrc {
+    const float* a;
+    const float* b;
+    int lda, ldb, k;
+};
+
+__device__ __forceinline__ SlabSrc slab_src(const GemmProblem& p, int k0) {
+    if (k0 < p.K1) return {p.A, p.B, p.lda, p.ldb, k0};
+    return {p.A2, p.B2, p.lda2, p.ldb2, k0 - p.K1};
+}
+
 // One 128 x 128 tile (tm, tn) of problem p computed by the whole workgroup,
-// followed by the epilogue EPI. a, b, sf are the polynomial coefficients and
-// the scale of EPI_POLY / EPI_SCALE; beta1 is the momentum of EPI_MOMENTUM.
+// followed by the problem's epilogue; beta1 is the momentum of EF_MOMENTUM.
 // Every thread of the workgroup must call it; it leaves LDS free for reuse.
-template <bool AK, bool BK, int EPI>
+//
+// Symmetric results (p.upper): only tiles with tm <= tn are computed. An
+// element (row, col) with row <= col is written at (row, col) and at
+// (col, row), elements below the diagonal of a diagonal tile are skipped,
+// so the stored matrix is bitwise symmetric whatever the product's rounding.
+// The epilogue reads X only at the positions it is about to write, by the
+// same thread, so X may alias C (an in-place update).
+template <bool AK, bool BK>
 __device__ __forceinline__ void gemm_tile(const GemmProblem& p, int tm, int tn, int slot, float beta1,
-                                          float a, float b, float sf, GemmLds& sm, double* red) {
+                                          GemmLds& sm, double* red) {
     const int row0 = tm * kTile, col0 = tn * kTile;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int wy = wave >> 1, wx = wave & 1;
@@ -156,8 +177,11 @@ __device__ __forceinline__ void gemm_tile(const GemmProblem& p, int tm, int tn, 
 
     f32x4 ra[4], rb[4];
     const int nk = p.K / kSlab;
-    load_slab<AK>(p.A, p.lda, row0, p.M, 0, ra);
-    load_slab<BK>(p.B, p.ldb, col0, p.N, 0, rb);
+    {
+        const SlabSrc s0 = slab_src(p, 0);
+        load_slab<AK>(s0.a, s0.lda, row0, p.M, s0.k, ra);
+        load_slab<BK>(s0.b, s0.ldb, col0, p.N, s0.k, rb);
+    }
     store_slab<AK>(sm.op[0][0], ra);
     store_slab<BK>(sm.op[0][1], rb);
     __syncthreads();
@@ -165,8 +189,9 @@ __device__ __forceinline__ void gemm_tile(const GemmProblem& p, int tm, int tn, 
         const int cur = kt & 1;
         const bool more = kt + 1 < nk;
         if (more) {
-            load_slab<AK>(p.A, p.lda, row0, p.M, (kt + 1) * kSlab, ra);
-            load_slab<BK>(p.B, p.ldb, col0, p.N, (kt + 1) * kSlab, rb);
+            const SlabSrc sn = slab_src(p, (kt + 1) * kSlab);
+            load_slab<AK>(sn.a, sn.lda, row0, p.M, sn.k, ra);
+            load_slab<BK>(sn.b, sn.ldb, col0, p.N, sn.k, rb);
         }
         // Raised issue priority while this wave runs its MFMAs: the two waves
         // sharing a SIMD then alternate between MFMA and memory phases.
@@ -182,6 +207,21 @@ __device__ __forceinline__ void gemm_tile(const GemmProblem& p, int tm, int tn, 
 
     // Epilogue. Accumulator register e of block (i, j) holds
     // C[row0 + wy*64 + i*32 + 8*(e/4) + 4*(lane/32) + e%4][col0 + wx*64 + j*32 + lane%32].
+    const int flags = p.flags;
+    const bool upper = p.upper != 0;
+    const bool diag = upper && tm == tn;
+    float ci = 0.f, cx = 0.f, cc = 1.f;
+    if (p.coef != CO_ONE) {
+        const FactorScalars* s = p.sc;
+        switch (p.coef) {
+            case CO_POLY: ci = 1.f; cx = -s->a; cc = s->b; break;
+            case CO_SCALE: cc = s->sf; break;
+            case CO_WMIX: cx = s->a; cc = -s->b; break;
+            case CO_SYR2K: cx = s->sf; cc = -0.5f * s->sf; break;
+            case CO_LITUPD: cx = s->sf; cc = -s->sf; break;
+            default: break;
+        }
+    }
     const int h = lane >> 5;
     double part = 0.0;
 #pragma unroll
@@ -192,42 +232,53 @@ __device__ __forceinline__ void gemm_tile(const GemmProblem& p, int tm, int tn, 
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
                 const int rowb = row0 + wy * 64 + i * 32 + q * 8 + h * 4;
-                if constexpr (EPI == EPI_SYM) {
-                    if (col < p.N && rowb < p.M && tm != tn) {
-                        f32x4 v;
-                        v[0] = acc[i][j][q * 4 + 0]; v[1] = acc[i][j][q * 4 + 1];
-                        v[2] = acc[i][j][q * 4 + 2]; v[3] = acc[i][j][q * 4 + 3];
-                        *reinterpret_cast<f32x4*>(p.C + (size_t)col * p.ldc + rowb) = v;
+                if (flags & EF_MOMENTUM) {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int row = rowb + e;
+                        if (row < p.valid_m && col < p.valid_n) {
+                            float* mp = p.mom + (size_t)row * p.ldmom + col;
+                            const float mn = beta1 * *mp + (1.0f - beta1) * acc[i][j][q * 4 + e];
+                            *mp = mn;
+                            part += (double)mn * (double)mn;
+                        }
                     }
+                    continue;
                 }
+                // rowb .. rowb+3 are all inside M when rowb is (M is a multiple of 4).
+                if (rowb >= p.M || col >= p.N) continue;
+                f32x4 out;
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     const int row = rowb + e;
                     const float v = acc[i][j][q * 4 + e];
-                    if constexpr (EPI == EPI_MOMENTUM) {
-                        if (row < p.valid_m && col < p.valid_n) {
-                            float* mp = p.mom + (size_t)row * p.ldmom + col;
-                            const float mn = beta1 * *mp + (1.0f - beta1) * v;
-                            *mp = mn;
-                            part += (double)mn * (double)mn;
-                        }
-                    } else {
-                        if (row < p.M && col < p.N) {
-                            float out = v;
-                            if constexpr (EPI == EPI_NORM) part += (double)v * (double)v;
-                            if constexpr (EPI == EPI_POLY) {
-                                const float x = *(global_f32*)(p.X + (size_t)row * p.ldx + col);
-                                const float id = (row == col && row < p.valid_m) ? 1.0f : 0.0f;
-                                out = id - a * x + b * v;
-                            }
-                            if constexpr (EPI == EPI_SCALE) out = sf * v;
-                            p.C[(size_t)row * p.ldc + col] = out;
-                        }
+                    out[e] = 0.f;
+                    if (upper && row > col) continue;   // lower half of a diagonal tile
+                    float o = cc * v;
+                    if (flags & EF_READX) {
+                        const float x = *(global_f32*)(p.X + (size_t)row * p.ldx + col);
+                        const float id = (row == col && row < p.valid_m) ? ci : 0.0f;
+                        o = (id + cx * x) + o;
+                    }
+                    out[e] = o;
+                    const double w = (upper && row != col) ? 2.0 : 1.0;
+                    if (flags & EF_NORM) part += w * (double)o * (double)o;
+                    if (flags & EF_DOT)
+                        part += w * (double)v * (double)*(global_f32*)(p.X + (size_t)row * p.ldx + col);
+                    if ((flags & EF_STORE) && diag) {
+                        p.C[(size_t)row * p.ldc + col] = o;
+                        if (row != col) p.C[(size_t)col * p.ldc + row] = o;
                     }
                 }
+                if ((flags & EF_STORE) && !diag) {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) p.C[(size_t)(rowb + e) * p.ldc + col] = out[e];
+                    if (upper) *reinterpret_cast<f32x4*>(p.C + (size_t)col * p.ldc + rowb) = out;
+                }
+                if (flags & EF_STORE_T) *reinterpret_cast<f32x4*>(p.C2 + (size_t)col * p.ldc2 + rowb) = out;
             }
         }
-    if constexpr (EPI == EPI_NORM || EPI == EPI_MOMENTUM) {
+    if (flags & (EF_NORM | EF_DOT | EF_MOMENTUM)) {
         const double total = block_sum_256(part, red);
         if (threadIdx.x == 0) p.partials[slot] = total;
     }
@@ -237,7 +288,7 @@ __device__ __forceinline__ void gemm_tile(const GemmProblem& p, int tm, int tn, 
 // dispatch order: consecutive workgroups go round-robin to the 8 XCDs, and the
 // host arranged the list so each XCD's share is balanced and reuses operand
 // panels in its own L2.
-template <bool AK, bool BK, int EPI>
+template <bool AK, bool BK>
 __global__ __launch_bounds__(kGemmThreads, 2) void gemm_grouped(const GemmProblem* __restrict__ probs,
                                                                 const TileDesc* __restrict__ tiles,
                                                                 float beta1) {
@@ -245,10 +296,7 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_grouped(const GemmProble
     __shared__ double red[4];
     const TileDesc td = tiles[blockIdx.x];
     const GemmProblem p = probs[td.prob];
-    float a = 0.f, b = 0.f, sf = 0.f;
-    if constexpr (EPI == EPI_POLY) { a = p.sc->a; b = p.sc->b; }
-    if constexpr (EPI == EPI_SCALE) sf = p.sc->sf;
-    gemm_tile<AK, BK, EPI>(p, td.tm, td.tn, td.slot, beta1, a, b, sf, sm, red);
+    gemm_tile<AK, BK>(p, td.tm, td.tn, td.slot, beta1, sm, red);
 }
 
 }  // namespace jorge

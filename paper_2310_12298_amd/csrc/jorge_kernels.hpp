@@ -93,16 +93,17 @@ __device__ __forceinline__ FactorScalars factor_scalars(double nu, double beta2,
 }
 
 // nu = ||X||_F from the per-tile partial sums, then the factor's scalars.
-// One wave per factor of the list.
-__global__ void factor_finalize_kernel(const FactorDev* __restrict__ f, const int* __restrict__ list,
-                                       double beta2, int mode) {
-    const FactorDev F = f[list[blockIdx.x]];
-    const double nu = sqrt(wave_sum_array(F.partials, F.nparts));
+// One wave per factor. The factored form's partials are terms of an inner
+// product of two positive semidefinite matrices whose exact sum is ||X||_F^2;
+// a sum that rounding left below zero is read as zero.
+__global__ void factor_finalize_kernel(const FactorDev* __restrict__ f, double beta2, int mode) {
+    const FactorDev F = f[blockIdx.x];
+    const double nu = sqrt(fmax(0.0, wave_sum_array(F.partials, F.nparts)));
     if (threadIdx.x == 0) *F.sc = factor_scalars(nu, beta2, mode);
 }
 
 // A_hat <- (Z + Z^T)/2 (or Z when not symmetrizing) for the pair of 64 x 64
-// tiles (ti, tj), (tj, ti), Z being in W0. fp32 addition commutes, so the
+// tiles (ti, tj), (tj, ti) of a factor in the explicit form. fp32 addition commutes, so the
 // result is bitwise symmetric. za, zb: 64 x 65 floats of LDS each. All threads
 // of the workgroup call it; it ends with a barrier so the LDS can be reused.
 __device__ __forceinline__ void symmetrize_pair(const FactorDev& F, int ti, int tj, int symmetrize,
@@ -114,11 +115,11 @@ __device__ __forceinline__ void symmetrize_pair(const FactorDev& F, int ti, int 
     for (int q = 0; q < 4; ++q) {
         const int u = tid + q * kEwThreads, r = u >> 4, c = (u & 15) * 4;
         if (i0 + r < dp && j0 + c < dp) {
-            const f32x4 v = *reinterpret_cast<const f32x4*>(F.W0 + (size_t)(i0 + r) * dp + j0 + c);
+            const f32x4 v = *reinterpret_cast<const f32x4*>(F.Z + (size_t)(i0 + r) * dp + j0 + c);
             za[r][c] = v[0]; za[r][c + 1] = v[1]; za[r][c + 2] = v[2]; za[r][c + 3] = v[3];
         }
         if (j0 + r < dp && i0 + c < dp) {
-            const f32x4 v = *reinterpret_cast<const f32x4*>(F.W0 + (size_t)(j0 + r) * dp + i0 + c);
+            const f32x4 v = *reinterpret_cast<const f32x4*>(F.Z + (size_t)(j0 + r) * dp + i0 + c);
             zb[r][c] = v[0]; zb[r][c + 1] = v[1]; zb[r][c + 2] = v[2]; zb[r][c + 3] = v[3];
         }
     }
@@ -151,94 +152,6 @@ __global__ __launch_bounds__(kEwThreads) void symmetrize_kernel(const FactorDev*
     __shared__ float zb[64][65];
     const SymTile st = tiles[blockIdx.x];
     symmetrize_pair(f[st.factor], st.ti, st.tj, symmetrize, za, zb);
-}
-
-// The whole update of one small factor by one workgroup (Algorithm 2 with
-// Appendix A.1): Gram statistic, A^2, A^4, X = A^4 M with ||X||_F, (c, s),
-// P = I - (c/4) X + (5c^2/32) X X, Z = s A P, and A <- (Z + Z^T)/2. The stages
-// are separated by workgroup barriers instead of kernel launches. Each product
-// uses the grouped launches' tile routine, tile decomposition, K order and
-// partial-sum slots, so a factor gets bitwise the same result on either path.
-// Intermediates live in the factor's workspace, which stays in L2.
-template <int SYMM>
-__global__ __launch_bounds__(kGemmThreads, 2) void chain_kernel(const FactorDev* __restrict__ f,
-                                                                const int* __restrict__ list,
-                                                                double beta2, int mode) {
-    __shared__ __attribute__((aligned(16))) GemmLds sm;
-    __shared__ double red[4];
-    __shared__ float scal[3];
-    const FactorDev F = f[list[blockIdx.x]];
-    const int dp = F.dp, nt = (dp + kTile - 1) / kTile;
-    GemmProblem g{};
-    g.M = g.N = g.K = dp;
-    g.lda = g.ldb = g.ldc = g.ldx = dp;
-    g.valid_m = g.valid_n = F.d;
-
-    GemmProblem s = g;                                   // Gram statistic -> W0
-    s.A = s.B = F.gop;
-    s.K = s.lda = s.ldb = F.gk;
-    s.C = F.W0;
-    for (int tm = 0; tm < nt; ++tm)
-        for (int tn = tm; tn < nt; ++tn) gemm_tile<true, true, EPI_SYM>(s, tm, tn, 0, 0.f, 0.f, 0.f, 0.f, sm, red);
-    __syncthreads();
-    GemmProblem p2 = g;                                  // A^2 -> W1
-    p2.A = p2.B = F.A;
-    p2.C = F.W1;
-    GemmProblem p4 = g;                                  // A^4 -> W2
-    p4.A = p4.B = F.W1;
-    p4.C = F.W2;
-    if constexpr (SYMM) {
-        for (int tm = 0; tm < nt; ++tm)
-            for (int tn = tm; tn < nt; ++tn) gemm_tile<true, true, EPI_SYM>(p2, tm, tn, 0, 0.f, 0.f, 0.f, 0.f, sm, red);
-        __syncthreads();
-        for (int tm = 0; tm < nt; ++tm)
-            for (int tn = tm; tn < nt; ++tn) gemm_tile<true, true, EPI_SYM>(p4, tm, tn, 0, 0.f, 0.f, 0.f, 0.f, sm, red);
-    } else {
-        for (int tn = 0; tn < nt; ++tn)
-            for (int tm = 0; tm < nt; ++tm) gemm_tile<true, false, EPI_STORE>(p2, tm, tn, 0, 0.f, 0.f, 0.f, 0.f, sm, red);
-        __syncthreads();
-        for (int tn = 0; tn < nt; ++tn)
-            for (int tm = 0; tm < nt; ++tm) gemm_tile<true, false, EPI_STORE>(p4, tm, tn, 0, 0.f, 0.f, 0.f, 0.f, sm, red);
-    }
-    __syncthreads();
-    GemmProblem px = g;                                  // X = A^4 M -> W1, ||X||^2 partials
-    px.A = F.W2;
-    px.B = F.W0;
-    px.C = F.W1;
-    px.partials = F.partials;
-    // Slots follow the grouped tile order (column by column within bands of 8 tile rows).
-    for (int tn = 0, slot = 0; tn < nt; ++tn)
-        for (int tm = 0; tm < nt; ++tm, ++slot)
-            gemm_tile<true, true, EPI_NORM>(px, tm, tn, slot, 0.f, 0.f, 0.f, 0.f, sm, red);
-    __syncthreads();
-    if (threadIdx.x < 64) {
-        const double nu = sqrt(wave_sum_array(F.partials, F.nparts));
-        if (threadIdx.x == 0) {
-            const FactorScalars fs = factor_scalars(nu, beta2, mode);
-            *F.sc = fs;
-            scal[0] = fs.a;
-            scal[1] = fs.b;
-            scal[2] = fs.sf;
-        }
-    }
-    __syncthreads();
-    GemmProblem pp = g;                                  // P = I - a X + b X X -> W2
-    pp.A = pp.B = pp.X = F.W1;
-    pp.C = F.W2;
-    for (int tn = 0; tn < nt; ++tn)
-        for (int tm = 0; tm < nt; ++tm) gemm_tile<true, false, EPI_POLY>(pp, tm, tn, 0, 0.f, scal[0], scal[1], 0.f, sm, red);
-    __syncthreads();
-    GemmProblem pu = g;                                  // Z = s A P -> W0
-    pu.A = F.A;
-    pu.B = F.W2;
-    pu.C = F.W0;
-    for (int tn = 0; tn < nt; ++tn)
-        for (int tm = 0; tm < nt; ++tm) gemm_tile<true, false, EPI_SCALE>(pu, tm, tn, 0, 0.f, 0.f, 0.f, scal[2], sm, red);
-    __syncthreads();
-    float (*za)[65] = reinterpret_cast<float (*)[65]>(&sm.op[0][0][0]);
-    float (*zb)[65] = za + 64;
-    for (int ti = 0; ti * 64 < dp; ++ti)
-        for (int tj = ti; tj * 64 < dp; ++tj) symmetrize_pair(F, ti, tj, SYMM, za, zb);
 }
 
 // Per-layer norms of m and m_SGD from their partial sums, and the grafted

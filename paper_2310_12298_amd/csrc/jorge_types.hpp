@@ -5,14 +5,26 @@
 
 namespace jorge {
 
-// Epilogues of the grouped GEMM (what is done with C = A * B of one tile).
-enum Epilogue : int {
-    EPI_STORE = 0,     // C
-    EPI_SYM = 1,       // C and its mirror C^T (upper tiles of a symmetric product only)
-    EPI_NORM = 2,      // C, plus the tile's sum of C_ij^2 (for ||X||_F)
-    EPI_POLY = 3,      // I - a X + b C with C = X X  (truncated series of Eq. 6)
-    EPI_SCALE = 4,     // s C                          (s A_hat P)
-    EPI_MOMENTUM = 5,  // m = beta1 m + (1-beta1) C, plus the tile's sum of m_ij^2
+// What the epilogue of a grouped GEMM does with one tile of the product
+// (bit flags, combined per problem).
+enum EpiFlags : int {
+    EF_STORE = 1,      // write the value to C (row-major)
+    EF_STORE_T = 2,    // write the value transposed to C2 (C2[col][row])
+    EF_NORM = 4,       // add the tile's sum of value^2 to the partial-sum slot
+    EF_DOT = 8,        // add the tile's sum of acc * X[row][col] (weighted for symmetric halves)
+    EF_MOMENTUM = 16,  // m = beta1 m + (1 - beta1) acc on the dense momentum, plus sum of m^2
+    EF_READX = 32,     // the value reads X[row][col] (coefficient cx below)
+};
+
+// Coefficient sets: value = ci [row == col < valid_m] + cx X[row][col] + cc acc,
+// with (a, b, s) = (c/4, 5c^2/32, beta^(-1/4)) of the factor being updated.
+enum Coef : int {
+    CO_ONE = 0,     // (0, 0, 1)          plain product
+    CO_POLY = 1,    // (1, -a, b)         P = I - (c/4) X + (5c^2/32) X X      (Eq. 6)
+    CO_SCALE = 2,   // (0, 0, s)          Z = s A P
+    CO_WMIX = 3,    // (0, a, -b)         W = A^5 H (a I - b S)
+    CO_SYR2K = 4,   // (0, s, -s/2)       A <- s A - (s/2) (W H^T + H W^T)
+    CO_LITUPD = 5,  // (0, s, -s)         A <- s A - s W H^T
 };
 
 // Scalars of one factor update, written on the device by the finalize kernel.
@@ -36,21 +48,32 @@ struct LayerScalars {
     float decay;      // 1 - lr * weight_decay as fp32
 };
 
-// One product C = A * B of a grouped launch. Operand layouts are fixed per
-// kernel instantiation: a "K-major" operand has K contiguous (A row-major,
-// or B stored as B^T row-major), an "MN-major" one has M (N) contiguous.
-// M, N, K are the padded extents (K a multiple of 32, ld's multiples of 4).
+// One product of a grouped launch. With both operands K-major (the "NT"
+// kernel) the product is C = A B^T: A is M x K row-major, B is N x K
+// row-major. With B MN-major (the "NN" kernel) B is K x N row-major.
+// K may consist of two segments: slabs with k >= K1 read A2 and B2 (at
+// k - K1) instead of A and B, which forms sums such as W H^T + H W^T in one
+// accumulation. M, N, K, K1 are padded extents (K and K1 multiples of 32,
+// leading dimensions multiples of 4).
 struct GemmProblem {
     const float* A;
     const float* B;
+    const float* A2;
+    const float* B2;
     float* C;
-    const float* X;            // EPI_POLY: the X of the polynomial
-    const FactorScalars* sc;   // EPI_POLY, EPI_SCALE
-    float* mom;                // EPI_MOMENTUM: dense valid_m x valid_n momentum
-    double* partials;          // EPI_NORM, EPI_MOMENTUM: one double per tile slot
-    int M, N, K;
-    int lda, ldb, ldc, ldx, ldmom;
+    float* C2;                 // EF_STORE_T destination
+    const float* X;            // EF_READX / EF_DOT operand
+    const FactorScalars* sc;   // coefficients (any Coef but CO_ONE)
+    float* mom;                // EF_MOMENTUM: dense valid_m x valid_n momentum
+    double* partials;          // EF_NORM, EF_DOT, EF_MOMENTUM: one double per tile slot
+    int M, N, K, K1;
+    int lda, ldb, lda2, ldb2;
+    int ldc, ldc2, ldx, ldmom;
     int valid_m, valid_n;      // unpadded extent (identity / momentum masks)
+    int flags;                 // EpiFlags
+    int coef;                  // Coef
+    int upper;                 // 1: symmetric result, only tiles tm <= tn are computed
+                               //    and each is written with its mirror image
     int pad0;
 };
 
@@ -64,15 +87,12 @@ struct TileDesc {
 // Device view of a factor (L_hat or R_hat of one layer).
 struct FactorDev {
     float* A;              // state, dp x dp, ld = dp, zero outside the d x d block
-    float* W0;             // workspace: statistic M, later Z
-    float* W1;             // workspace: A^2, later X
-    float* W2;             // workspace: A^4, later P
     FactorScalars* sc;
-    double* partials;      // per-tile sums of X_ij^2
-    const float* gop;      // Gram operand with K contiguous: Gp (L side) or Gpt (R side)
-    int gk;                // its K (np or mp), also its row stride
+    double* partials;      // per-tile partial sums of ||X||_F^2
+    float* Z;              // explicit form: the unsymmetrized product s A P (dp x dp)
     int d, dp;
     int nparts;
+    int explicit_form;     // 1: explicit powers; 0: factored through the statistic's factor
 };
 
 // Device view of a layer.

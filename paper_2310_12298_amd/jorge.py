@@ -16,6 +16,7 @@ LIB_PATH = os.path.join(PKG, "libjorge.so")
 JORGE_OK = 0
 BETA_MODES = {"fixed": 0, "dynamic": 1, "clamped": 2}
 STATE_KINDS = {"L": 0, "R": 1, "mom": 2, "mom_sgd": 3}
+FACTOR_FORMS = {"auto": 0, "explicit": 1, "factored": 2}
 DIAG_NAMES = ("nu_L", "nu_R", "beta_L", "beta_R", "norm_m", "norm_sgd", "g")
 
 
@@ -32,7 +33,7 @@ class Shape(ctypes.Structure):
 class HParams(ctypes.Structure):
     _fields_ = [("eps", ctypes.c_double), ("precond_interval", ctypes.c_int32),
                 ("beta_mode", ctypes.c_int32), ("graft", ctypes.c_int32),
-                ("symmetrize", ctypes.c_int32), ("small_factor_max", ctypes.c_int32)]
+                ("symmetrize", ctypes.c_int32), ("factor_form", ctypes.c_int32)]
 
 
 _LIB = None
@@ -43,6 +44,8 @@ _SIGNATURES = {
     "jorge_hparams_default": (ctypes.c_int32, [ctypes.POINTER(HParams)]),
     "jorge_create": (ctypes.c_int32, [ctypes.POINTER(Shape), ctypes.c_int32, ctypes.POINTER(HParams), _P,
                                       ctypes.POINTER(_P)]),
+    "jorge_plan": (ctypes.c_int32, [ctypes.POINTER(Shape), ctypes.c_int32, ctypes.POINTER(HParams),
+                                    ctypes.POINTER(ctypes.c_int64)]),
     "jorge_step": (ctypes.c_int32, [_P, ctypes.POINTER(_P), ctypes.POINTER(_P), ctypes.c_double,
                                     ctypes.c_double, ctypes.c_double, ctypes.c_double]),
     "jorge_get_state": (ctypes.c_int32, [_P, ctypes.c_int32, ctypes.c_int32, _P, ctypes.c_int64]),
@@ -60,6 +63,8 @@ _SIGNATURES = {
                                            ctypes.POINTER(ctypes.c_int64), ctypes.c_int32]),
     "jorge_reset_timing": (ctypes.c_int32, [_P]),
     "jorge_num_stages": (ctypes.c_int32, []),
+    "jorge_stage_flops": (ctypes.c_int32, [_P, ctypes.POINTER(ctypes.c_double), ctypes.c_int32]),
+    "jorge_factor_form": (ctypes.c_int32, [_P, ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(ctypes.c_int32)]),
     "jorge_stage_name": (ctypes.c_char_p, [ctypes.c_int32]),
     "jorge_destroy": (None, [_P]),
     "jorge_status_string": (ctypes.c_char_p, [ctypes.c_int32]),
@@ -106,24 +111,41 @@ class Jorge:
     """
 
     def __init__(self, shapes, eps=1e-6, precond_interval=1, beta_mode="clamped", graft=True,
-                 symmetrize=True, small_factor_max=None, stream=None):
+                 symmetrize=True, factor_form="auto", stream=None):
         self.lib = load_library()
         self.shapes = [(int(m), int(n)) for m, n in shapes]
-        hp = HParams()
-        _check(self.lib, self.lib.jorge_hparams_default(ctypes.byref(hp)))
-        hp.eps = float(eps)
-        hp.precond_interval = int(precond_interval)
-        hp.beta_mode = BETA_MODES[beta_mode] if isinstance(beta_mode, str) else int(beta_mode)
-        hp.graft = int(bool(graft))
-        hp.symmetrize = int(bool(symmetrize))
-        if small_factor_max is not None:
-            hp.small_factor_max = int(small_factor_max)
+        hp = self.hparams(eps, precond_interval, beta_mode, graft, symmetrize, factor_form)
         arr = (Shape * len(self.shapes))(*[Shape(m, n) for m, n in self.shapes])
         ctx = _P()
         s = _current_stream() if stream is None else int(stream)
         _check(self.lib, self.lib.jorge_create(arr, len(self.shapes), ctypes.byref(hp), _P(s),
                                                ctypes.byref(ctx)))
         self.ctx = ctx
+
+    @staticmethod
+    def hparams(eps=1e-6, precond_interval=1, beta_mode="clamped", graft=True, symmetrize=True,
+                factor_form="auto"):
+        lib = load_library()
+        hp = HParams()
+        _check(lib, lib.jorge_hparams_default(ctypes.byref(hp)))
+        hp.eps = float(eps)
+        hp.precond_interval = int(precond_interval)
+        hp.beta_mode = BETA_MODES[beta_mode] if isinstance(beta_mode, str) else int(beta_mode)
+        hp.graft = int(bool(graft))
+        hp.symmetrize = int(bool(symmetrize))
+        hp.factor_form = FACTOR_FORMS[factor_form] if isinstance(factor_form, str) else int(factor_form)
+        return hp
+
+    @staticmethod
+    def plan(shapes, **hp):
+        """Device bytes a context would hold; builds and checks its launch tables on the host (no GPU)."""
+        lib = load_library()
+        shapes = [(int(m), int(n)) for m, n in shapes]
+        arr = (Shape * max(1, len(shapes)))(*[Shape(m, n) for m, n in shapes])
+        h = Jorge.hparams(**hp)
+        v = ctypes.c_int64()
+        _check(lib, lib.jorge_plan(arr, len(shapes), ctypes.byref(h), ctypes.byref(v)))
+        return v.value
 
     # -------------------------------------------------------------- stepping
     def _ptrs(self, tensors, what):
@@ -209,6 +231,12 @@ class Jorge:
         _check(self.lib, self.lib.jorge_device_bytes(self.ctx, ctypes.byref(v)))
         return v.value
 
+    def factor_form(self, layer, side):
+        """'explicit' or 'factored': the evaluation order of L_hat (side 0) or R_hat (side 1)."""
+        v = ctypes.c_int32()
+        _check(self.lib, self.lib.jorge_factor_form(self.ctx, int(layer), int(side), ctypes.byref(v)), self.ctx)
+        return {1: "explicit", 2: "factored"}[v.value]
+
     # -------------------------------------------------------------- timing
     def set_timing(self, enable: bool):
         _check(self.lib, self.lib.jorge_set_timing(self.ctx, int(bool(enable))), self.ctx)
@@ -223,6 +251,13 @@ class Jorge:
         cnt = (ctypes.c_int64 * n)()
         _check(self.lib, self.lib.jorge_read_timing(self.ctx, ms, cnt, n), self.ctx)
         return {self.lib.jorge_stage_name(i).decode(): (ms[i], cnt[i]) for i in range(n)}
+
+    def stage_flops(self):
+        """{stage name: algorithmic flops of that stage in one factor-updating step}."""
+        n = self.lib.jorge_num_stages()
+        fl = (ctypes.c_double * n)()
+        _check(self.lib, self.lib.jorge_stage_flops(self.ctx, fl, n), self.ctx)
+        return {self.lib.jorge_stage_name(i).decode(): fl[i] for i in range(n)}
 
     # -------------------------------------------------------------- lifetime
     def close(self):

@@ -46,7 +46,7 @@ def test_hparams_default(lib):
     hp = J.HParams()
     assert lib.jorge_hparams_default(ctypes.byref(hp)) == 0
     assert (hp.eps, hp.precond_interval, hp.beta_mode, hp.graft, hp.symmetrize,
-            hp.small_factor_max) == (1e-6, 1, 2, 1, 1, 0)
+            hp.factor_form) == (1e-6, 1, 2, 1, 1, 0)
     assert lib.jorge_hparams_default(None) == ERR_INVALID
 
 
@@ -71,8 +71,8 @@ def test_create_rejects_oversize(lib):
 @pytest.mark.parametrize("field,value", [("eps", 0.0), ("eps", -1.0), ("eps", float("inf")),
                                          ("eps", float("nan")), ("precond_interval", 0),
                                          ("beta_mode", 3), ("beta_mode", -1), ("graft", 2),
-                                         ("symmetrize", -1), ("small_factor_max", -1),
-                                         ("small_factor_max", 4097)])
+                                         ("symmetrize", -1), ("factor_form", -1),
+                                         ("factor_form", 3)])
 def test_create_rejects_bad_hparams(lib, field, value):
     hp = J.HParams()
     lib.jorge_hparams_default(ctypes.byref(hp))
@@ -100,6 +100,10 @@ def test_null_arguments(lib):
     assert lib.jorge_set_timing(None, 1) == ERR_INVALID
     assert lib.jorge_read_timing(None, None, None, 0) == ERR_INVALID
     assert lib.jorge_reset_timing(None) == ERR_INVALID
+    assert lib.jorge_stage_flops(None, (ctypes.c_double * 1)(), 1) == ERR_INVALID
+    assert lib.jorge_factor_form(None, 0, 0, ctypes.byref(ctypes.c_int32())) == ERR_INVALID
+    assert lib.jorge_plan(shp, 1, None, None) == ERR_INVALID
+    assert lib.jorge_plan(None, 1, None, ctypes.byref(ctypes.c_int64())) == ERR_INVALID
     lib.jorge_destroy(None)
     assert lib.jorge_last_error(None) == b""
 
@@ -119,3 +123,51 @@ def test_binding_fails_loudly_without_library(tmp_path, monkeypatch):
     monkeypatch.setattr(J, "_LIB", None)
     with pytest.raises(FileNotFoundError):
         J.load_library(str(tmp_path / "missing.so"))
+
+
+# ---------------------------------------------------------------- host-side plan checks
+# jorge_plan builds every launch table exactly as jorge_create does and checks,
+# on the host, that each access of each grouped launch stays inside its buffer
+# with the alignment and extents the kernels assume. These run without a GPU.
+
+from paper_2310_12298_amd.workloads import CONFIGS  # noqa: E402
+
+FORMS = ("auto", "explicit", "factored")
+
+
+@pytest.mark.parametrize("name", sorted(CONFIGS))
+@pytest.mark.parametrize("symmetrize", [True, False])
+def test_plan_tables_of_every_workload(lib, name, symmetrize):
+    shapes = CONFIGS[name][0]
+    sizes = {f: J.Jorge.plan(shapes, symmetrize=symmetrize, factor_form=f) for f in FORMS}
+    assert all(v > 0 for v in sizes.values())
+    # Per factor, auto takes one of the two forms' workspaces.
+    assert sizes["auto"] <= max(sizes["explicit"], sizes["factored"])
+
+
+@pytest.mark.parametrize("form", FORMS)
+@pytest.mark.parametrize("symmetrize", [True, False])
+def test_plan_tables_of_edge_shapes(lib, form, symmetrize):
+    shapes = [(1, 1), (1, 40), (40, 1), (33, 65), (5, 3), (127, 129), (128, 128), (129, 4000),
+              (4000, 129), (32, 32), (300, 200), (1, 4608)]
+    assert J.Jorge.plan(shapes, symmetrize=symmetrize, factor_form=form) > 0
+    for s in shapes:
+        assert J.Jorge.plan([s], symmetrize=symmetrize, factor_form=form) > 0
+
+
+def test_plan_tables_of_random_shapes(lib):
+    import numpy as np
+    rng = np.random.default_rng(11)
+    for _ in range(40):
+        shapes = [tuple(int(x) for x in rng.integers(1, 700, size=2)) for _ in range(int(rng.integers(1, 6)))]
+        for form in FORMS:
+            assert J.Jorge.plan(shapes, factor_form=form) > 0, shapes
+
+
+def test_plan_rejects_what_create_rejects(lib):
+    with pytest.raises(J.JorgeError):
+        J.Jorge.plan([(4, 0)])
+    with pytest.raises(J.JorgeError):
+        J.Jorge.plan([(4, 32769)])
+    with pytest.raises(J.JorgeError):
+        J.Jorge.plan([(4, 4)], factor_form=7)

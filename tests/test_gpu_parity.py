@@ -20,6 +20,9 @@ pytestmark = pytest.mark.gpu
 
 STEP_TOL = 1e-5
 TRAJ_TOL = 1e-3
+# Evaluation orders of the factor update: the paper's explicit powers, the
+# factored order through the statistic's factor H, and the per-factor choice.
+FORMS = ("explicit", "factored", "auto")
 HP = dict(lr=0.1, beta2=0.9, beta1=0.9, weight_decay=5e-5)
 KINDS = ("L", "R", "mom", "mom_sgd")
 
@@ -79,6 +82,7 @@ def run_pair(shapes, steps, sigma, seed=0, check_every=None, tol=TRAJ_TOL, gpu_k
     return opt, orc, pg, po, worst
 
 
+@pytest.mark.parametrize("form", FORMS)
 @pytest.mark.parametrize("shapes", [
     [(64, 576)],                       # 3x3 conv 64 -> 64
     [(64, 147)],                       # ragged stem
@@ -88,25 +92,28 @@ def run_pair(shapes, steps, sigma, seed=0, check_every=None, tol=TRAJ_TOL, gpu_k
     [(130, 260)],
     [(64, 576), (100, 70), (256, 64), (5, 3)],
 ])
-def test_first_step_parity(shapes):
-    say("first step", shapes)
-    _, _, _, _, worst = run_pair(shapes, 1, 1e-2)
+def test_first_step_parity(shapes, form):
+    say("first step", shapes, form)
+    _, _, _, _, worst = run_pair(shapes, 1, 1e-2, gpu_kw=dict(factor_form=form))
     say("  worst rel err", worst)
 
 
-def test_trajectory_64x576_100_steps():
-    say("trajectory 64x576 x 100")
-    _, _, _, _, worst = run_pair([(64, 576)], 100, 1e-2, check_every=10)
+@pytest.mark.parametrize("form", FORMS)
+def test_trajectory_64x576_100_steps(form):
+    say("trajectory 64x576 x 100", form)
+    _, _, _, _, worst = run_pair([(64, 576)], 100, 1e-2, check_every=10, gpu_kw=dict(factor_form=form))
     say("  worst rel err", worst)
 
 
-def test_trajectory_multitile_30_steps():
-    say("trajectory (256x1152, 300x200) x 30")
-    run_pair([(256, 1152), (300, 200)], 30, 1e-3, check_every=15)
+@pytest.mark.parametrize("form", FORMS)
+def test_trajectory_multitile_30_steps(form):
+    say("trajectory (256x1152, 300x200) x 30", form)
+    run_pair([(256, 1152), (300, 200)], 30, 1e-3, check_every=15, gpu_kw=dict(factor_form=form))
 
 
+@pytest.mark.parametrize("form", ["explicit", "factored"])
 @pytest.mark.parametrize("t_inject", [2, 5, 20, 50])
-def test_per_step_parity_from_injected_state(t_inject):
+def test_per_step_parity_from_injected_state(t_inject, form):
     """Oracle state after t-1 steps (rounded to fp32) is injected; one step on both."""
     shapes = [(64, 576)]
     say("inject at", t_inject)
@@ -118,7 +125,7 @@ def test_per_step_parity_from_injected_state(t_inject):
     for k in ("L", "R", "m", "m_sgd"):
         setattr(st, k, getattr(st, k).astype(np.float32).astype(np.float64))
     po = [po[0].astype(np.float32).astype(np.float64)]
-    opt = Jorge(shapes)
+    opt = Jorge(shapes, factor_form=form)
     for k, v in oracle_state(orc, 0).items():
         opt.set_state(0, k, to_dev(v))
     opt.t = t_inject - 1
@@ -129,19 +136,21 @@ def test_per_step_parity_from_injected_state(t_inject):
     compare(opt, orc, pg, po, STEP_TOL, f"injected step {t_inject}")
 
 
+@pytest.mark.parametrize("form", ["explicit", "factored"])
 @pytest.mark.parametrize("mode,sigma,beta2", [("fixed", 1e-4, 0.9), ("dynamic", 1e-2, 0.9),
                                               ("clamped", 3e-4, 0.9)])
-def test_beta_modes(mode, sigma, beta2):
-    say("mode", mode)
+def test_beta_modes(mode, sigma, beta2, form):
+    say("mode", mode, form)
     code = {"fixed": 0, "dynamic": 1, "clamped": 2}[mode]
-    run_pair([(48, 96), (70, 40)], 6, sigma, check_every=3, gpu_kw=dict(beta_mode=mode),
+    run_pair([(48, 96), (70, 40)], 6, sigma, check_every=3, gpu_kw=dict(beta_mode=mode, factor_form=form),
              orc_kw=dict(beta_mode=code), hp=dict(HP, beta2=beta2))
 
 
-def test_literal_mode_without_symmetrization():
-    say("literal mode")
-    run_pair([(48, 96), (160, 40)], 6, 1e-2, check_every=3, gpu_kw=dict(symmetrize=False),
-             orc_kw=dict(symmetrize=False))
+@pytest.mark.parametrize("form", FORMS)
+def test_literal_mode_without_symmetrization(form):
+    say("literal mode", form)
+    run_pair([(48, 96), (160, 40), (300, 130)], 6, 1e-2, check_every=3,
+             gpu_kw=dict(symmetrize=False, factor_form=form), orc_kw=dict(symmetrize=False))
 
 
 def test_without_grafting():
@@ -168,11 +177,12 @@ def test_update_interval_parity_and_frozen_factors():
     compare(opt, orc, pg, po, TRAJ_TOL, "k=3")
 
 
-def test_factors_bitwise_symmetric_and_deterministic():
-    shapes = [(200, 300), (64, 147)]
-    say("symmetry + determinism")
-    a = run_pair(shapes, 4, 1e-2)
-    b = run_pair(shapes, 4, 1e-2)
+@pytest.mark.parametrize("form", FORMS)
+def test_factors_bitwise_symmetric_and_deterministic(form):
+    shapes = [(200, 300), (64, 147), (130, 600)]
+    say("symmetry + determinism", form)
+    a = run_pair(shapes, 4, 1e-2, gpu_kw=dict(factor_form=form))
+    b = run_pair(shapes, 4, 1e-2, gpu_kw=dict(factor_form=form))
     for l in range(len(shapes)):
         for k in ("L", "R"):
             A = a[0].get_state(l, k)
@@ -183,7 +193,7 @@ def test_factors_bitwise_symmetric_and_deterministic():
 
 
 def test_grouping_invariance():
-    shapes = [(64, 576), (256, 64), (130, 90)]
+    shapes = [(64, 576), (256, 64), (130, 90), (256, 2304)]
     say("grouping invariance")
     grouped = Jorge(shapes)
     singles = [Jorge([s]) for s in shapes]
@@ -200,10 +210,11 @@ def test_grouping_invariance():
         assert torch.equal(pg[l], ps[l])
 
 
-def test_zero_gradient_is_exact_beta_scaling():
+@pytest.mark.parametrize("form", ["explicit", "factored"])
+def test_zero_gradient_is_exact_beta_scaling(form):
     shapes = [(64, 96)]
-    say("G = 0")
-    opt, _, pg, _, _ = run_pair(shapes, 3, 1e-2)
+    say("G = 0", form)
+    opt, _, pg, _, _ = run_pair(shapes, 3, 1e-2, gpu_kw=dict(factor_form=form))
     before = {k: opt.get_state(0, k) for k in KINDS}
     theta = pg[0].clone()
     opt.step(pg, [torch.zeros(shapes[0], device="cuda")], 0.1, 0.8, 0.9, 1e-3)
@@ -252,7 +263,16 @@ def test_many_small_layers():
 
 def test_full_size_512x4608_first_step():
     say("512x4608 first step")
-    run_pair([(512, 4608)], 1, 1e-3)
+    opt, _, _, _, _ = run_pair([(512, 4608)], 1, 1e-3)
+    assert (opt.factor_form(0, 0), opt.factor_form(0, 1)) == ("explicit", "factored")
+
+
+def test_auto_form_choice():
+    """The cheaper order by tile work: factored when the statistic's rank k is well below d."""
+    opt = Jorge([(64, 576), (512, 512), (256, 2304), (2048, 512), (64, 64)])
+    forms = [(opt.factor_form(l, 0), opt.factor_form(l, 1)) for l in range(5)]
+    assert forms == [("explicit", "factored"), ("explicit", "explicit"), ("explicit", "factored"),
+                     ("factored", "explicit"), ("explicit", "explicit")], forms
 
 
 def test_diagnostics_match_oracle():
@@ -290,33 +310,19 @@ def test_stage_timing_reports_every_update_stage():
     opt.set_timing(True)
     opt.step(p, g, 0.1)
     tm = opt.read_timing()
-    for name in ("stage_in", "gram", "pow4", "xform", "factor_finalize", "poly", "update", "symmetrize",
-                 "precond_L", "precond_R", "layer_finalize", "weight"):
+    # L_hat (256) is explicit and R_hat (512, rank 256) factored, so every stage runs once.
+    assert (opt.factor_form(0, 0), opt.factor_form(0, 1)) == ("explicit", "factored")
+    for name in ("stage_in", "gram", "pow4", "xform", "chain4", "chain5", "factor_finalize", "poly",
+                 "update", "symmetrize", "precond_L", "precond_R", "layer_finalize", "weight"):
         assert tm[name][1] == 1 and tm[name][0] > 0, name
-    assert tm["pow2"] == (0.0, 0)          # A^2 shares the gram launch
+    fl = opt.stage_flops()
+    m, n = 256, 512
+    assert fl["precond_L"] == 2 * m * m * n and fl["precond_R"] == 2 * m * n * n
+    assert fl["stage_in"] == 0 and fl["weight"] == 0
+    # The literal mode launches the powers of non-symmetric factors apart (MN-major B).
     lit = Jorge([(256, 512)], symmetrize=False)
     lit.set_timing(True)
     lit.step([torch.zeros((256, 512), device="cuda")], g, 0.1)
-    assert lit.read_timing()["pow2"][1] == 1
+    assert lit.read_timing()["gram"][1] == 2 and lit.read_timing()["pow4"][1] == 2
     opt.reset_timing()
     assert all(v == (0.0, 0) for v in opt.read_timing().values())
-
-
-@pytest.mark.parametrize("symmetrize", [True, False])
-def test_small_factor_chain_matches_grouped_bitwise(symmetrize):
-    """One workgroup per small factor (second stream) gives the grouped launches' bits."""
-    shapes = [(64, 576), (32, 256), (64, 147), (200, 100), (256, 512)]
-    say("chain vs grouped, symmetrize", symmetrize)
-    chain = Jorge(shapes, symmetrize=symmetrize, small_factor_max=256)
-    grouped = Jorge(shapes, symmetrize=symmetrize, small_factor_max=0)
-    pa = [to_dev(initial_params(0, l, s)) for l, s in enumerate(shapes)]
-    pb = [p.clone() for p in pa]
-    for t in range(1, 4):
-        G = [to_dev(gradient(0, l, t, s, 1e-2)) for l, s in enumerate(shapes)]
-        chain.step(pa, G, **HP)
-        grouped.step(pb, G, **HP)
-    for l in range(len(shapes)):
-        for k in KINDS:
-            assert torch.equal(chain.get_state(l, k), grouped.get_state(l, k)), (l, k)
-        assert torch.equal(pa[l], pb[l])
-        assert chain.read_diag(l) == grouped.read_diag(l)
