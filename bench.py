@@ -44,6 +44,39 @@ def stage_bytes(shapes):
             "stage_in": 16 * mn}     # read G, write the padded copy, read and write m_SGD
 
 
+PROFILE = os.path.join(ROOT, "profiles", "gemm_grouped_resnet50.md")
+
+
+def kernel_sources_sha256():
+    import glob
+    import hashlib
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2310_12298_amd", "csrc", "*"))):
+        h.update(os.path.basename(f).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(config):
+    """HBM bytes per gemm_grouped launch from the committed counter summary, or None.
+
+    The figure applies only to the workload it was taken on, and only while the
+    kernel sources are the ones it was taken with.
+    """
+    if config != "resnet50" or not os.path.exists(PROFILE):
+        return None
+    vals = {}
+    with open(PROFILE) as fh:
+        for line in fh:
+            if ":" in line and line.split(":")[0] in ("traffic_bytes_per_launch", "kernel_sources_sha256"):
+                k, v = line.split(":", 1)
+                vals[k] = v.strip()
+    if vals.get("kernel_sources_sha256") != kernel_sources_sha256():
+        return None
+    return float(vals["traffic_bytes_per_launch"]) if "traffic_bytes_per_launch" in vals else None
+
+
 GEMM_STAGES = ("gram", "pow4", "xform", "chain4", "chain5", "poly", "update", "precond_L", "precond_R")
 
 
@@ -186,7 +219,7 @@ def main():
                    "factor_updates": updates, "factor_form": args.form, "factors": forms, "seed": args.seed},
         "roofline": {"bound": "mfma", "kernel": "gemm_grouped<true, true> (every GEMM stage of the step)",
                      "achieved": achieved, "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / PEAK_FP32_MFMA_TFLOPS, "traffic": None,
+                     "frac": achieved / PEAK_FP32_MFMA_TFLOPS, "traffic": measured_traffic(args.config), "traffic_unit": "HBM bytes per launch",
                      "launches": g_launches, "ms_per_launch": g_ms / max(1, g_launches),
                      "gflop_per_launch": g_flops / max(1, g_launches) / 1e9},
         # executed algorithmic flops of the whole step / (step time x fp32 MFMA peak)
