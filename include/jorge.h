@@ -97,6 +97,11 @@ typedef struct jorge_hparams {
                                  Algorithm 2's product; 0: Z itself. Default 1. */
     int32_t factor_form;      /* JORGE_FORM_*: evaluation order of each factor update.
                                  Default JORGE_FORM_AUTO. */
+    int32_t split_k;          /* 1: a GEMM level with too few tiles for the GPU splits its
+                                 long tiles along K (partial products summed in a fixed
+                                 order: deterministic, but rounded differently from an
+                                 unsplit tile, and the split plan depends on every layer of
+                                 the context); 0: never. Default 1. */
 } jorge_hparams;
 
 /* Largest rows or cols of a layer the library accepts. */

@@ -60,11 +60,11 @@ namespace {
 // Timed stages: one per dependency level of the update (see above).
 enum Stage : int {
     ST_STAGEIN = 0, ST_GRAM, ST_POW4, ST_XFORM, ST_CHAIN4, ST_CHAIN5, ST_FFINAL, ST_POLY, ST_UPDATE,
-    ST_SYMM, ST_PRECOND_L, ST_PRECOND_R, ST_LFINAL, ST_WEIGHT, ST_COUNT
+    ST_SYMM, ST_PRECOND_L, ST_PRECOND_R, ST_LFINAL, ST_WEIGHT, ST_FIXUP, ST_COUNT
 };
 const char* const kStageNames[ST_COUNT] = {
     "stage_in", "gram", "pow4", "xform", "chain4", "chain5", "factor_finalize", "poly", "update",
-    "symmetrize", "precond_L", "precond_R", "layer_finalize", "weight"};
+    "symmetrize", "precond_L", "precond_R", "layer_finalize", "weight", "split_fixup"};
 // The GEMM levels of an update step, in launch order.
 constexpr int kLevels[] = {ST_GRAM, ST_POW4, ST_XFORM, ST_CHAIN4, ST_CHAIN5, ST_POLY, ST_UPDATE};
 
@@ -77,10 +77,13 @@ inline int64_t tiles_of(int64_t x) { return (x + kTile - 1) / kTile; }
 
 struct GemmStage {
     std::vector<GemmProblem> probs;
-    std::vector<TileDesc> tiles;
-    double flops = 0.0;  // algorithmic flops of all its products
+    std::vector<TileDesc> tiles;    // work units, in dispatch order once uploaded
+    std::vector<FixupDesc> fix;     // split tiles
+    int nparts = 0;                 // split-workspace blocks the stage uses
+    double flops = 0.0;             // algorithmic flops of all its products
     GemmProblem* dprobs = nullptr;
     TileDesc* dtiles = nullptr;
+    FixupDesc* dfix = nullptr;
     int ntiles() const { return (int)tiles.size(); }
 };
 
@@ -129,6 +132,8 @@ struct jorge_ctx {
     std::vector<FlatChunk> flat_chunks;
     std::vector<int> stage_batch_start, flat_batch_start;  // first block of each layer batch
     std::vector<SymTile> sym_tiles;
+    float* splitws = nullptr;     // partial products of split tiles (shared by the stages, in turn)
+    int64_t splitws_blocks = 0;
     // Per stage: products with both operands K-major, and (literal mode only)
     // powers of non-symmetric factors, which need an MN-major B.
     GemmStage nt[ST_COUNT], nn[ST_COUNT];
@@ -213,7 +218,7 @@ int add_problem(GemmStage& st, const GemmProblem& p, double flops) {
         for (int tn = 0; tn < tn_n; ++tn)
             for (int tm = g; tm < std::min(g + kGroupRows, tm_n); ++tm) {
                 if (p.upper && tm > tn) continue;
-                st.tiles.push_back({idx, tm, tn, slot++});
+                st.tiles.push_back({idx, tm, tn, slot++, 0, p.K, -1, 0});
             }
     return slot;
 }
@@ -221,6 +226,42 @@ int add_problem(GemmStage& st, const GemmProblem& p, double flops) {
 int tile_count(int M, int N) { return (int)(tiles_of(M) * tiles_of(N)); }
 
 constexpr int kXcds = 8;  // workgroup b of a launch runs on XCD b % 8, in increasing b
+constexpr int kSlots = 512;   // resident GEMM workgroups: 256 CUs x 2
+constexpr int kMinSplitK = 512;  // shortest K piece of a split tile
+
+// Splits the K range of long tiles when a stage has too few tiles to keep
+// every workgroup slot busy: with W the stage's total tile work (sum of K)
+// and target = max(W / kSlots, kMinSplitK), a tile of length K >= 2 target
+// is cut into floor(K / target) pieces of equal length (multiples of 32). Each piece leaves a partial product
+// in the split workspace; a fixup unit per split tile sums them in K order
+// and runs the epilogue.
+void split_stage(GemmStage& st) {
+    int64_t W = 0;
+    for (const TileDesc& t : st.tiles) W += t.k1 - t.k0;
+    const int64_t target = std::max<int64_t>(kMinSplitK, round_up((W + kSlots - 1) / kSlots, kSlab));
+    std::vector<TileDesc> out;
+    out.reserve(st.tiles.size());
+    for (const TileDesc& t : st.tiles) {
+        const int64_t K = t.k1 - t.k0;
+        const int64_t ns = K / target;  // pieces no shorter than the target
+        if (ns < 2) {
+            out.push_back(t);
+            continue;
+        }
+        const int chunk = (int)round_up((K + ns - 1) / ns, kSlab);
+        const int n = (int)((K + chunk - 1) / chunk);
+        st.fix.push_back({t.prob, t.tm, t.tn, t.slot, st.nparts, n, 0, 0});
+        for (int q = 0; q < n; ++q) {
+            TileDesc u = t;
+            u.k0 = t.k0 + q * chunk;
+            u.k1 = std::min(t.k1, u.k0 + chunk);
+            u.part = st.nparts + q;
+            out.push_back(u);
+        }
+        st.nparts += n;
+    }
+    st.tiles.swap(out);
+}
 
 // Puts a stage's tiles in dispatch order. The tiles are sorted by K, longest
 // first; each problem's tiles stay in bands of kGroupRows tile rows walked
@@ -234,20 +275,20 @@ constexpr int kXcds = 8;  // workgroup b of a launch runs on XCD b % 8, in incre
 void order_for_xcds(GemmStage& st) {
     const size_t n = st.tiles.size();
     if (n == 0) return;
-    // Longest K first (stable: each problem's tiles stay together and in order).
+    // Longest K range first (stable: each problem's tiles stay together and in order).
     std::stable_sort(st.tiles.begin(), st.tiles.end(), [&](const TileDesc& a, const TileDesc& b) {
-        return st.probs[a.prob].K > st.probs[b.prob].K;
+        return a.k1 - a.k0 > b.k1 - b.k0;
     });
     std::vector<std::vector<TileDesc>> share(kXcds);
     std::vector<int64_t> work(kXcds, 0);
     for (size_t i = 0; i < n;) {
         size_t j = i + 1;
         while (j < n && st.tiles[j].prob == st.tiles[i].prob && st.tiles[j].tn == st.tiles[i].tn &&
-               st.tiles[j].tm / kGroupRows == st.tiles[i].tm / kGroupRows)
+               st.tiles[j].k0 == st.tiles[i].k0 && st.tiles[j].tm / kGroupRows == st.tiles[i].tm / kGroupRows)
             ++j;
         const int x = (int)(std::min_element(work.begin(), work.end()) - work.begin());
         for (size_t k = i; k < j; ++k) share[x].push_back(st.tiles[k]);
-        work[x] += (int64_t)(j - i) * st.probs[st.tiles[i].prob].K;
+        work[x] += (int64_t)(j - i) * (st.tiles[i].k1 - st.tiles[i].k0);
         i = j;
     }
     std::vector<size_t> next(kXcds, 0);
@@ -273,9 +314,16 @@ jorge_status launch_gemm(jorge_ctx* c, const GemmStage& st, int stage, float bet
     if (st.ntiles() == 0) return JORGE_OK;
     TimedLaunch tl(c, stage);
     hipLaunchKernelGGL((gemm_grouped<AK, BK>), dim3(st.ntiles()), dim3(kGemmThreads), 0, c->stream,
-                       st.dprobs, st.dtiles, beta1);
+                       st.dprobs, st.dtiles, beta1, c->splitws);
     tl.finish();
     JORGE_HIP(c, hipGetLastError());
+    if (!st.fix.empty()) {
+        TimedLaunch tf(c, ST_FIXUP);
+        hipLaunchKernelGGL(gemm_fixup, dim3((unsigned)st.fix.size()), dim3(kGemmThreads), 0, c->stream,
+                           st.dprobs, st.dfix, beta1, c->splitws);
+        tf.finish();
+        JORGE_HIP(c, hipGetLastError());
+    }
     return JORGE_OK;
 }
 
@@ -290,6 +338,7 @@ jorge_status validate_hparams(const jorge_hparams* hp) {
         return JORGE_ERR_INVALID_ARGUMENT;
     if (hp->factor_form < JORGE_FORM_AUTO || hp->factor_form > JORGE_FORM_FACTORED)
         return JORGE_ERR_INVALID_ARGUMENT;
+    if (hp->split_k != 0 && hp->split_k != 1) return JORGE_ERR_INVALID_ARGUMENT;
     return JORGE_OK;
 }
 
@@ -620,15 +669,56 @@ std::string check_stage(const jorge_ctx* c, const GemmStage& st, bool bk, const 
             return where + "momentum";
         if (p.coef != CO_ONE && !in_buffer(c, p.sc, (int64_t)sizeof(FactorScalars))) return where + "scalars";
     }
-    for (const TileDesc& t : st.tiles) {
-        if (t.prob < 0 || t.prob >= (int)st.probs.size()) return std::string(name) + ": tile problem";
-        const GemmProblem& p = st.probs[t.prob];
-        if (t.tm < 0 || t.tn < 0 || t.tm >= tiles_of(p.M) || t.tn >= tiles_of(p.N) || (p.upper && t.tm > t.tn))
+    // Every tile of every problem is covered exactly once: whole, or by split
+    // units whose K ranges tile [0, K) and whose parts match one fixup.
+    std::vector<int> parts_seen(st.nparts, 0);
+    std::vector<const TileDesc*> part_unit(st.nparts, nullptr);
+    auto check_tile = [&](int prob, int tm, int tn, int slot) -> std::string {
+        if (prob < 0 || prob >= (int)st.probs.size()) return std::string(name) + ": tile problem";
+        const GemmProblem& p = st.probs[prob];
+        if (tm < 0 || tn < 0 || tm >= tiles_of(p.M) || tn >= tiles_of(p.N) || (p.upper && tm > tn))
             return std::string(name) + ": tile index";
         if ((p.flags & (EF_NORM | EF_DOT | EF_MOMENTUM)) &&
-            (t.slot < 0 || !in_buffer(c, p.partials, (int64_t)(t.slot + 1) * (int64_t)sizeof(double))))
+            (slot < 0 || !in_buffer(c, p.partials, (int64_t)(slot + 1) * (int64_t)sizeof(double))))
             return std::string(name) + ": partial slot";
+        return "";
+    };
+    int64_t whole = 0, pieces = 0;
+    for (const TileDesc& t : st.tiles) {
+        const std::string e = check_tile(t.prob, t.tm, t.tn, t.slot);
+        if (!e.empty()) return e;
+        const GemmProblem& p = st.probs[t.prob];
+        if (t.k0 < 0 || t.k1 > p.K || t.k0 >= t.k1 || t.k0 % kSlab || t.k1 % kSlab)
+            return std::string(name) + ": unit K range";
+        if (t.part < 0) {
+            if (t.k0 != 0 || t.k1 != p.K) return std::string(name) + ": whole tile K range";
+            ++whole;
+        } else {
+            if (t.part >= st.nparts || parts_seen[t.part]++) return std::string(name) + ": split part";
+            part_unit[t.part] = &t;
+            ++pieces;
+        }
     }
+    for (const FixupDesc& f : st.fix) {
+        const std::string e = check_tile(f.prob, f.tm, f.tn, f.slot);
+        if (!e.empty()) return e;
+        if (f.nsplit < 2 || f.part0 < 0 || f.part0 + f.nsplit > st.nparts) return std::string(name) + ": fixup";
+        int k = 0;
+        for (int q = 0; q < f.nsplit; ++q) {  // the parts are this tile's, in K order, covering [0, K)
+            const TileDesc* u = part_unit[f.part0 + q];
+            if (!u || u->prob != f.prob || u->tm != f.tm || u->tn != f.tn || u->slot != f.slot || u->k0 != k)
+                return std::string(name) + ": fixup parts";
+            k = u->k1;
+        }
+        if (k != st.probs[f.prob].K) return std::string(name) + ": fixup K coverage";
+        pieces -= f.nsplit;
+    }
+    int64_t tiles_total = 0;
+    for (const GemmProblem& p : st.probs) {
+        const int64_t a = tiles_of(p.M), b = tiles_of(p.N);
+        tiles_total += p.upper ? a * (a + 1) / 2 : a * b;
+    }
+    if (pieces != 0 || whole + (int64_t)st.fix.size() != tiles_total) return std::string(name) + ": coverage";
     return "";
 }
 
@@ -673,6 +763,12 @@ jorge_status layout_context(jorge_ctx* c, const jorge_shape* shapes, int32_t num
 jorge_status tables_context(jorge_ctx* c, std::vector<LayerDev>& ld, std::vector<FactorDev>& fd) {
     try {
         build_tables(c, ld, fd);
+        for (int i = 0; i < ST_COUNT; ++i)
+            for (GemmStage* st : {&c->nt[i], &c->nn[i]}) {
+                if (c->hp.split_k) split_stage(*st);
+                order_for_xcds(*st);
+                c->splitws_blocks = std::max<int64_t>(c->splitws_blocks, st->nparts);
+            }
         const std::string e = check_tables(c, fd);
         if (!e.empty()) return fail(c, JORGE_ERR_HIP, "launch table check failed: " + e);
     } catch (const std::bad_alloc&) {
@@ -705,9 +801,9 @@ jorge_status upload(jorge_ctx* c, const std::vector<T>& v, T** dptr) {
 }
 
 jorge_status upload_stage(jorge_ctx* c, GemmStage& st) {
-    order_for_xcds(st);
     jorge_status s = upload(c, st.probs, &st.dprobs);
     if (s != JORGE_OK) return s;
+    if ((s = upload(c, st.fix, &st.dfix)) != JORGE_OK) return s;
     return upload(c, st.tiles, &st.dtiles);
 }
 
@@ -717,7 +813,9 @@ void free_ctx(jorge_ctx* c) {
         for (GemmStage* st : {&c->nt[i], &c->nn[i]}) {
             if (st->dprobs) (void)hipFree(st->dprobs);
             if (st->dtiles) (void)hipFree(st->dtiles);
+            if (st->dfix) (void)hipFree(st->dfix);
         }
+    if (c->splitws) (void)hipFree(c->splitws);
     if (c->dlayers) (void)hipFree(c->dlayers);
     if (c->dfactors) (void)hipFree(c->dfactors);
     if (c->dstage) (void)hipFree(c->dstage);
@@ -794,6 +892,7 @@ jorge_status jorge_hparams_default(jorge_hparams* hp) {
     hp->graft = 1;
     hp->symmetrize = 1;
     hp->factor_form = JORGE_FORM_AUTO;
+    hp->split_k = 1;
     return JORGE_OK;
 }
 
@@ -820,6 +919,10 @@ jorge_status jorge_create(const jorge_shape* shapes, int32_t num_layers, const j
     std::vector<LayerDev> ld;
     std::vector<FactorDev> fd;
     if ((st = tables_context(c, ld, fd)) != JORGE_OK) return bail(st);
+    if (c->splitws_blocks > 0) {
+        e = hipMalloc(reinterpret_cast<void**>(&c->splitws), (size_t)c->splitws_blocks * kSplitBlock * sizeof(float));
+        if (e != hipSuccess) return bail(e == hipErrorOutOfMemory ? JORGE_ERR_OUT_OF_MEMORY : JORGE_ERR_HIP);
+    }
     if ((st = upload(c, ld, &c->dlayers)) != JORGE_OK) return bail(st);
     if ((st = upload(c, fd, &c->dfactors)) != JORGE_OK) return bail(st);
     if ((st = upload(c, c->stage_tiles, &c->dstage)) != JORGE_OK) return bail(st);
@@ -853,7 +956,7 @@ jorge_status jorge_plan(const jorge_shape* shapes, int32_t num_layers, const jor
         st = tables_context(c, ld, fd);
         c->arena = nullptr;
     }
-    if (st == JORGE_OK) *arena_bytes = (int64_t)c->arena_bytes;
+    if (st == JORGE_OK) *arena_bytes = (int64_t)c->arena_bytes + c->splitws_blocks * kSplitBlock * (int64_t)sizeof(float);
     delete c;
     return st;
 }
@@ -982,7 +1085,7 @@ jorge_status jorge_synchronize(jorge_ctx* c) {
 
 jorge_status jorge_device_bytes(const jorge_ctx* c, int64_t* bytes) {
     if (!c || !bytes) return JORGE_ERR_INVALID_ARGUMENT;
-    *bytes = (int64_t)c->arena_bytes;
+    *bytes = (int64_t)c->arena_bytes + c->splitws_blocks * kSplitBlock * (int64_t)sizeof(float);
     return JORGE_OK;
 }
 

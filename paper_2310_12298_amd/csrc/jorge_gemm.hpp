@@ -150,24 +150,16 @@ __device__ __forceinline__ SlabSrc slab_src(const GemmProblem& p, int k0) {
     return {p.A2, p.B2, p.lda2, p.ldb2, k0 - p.K1};
 }
 
-// One 128 x 128 tile (tm, tn) of problem p computed by the whole workgroup,
-// followed by the problem's epilogue; beta1 is the momentum of EF_MOMENTUM.
-// Every thread of the workgroup must call it; it leaves LDS free for reuse.
-//
-// Symmetric results (p.upper): only tiles with tm <= tn are computed. An
-// element (row, col) with row <= col is written at (row, col) and at
-// (col, row), elements below the diagonal of a diagonal tile are skipped,
-// so the stored matrix is bitwise symmetric whatever the product's rounding.
-// The epilogue reads X only at the positions it is about to write, by the
-// same thread, so X may alias C (an in-place update).
+// The product of one 128 x 128 tile (tm, tn) of problem p over K range
+// [k0, k1), accumulated by the whole workgroup into acc. Every thread of the
+// workgroup must call it; it leaves LDS free for reuse.
 template <bool AK, bool BK>
-__device__ __forceinline__ void gemm_tile(const GemmProblem& p, int tm, int tn, int slot, float beta1,
-                                          GemmLds& sm, double* red) {
+__device__ __forceinline__ void gemm_mainloop(const GemmProblem& p, int tm, int tn, int k0, int k1,
+                                              GemmLds& sm, f32x16 (&acc)[2][2]) {
     const int row0 = tm * kTile, col0 = tn * kTile;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int wy = wave >> 1, wx = wave & 1;
 
-    f32x16 acc[2][2];
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
@@ -176,9 +168,9 @@ __device__ __forceinline__ void gemm_tile(const GemmProblem& p, int tm, int tn, 
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
 
     f32x4 ra[4], rb[4];
-    const int nk = p.K / kSlab;
+    const int nk = (k1 - k0) / kSlab;
     {
-        const SlabSrc s0 = slab_src(p, 0);
+        const SlabSrc s0 = slab_src(p, k0);
         load_slab<AK>(s0.a, s0.lda, row0, p.M, s0.k, ra);
         load_slab<BK>(s0.b, s0.ldb, col0, p.N, s0.k, rb);
     }
@@ -189,7 +181,7 @@ __device__ __forceinline__ void gemm_tile(const GemmProblem& p, int tm, int tn, 
         const int cur = kt & 1;
         const bool more = kt + 1 < nk;
         if (more) {
-            const SlabSrc sn = slab_src(p, (kt + 1) * kSlab);
+            const SlabSrc sn = slab_src(p, k0 + (kt + 1) * kSlab);
             load_slab<AK>(sn.a, sn.lda, row0, p.M, sn.k, ra);
             load_slab<BK>(sn.b, sn.ldb, col0, p.N, sn.k, rb);
         }
@@ -204,8 +196,52 @@ __device__ __forceinline__ void gemm_tile(const GemmProblem& p, int tm, int tn, 
         }
         __syncthreads();
     }
+}
 
-    // Epilogue. Accumulator register e of block (i, j) holds
+// Partial products of split tiles: thread t keeps its 64 accumulators as 16
+// float4, float4 q of a block at q * 1024 + 4 t (coalesced across threads).
+__device__ __forceinline__ void store_partial(float* __restrict__ blk, const f32x16 (&acc)[2][2]) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                f32x4 v;
+                v[0] = acc[i][j][q * 4 + 0]; v[1] = acc[i][j][q * 4 + 1];
+                v[2] = acc[i][j][q * 4 + 2]; v[3] = acc[i][j][q * 4 + 3];
+                *reinterpret_cast<f32x4*>(blk + ((i * 2 + j) * 4 + q) * 1024 + 4 * threadIdx.x) = v;
+            }
+}
+
+__device__ __forceinline__ void add_partial(const float* __restrict__ blk, f32x16 (&acc)[2][2]) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const f32x4 v = *(global_f32x4*)(blk + ((i * 2 + j) * 4 + q) * 1024 + 4 * threadIdx.x);
+                acc[i][j][q * 4 + 0] += v[0]; acc[i][j][q * 4 + 1] += v[1];
+                acc[i][j][q * 4 + 2] += v[2]; acc[i][j][q * 4 + 3] += v[3];
+            }
+}
+
+// The epilogue of tile (tm, tn) of problem p for the product in acc; beta1
+// is the momentum of EF_MOMENTUM. All threads of the workgroup call it.
+//
+// Symmetric results (p.upper): only tiles with tm <= tn are computed. An
+// element (row, col) with row <= col is written at (row, col) and at
+// (col, row), elements below the diagonal of a diagonal tile are skipped,
+// so the stored matrix is bitwise symmetric whatever the product's rounding.
+// The epilogue reads X only at the positions it is about to write, by the
+// same thread, so X may alias C (an in-place update).
+__device__ __forceinline__ void gemm_epilogue(const GemmProblem& p, int tm, int tn, int slot, float beta1,
+                                              const f32x16 (&acc)[2][2], double* red) {
+    const int row0 = tm * kTile, col0 = tn * kTile;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wy = wave >> 1, wx = wave & 1;
+    // Accumulator register e of block (i, j) holds
     // C[row0 + wy*64 + i*32 + 8*(e/4) + 4*(lane/32) + e%4][col0 + wx*64 + j*32 + lane%32].
     const int flags = p.flags;
     const bool upper = p.upper != 0;
@@ -284,19 +320,44 @@ __device__ __forceinline__ void gemm_tile(const GemmProblem& p, int tm, int tn, 
     }
 }
 
-// Grouped launch: one workgroup per tile of the list. The tile list is in
-// dispatch order: consecutive workgroups go round-robin to the 8 XCDs, and the
-// host arranged the list so each XCD's share is balanced and reuses operand
-// panels in its own L2.
+// Grouped launch: one workgroup per work unit of the list. The list is in
+// dispatch order: consecutive workgroups go round-robin to the 8 XCDs, and
+// the host arranged it so each XCD's share is balanced and reuses operand
+// panels in its own L2. Units of split tiles leave their partial product in
+// ws for gemm_fixup.
 template <bool AK, bool BK>
 __global__ __launch_bounds__(kGemmThreads, 2) void gemm_grouped(const GemmProblem* __restrict__ probs,
                                                                 const TileDesc* __restrict__ tiles,
-                                                                float beta1) {
+                                                                float beta1, float* __restrict__ ws) {
     __shared__ __attribute__((aligned(16))) GemmLds sm;
     __shared__ double red[4];
     const TileDesc td = tiles[blockIdx.x];
     const GemmProblem p = probs[td.prob];
-    gemm_tile<AK, BK>(p, td.tm, td.tn, td.slot, beta1, sm, red);
+    f32x16 acc[2][2];
+    gemm_mainloop<AK, BK>(p, td.tm, td.tn, td.k0, td.k1, sm, acc);
+    if (td.part >= 0)
+        store_partial(ws + (size_t)td.part * kSplitBlock, acc);
+    else
+        gemm_epilogue(p, td.tm, td.tn, td.slot, beta1, acc, red);
+}
+
+// Split tiles of a grouped launch: sums the partial products in K order
+// (a fixed order, so results are deterministic) and runs the epilogue.
+__global__ __launch_bounds__(kGemmThreads) void gemm_fixup(const GemmProblem* __restrict__ probs,
+                                                           const FixupDesc* __restrict__ fix, float beta1,
+                                                           const float* __restrict__ ws) {
+    __shared__ double red[4];
+    const FixupDesc fd = fix[blockIdx.x];
+    const GemmProblem p = probs[fd.prob];
+    f32x16 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+    for (int s = 0; s < fd.nsplit; ++s) add_partial(ws + (size_t)(fd.part0 + s) * kSplitBlock, acc);
+    gemm_epilogue(p, fd.tm, fd.tn, fd.slot, beta1, acc, red);
 }
 
 }  // namespace jorge

@@ -77,12 +77,35 @@ struct GemmProblem {
     int pad0;
 };
 
+// One work unit of a grouped launch: tile (tm, tn) of a problem over the K
+// range [k0, k1). A unit of a split tile (part >= 0) writes its partial
+// product to block `part` of the launch's split workspace instead of running
+// the epilogue; a fixup unit then sums the parts and runs it.
 struct TileDesc {
     int prob;  // index into the launch's problem table
     int tm;    // tile row
     int tn;    // tile column
     int slot;  // partial-sum slot within the problem
+    int k0;    // K range (multiples of 32)
+    int k1;
+    int part;  // split workspace block, or -1 for a whole tile
+    int pad0;
 };
+
+// A split tile of a grouped launch: its nsplit partial products sit in
+// workspace blocks part0 .. part0 + nsplit - 1, in K order.
+struct FixupDesc {
+    int prob;
+    int tm;
+    int tn;
+    int slot;
+    int part0;
+    int nsplit;
+    int pad0, pad1;
+};
+
+// Floats per split-workspace block: one 128 x 128 tile.
+constexpr int kSplitBlock = 128 * 128;
 
 // Device view of a factor (L_hat or R_hat of one layer).
 struct FactorDev {

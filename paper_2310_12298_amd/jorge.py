@@ -33,7 +33,8 @@ class Shape(ctypes.Structure):
 class HParams(ctypes.Structure):
     _fields_ = [("eps", ctypes.c_double), ("precond_interval", ctypes.c_int32),
                 ("beta_mode", ctypes.c_int32), ("graft", ctypes.c_int32),
-                ("symmetrize", ctypes.c_int32), ("factor_form", ctypes.c_int32)]
+                ("symmetrize", ctypes.c_int32), ("factor_form", ctypes.c_int32),
+                ("split_k", ctypes.c_int32)]
 
 
 _LIB = None
@@ -111,10 +112,10 @@ class Jorge:
     """
 
     def __init__(self, shapes, eps=1e-6, precond_interval=1, beta_mode="clamped", graft=True,
-                 symmetrize=True, factor_form="auto", stream=None):
+                 symmetrize=True, factor_form="auto", split_k=True, stream=None):
         self.lib = load_library()
         self.shapes = [(int(m), int(n)) for m, n in shapes]
-        hp = self.hparams(eps, precond_interval, beta_mode, graft, symmetrize, factor_form)
+        hp = self.hparams(eps, precond_interval, beta_mode, graft, symmetrize, factor_form, split_k)
         arr = (Shape * len(self.shapes))(*[Shape(m, n) for m, n in self.shapes])
         ctx = _P()
         s = _current_stream() if stream is None else int(stream)
@@ -124,7 +125,7 @@ class Jorge:
 
     @staticmethod
     def hparams(eps=1e-6, precond_interval=1, beta_mode="clamped", graft=True, symmetrize=True,
-                factor_form="auto"):
+                factor_form="auto", split_k=True):
         lib = load_library()
         hp = HParams()
         _check(lib, lib.jorge_hparams_default(ctypes.byref(hp)))
@@ -134,6 +135,7 @@ class Jorge:
         hp.graft = int(bool(graft))
         hp.symmetrize = int(bool(symmetrize))
         hp.factor_form = FACTOR_FORMS[factor_form] if isinstance(factor_form, str) else int(factor_form)
+        hp.split_k = int(split_k)
         return hp
 
     @staticmethod

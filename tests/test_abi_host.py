@@ -46,7 +46,7 @@ def test_hparams_default(lib):
     hp = J.HParams()
     assert lib.jorge_hparams_default(ctypes.byref(hp)) == 0
     assert (hp.eps, hp.precond_interval, hp.beta_mode, hp.graft, hp.symmetrize,
-            hp.factor_form) == (1e-6, 1, 2, 1, 1, 0)
+            hp.factor_form, hp.split_k) == (1e-6, 1, 2, 1, 1, 0, 1)
     assert lib.jorge_hparams_default(None) == ERR_INVALID
 
 
@@ -72,7 +72,7 @@ def test_create_rejects_oversize(lib):
                                          ("eps", float("nan")), ("precond_interval", 0),
                                          ("beta_mode", 3), ("beta_mode", -1), ("graft", 2),
                                          ("symmetrize", -1), ("factor_form", -1),
-                                         ("factor_form", 3)])
+                                         ("factor_form", 3), ("split_k", 2), ("split_k", -1)])
 def test_create_rejects_bad_hparams(lib, field, value):
     hp = J.HParams()
     lib.jorge_hparams_default(ctypes.byref(hp))
@@ -111,7 +111,7 @@ def test_null_arguments(lib):
 def test_stage_names_and_status_strings(lib):
     n = lib.jorge_num_stages()
     names = [lib.jorge_stage_name(i).decode() for i in range(n)]
-    assert names[0] == "stage_in" and "xform" in names and names[-1] == "weight"
+    assert names[0] == "stage_in" and "xform" in names and "weight" in names and "split_fixup" in names
     assert len(set(names)) == n
     assert lib.jorge_stage_name(n) is None and lib.jorge_stage_name(-1) is None
     assert lib.jorge_status_string(0) == b"ok"
@@ -139,10 +139,21 @@ FORMS = ("auto", "explicit", "factored")
 @pytest.mark.parametrize("symmetrize", [True, False])
 def test_plan_tables_of_every_workload(lib, name, symmetrize):
     shapes = CONFIGS[name][0]
-    sizes = {f: J.Jorge.plan(shapes, symmetrize=symmetrize, factor_form=f) for f in FORMS}
+    sizes = {f: J.Jorge.plan(shapes, symmetrize=symmetrize, factor_form=f, split_k=False) for f in FORMS}
     assert all(v > 0 for v in sizes.values())
     # Per factor, auto takes one of the two forms' workspaces.
     assert sizes["auto"] <= max(sizes["explicit"], sizes["factored"])
+    for f in FORMS:   # split plans are checked too; they only add their workspace
+        assert J.Jorge.plan(shapes, symmetrize=symmetrize, factor_form=f) >= sizes[f]
+
+
+def test_plan_splits_long_tiles_of_sparse_levels(lib):
+    # One 512 x 4608 layer: ~150 tiles per level with K up to 4608 get split;
+    # the ResNet-50 set keeps every level full without splitting.
+    one = [(512, 4608)]
+    assert J.Jorge.plan(one) > J.Jorge.plan(one, split_k=False)
+    r50 = CONFIGS["resnet50"][0]
+    assert J.Jorge.plan(r50) == J.Jorge.plan(r50, split_k=False)
 
 
 @pytest.mark.parametrize("form", FORMS)
@@ -153,6 +164,7 @@ def test_plan_tables_of_edge_shapes(lib, form, symmetrize):
     assert J.Jorge.plan(shapes, symmetrize=symmetrize, factor_form=form) > 0
     for s in shapes:
         assert J.Jorge.plan([s], symmetrize=symmetrize, factor_form=form) > 0
+        assert J.Jorge.plan([s], symmetrize=symmetrize, factor_form=form, split_k=False) > 0
 
 
 def test_plan_tables_of_random_shapes(lib):

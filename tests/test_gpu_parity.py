@@ -193,10 +193,14 @@ def test_factors_bitwise_symmetric_and_deterministic(form):
 
 
 def test_grouping_invariance():
+    """Each tile is computed the same way whatever else shares its launch.
+
+    Split-K is off: its split plan depends on every layer of the context.
+    """
     shapes = [(64, 576), (256, 64), (130, 90), (256, 2304)]
     say("grouping invariance")
-    grouped = Jorge(shapes)
-    singles = [Jorge([s]) for s in shapes]
+    grouped = Jorge(shapes, split_k=False)
+    singles = [Jorge([s], split_k=False) for s in shapes]
     pg = [to_dev(initial_params(0, l, s)) for l, s in enumerate(shapes)]
     ps = [p.clone() for p in pg]
     for t in range(1, 4):
@@ -326,3 +330,24 @@ def test_stage_timing_reports_every_update_stage():
     assert lit.read_timing()["gram"][1] == 2 and lit.read_timing()["pow4"][1] == 2
     opt.reset_timing()
     assert all(v == (0.0, 0) for v in opt.read_timing().values())
+
+
+@pytest.mark.parametrize("form", ["explicit", "factored", "auto"])
+def test_split_k_parity_and_determinism(form):
+    """Levels with few, long tiles split K; the fixup sums the parts in a fixed order."""
+    shapes = [(128, 2048), (64, 4096)]
+    say("split-K", form)
+    probe = Jorge(shapes, factor_form=form)
+    probe.set_timing(True)
+    probe.step([torch.zeros(s, device="cuda") for s in shapes],
+               [to_dev(gradient(0, l, 1, s, 1e-2)) for l, s in enumerate(shapes)], **HP)
+    assert probe.read_timing()["split_fixup"][1] >= 1          # the plan does split
+    a = run_pair(shapes, 3, 1e-2, gpu_kw=dict(factor_form=form))                 # vs the oracle
+    b = run_pair(shapes, 3, 1e-2, gpu_kw=dict(factor_form=form))
+    c = run_pair(shapes, 3, 1e-2, gpu_kw=dict(factor_form=form, split_k=False))
+    for l in range(len(shapes)):
+        assert torch.equal(a[2][l], b[2][l])
+        for k in KINDS:
+            x, y, z = (r[0].get_state(l, k) for r in (a, b, c))
+            assert torch.equal(x, y), (l, k)                     # deterministic
+            assert rel(x.cpu().numpy(), z.cpu().numpy()) < 1e-5, (l, k)   # split vs unsplit rounding
