@@ -3,12 +3,15 @@
 // One launch covers every tile of a list of independent products (all
 // factors' products of one dependency level of the step). Each product
 // carries its own epilogue (flags and coefficient set, decided at run time
-// per problem), so products with different epilogues share a launch. A workgroup of 256 threads computes one
-// 128 x 128 tile of C = A * B; its four waves each own a 64 x 64 sub-tile held
+// per problem), so products with different epilogues share a launch. A
+// workgroup of 256 threads computes one 128 x 128 tile of C = A * B; its
+// four waves each own a 64 x 64 sub-tile held
 // as 2 x 2 blocks of v_mfma_f32_32x32x2_f32 accumulators. K is consumed in
-// slabs of 32 staged through double-buffered LDS: while the waves run the
-// MFMAs of slab k, each thread holds slab k+1 in registers and writes it to
-// the other LDS buffer afterwards (one barrier per slab).
+// slabs of 32 staged through double-buffered LDS (one barrier per slab): while
+// the waves run the MFMAs of slab k, slab k+1 streams into the other buffer.
+// K-contiguous operands go straight from global memory to LDS
+// (global_load_lds_dwordx4, no register staging); an MN-contiguous operand
+// (the NN kernel's B) is held in registers and written to LDS after the MFMAs.
 //
 // Within a slab, lane l of a wave contributes k = 8*k8 + 4*(l/32) + s to the
 // MFMA of step s (s = 0..3): the half-waves take disjoint halves of each
@@ -29,9 +32,17 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 constexpr int kTile = 128;                    // tile rows = tile columns
 constexpr int kSlab = 32;                     // K per LDS stage
 constexpr int kGemmThreads = 256;
-constexpr int kLdsK = kSlab + 4;              // row stride of a K-contiguous operand in LDS
+// A K-contiguous operand slab (128 rows x 32 k) sits in LDS as 16 blocks of
+// 8 rows of 128 bytes, the 1 KB one wave-wide 16-byte load to LDS writes:
+// lane L loads row L / 8 of the block, so eight consecutive lanes read one
+// contiguous 128-byte row of global memory. The lane loads logical chunk
+// (L % 8) ^ (L / 8) (k = 4c .. 4c+3 is chunk c), so chunk c of block row r
+// sits at physical chunk c ^ r: eight lanes reading one chunk of 8 rows hit
+// 8 distinct 16-byte bank groups, and the 128-byte pad between blocks moves
+// the next 8 rows to the other half of a 64-bank LDS.
+constexpr int kLdsBlock = 8 * 32 + 32;        // floats per 8-row block, with its pad
 constexpr int kLdsMN = kTile + 8;             // row stride of an M/N-contiguous operand in LDS
-constexpr int kLdsOperand = kTile * kLdsK;    // floats per operand per stage (>= kSlab * kLdsMN)
+constexpr int kLdsOperand = 16 * kLdsBlock;   // floats per operand per stage (>= kSlab * kLdsMN)
 static_assert(kLdsOperand >= kSlab * kLdsMN, "LDS operand buffer too small");
 
 // Pointers into global memory (address space 1): loads through them compile
@@ -44,45 +55,58 @@ __device__ __forceinline__ f32x4 gload4(const float* p) {
     return *(global_f32x4*)p;
 }
 
-// Global -> registers: one 128 x 32 operand slab, four 16-byte loads per thread.
-// Rows (K-major) or columns (MN-major) past the extent `lim` are clamped to
-// the last valid one: they only feed outputs that the epilogue discards.
-template <bool KMAJ>
-__device__ __forceinline__ void load_slab(const float* __restrict__ base, int ld, int mn0, int lim,
-                                          int k0, f32x4 (&r)[4]) {
+typedef __attribute__((address_space(1))) void global_void;
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Global -> LDS directly: one 128 x 32 K-contiguous operand slab. Wave w
+// fills blocks 4w .. 4w+3 with one 16-byte load per lane each. Rows past
+// the extent `lim` are clamped to the last valid one: they only feed outputs
+// that the epilogue discards. The loads complete asynchronously (vmcnt).
+__device__ __forceinline__ void load_slab_lds(const float* __restrict__ base, int ld, int mn0, int lim,
+                                              int k0, float* s) {
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int chunk = (lane & 7) ^ (lane >> 3);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int b = wave * 4 + j;
+        const int row = min(mn0 + b * 8 + (lane >> 3), lim - 1);
+        const float* g = base + (size_t)row * ld + k0 + chunk * 4;
+        __builtin_amdgcn_global_load_lds((global_void*)g, (lds_void*)(s + b * kLdsBlock), 16, 0, 0);
+    }
+}
+
+// Global -> registers: one 32 x 128 MN-contiguous operand slab, four 16-byte
+// loads per thread (columns past `lim` clamped as above).
+__device__ __forceinline__ void load_slab_mn(const float* __restrict__ base, int ld, int mn0, int lim,
+                                             int k0, f32x4 (&r)[4]) {
     const int tid = threadIdx.x;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int u = tid + i * kGemmThreads;
-        if constexpr (KMAJ) {
-            const int row = min(mn0 + (u >> 3), lim - 1);
-            r[i] = gload4(base + (size_t)row * ld + k0 + (u & 7) * 4);
-        } else {
-            const int col = min(mn0 + (u & 31) * 4, lim - 4);
-            r[i] = gload4(base + (size_t)(k0 + (u >> 5)) * ld + col);
-        }
+        const int col = min(mn0 + (u & 31) * 4, lim - 4);
+        r[i] = gload4(base + (size_t)(k0 + (u >> 5)) * ld + col);
     }
 }
 
-// Registers -> LDS, in the operand's own layout.
-template <bool KMAJ>
-__device__ __forceinline__ void store_slab(float* s, const f32x4 (&r)[4]) {
+// Registers -> LDS for the MN-contiguous operand.
+__device__ __forceinline__ void store_slab_mn(float* s, const f32x4 (&r)[4]) {
     const int tid = threadIdx.x;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int u = tid + i * kGemmThreads;
-        if constexpr (KMAJ)
-            *reinterpret_cast<f32x4*>(s + (u >> 3) * kLdsK + (u & 7) * 4) = r[i];
-        else
-            *reinterpret_cast<f32x4*>(s + (u >> 5) * kLdsMN + (u & 31) * 4) = r[i];
+        *reinterpret_cast<f32x4*>(s + (u >> 5) * kLdsMN + (u & 31) * 4) = r[i];
     }
 }
 
-// LDS -> MFMA operand registers: values for k = k .. k+3 at row/column mn.
+// LDS -> MFMA operand registers: values for k = k .. k+3 (k a multiple of 4)
+// at row/column mn.
 template <bool KMAJ>
 __device__ __forceinline__ void fragment(const float* s, int mn, int k, float (&f)[4]) {
     if constexpr (KMAJ) {
-        const f32x4 v = *reinterpret_cast<const f32x4*>(s + mn * kLdsK + k);
+        const int r = mn & 7;
+        const f32x4 v =
+            *reinterpret_cast<const f32x4*>(s + (mn >> 3) * kLdsBlock + r * 32 + (((k >> 2) ^ r) << 2));
         f[0] = v[0]; f[1] = v[1]; f[2] = v[2]; f[3] = v[3];
     } else {
 #pragma unroll
@@ -91,7 +115,9 @@ __device__ __forceinline__ void fragment(const float* s, int mn, int k, float (&
 }
 
 // The MFMAs of one LDS slab. Fragments of the next 8-wide k group are read
-// from LDS while the MFMAs of the current group run.
+// from LDS while the MFMAs of the current group run: the scheduling groups
+// at the end place each of those four reads after one of the group's first
+// MFMAs, so their latency hides behind the remaining twelve.
 template <bool AK, bool BK>
 __device__ __forceinline__ void mma_slab(const float* sa, const float* sb, int wy, int wx, int lane,
                                          f32x16 (&acc)[2][2]) {
@@ -121,6 +147,20 @@ __device__ __forceinline__ void mma_slab(const float* sa, const float* sb, int w
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[cur][i][s], b[cur][j][s], acc[i][j],
                                                                      0, 0, 0);
     }
+    if constexpr (AK && BK) {
+        constexpr int kMfma = 0x008, kDsRead = 0x100;
+        __builtin_amdgcn_sched_group_barrier(kDsRead, 4, 0);      // group 0's fragments
+#pragma unroll
+        for (int k8 = 0; k8 + 1 < kSlab / 8; ++k8) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(kDsRead, 1, 0);  // group k8+1's fragments
+            }
+            __builtin_amdgcn_sched_group_barrier(kMfma, 12, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(kMfma, 16, 0);
+    }
 }
 
 // Sum of one double per thread over the workgroup, in a fixed order.
@@ -131,11 +171,6 @@ __device__ __forceinline__ double block_sum_256(double v, double* red) {
     __syncthreads();
     return (red[0] + red[1]) + (red[2] + red[3]);
 }
-
-// LDS of one workgroup of the GEMM: two stages of the A and B operand slabs.
-struct GemmLds {
-    float op[2][2][kLdsOperand];
-};
 
 // Operand base pointer, leading dimension and local k of one slab: the
 // second K segment (k >= K1) reads A2 / B2.
@@ -150,12 +185,43 @@ __device__ __forceinline__ SlabSrc slab_src(const GemmProblem& p, int k0) {
     return {p.A2, p.B2, p.lda2, p.ldb2, k0 - p.K1};
 }
 
+// One LDS stage of the GEMM: the A and B operand slabs. The two stages of
+// the double buffer are separate __shared__ objects, so the compiler can see
+// that loads into one stage never alias reads of the other and does not wait
+// for the in-flight prefetch before reading the current stage.
+struct GemmStageLds {
+    float a[kLdsOperand];
+    float b[kLdsOperand];
+};
+
+// Starts the copy of slab k0 (absolute K) of tile (row0, col0) into stage st.
+// K-contiguous operands load to LDS directly; the MN-contiguous B is held in rb
+// until store_b (after the MFMAs of the other stage).
+template <bool BK>
+__device__ __forceinline__ void issue_slab(const GemmProblem& p, int row0, int col0, int k0, GemmStageLds& st,
+                                           f32x4 (&rb)[4]) {
+    const SlabSrc s = slab_src(p, k0);
+    load_slab_lds(s.a, s.lda, row0, p.M, s.k, st.a);
+    if constexpr (BK) load_slab_lds(s.b, s.ldb, col0, p.N, s.k, st.b);
+    else load_slab_mn(s.b, s.ldb, col0, p.N, s.k, rb);
+}
+
+template <bool BK>
+__device__ __forceinline__ void finish_slab(GemmStageLds& st, const f32x4 (&rb)[4]) {
+    if constexpr (!BK) store_slab_mn(st.b, rb);
+    // This wave's loads to LDS have landed; the barrier makes every wave's visible.
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+}
+
 // The product of one 128 x 128 tile (tm, tn) of problem p over K range
 // [k0, k1), accumulated by the whole workgroup into acc. Every thread of the
-// workgroup must call it; it leaves LDS free for reuse.
+// workgroup must call it; it leaves LDS free for reuse. The slab loop is
+// unrolled by two so each half reads one stage and fills the other.
 template <bool AK, bool BK>
 __device__ __forceinline__ void gemm_mainloop(const GemmProblem& p, int tm, int tn, int k0, int k1,
-                                              GemmLds& sm, f32x16 (&acc)[2][2]) {
+                                              GemmStageLds& s0, GemmStageLds& s1, f32x16 (&acc)[2][2]) {
+    static_assert(AK, "the A operand is always K-contiguous");
     const int row0 = tm * kTile, col0 = tn * kTile;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int wy = wave >> 1, wx = wave & 1;
@@ -167,35 +233,33 @@ __device__ __forceinline__ void gemm_mainloop(const GemmProblem& p, int tm, int 
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
 
-    f32x4 ra[4], rb[4];
+    f32x4 rb[4];
     const int nk = (k1 - k0) / kSlab;
-    {
-        const SlabSrc s0 = slab_src(p, k0);
-        load_slab<AK>(s0.a, s0.lda, row0, p.M, s0.k, ra);
-        load_slab<BK>(s0.b, s0.ldb, col0, p.N, s0.k, rb);
-    }
-    store_slab<AK>(sm.op[0][0], ra);
-    store_slab<BK>(sm.op[0][1], rb);
-    __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-        const int cur = kt & 1;
-        const bool more = kt + 1 < nk;
-        if (more) {
-            const SlabSrc sn = slab_src(p, k0 + (kt + 1) * kSlab);
-            load_slab<AK>(sn.a, sn.lda, row0, p.M, sn.k, ra);
-            load_slab<BK>(sn.b, sn.ldb, col0, p.N, sn.k, rb);
-        }
+    issue_slab<BK>(p, row0, col0, k0, s0, rb);
+    finish_slab<BK>(s0, rb);
+    // Pairs of slabs: slab kt is in s0, kt+1 goes to s1 and kt+2 back to s0.
+    // The loop has no other exit, so the accumulators stay in place.
+    int kt = 0;
+    for (; kt + 2 <= nk; kt += 2) {
+        issue_slab<BK>(p, row0, col0, k0 + (kt + 1) * kSlab, s1, rb);
         // Raised issue priority while this wave runs its MFMAs: the two waves
         // sharing a SIMD then alternate between MFMA and memory phases.
         __builtin_amdgcn_s_setprio(1);
-        mma_slab<AK, BK>(sm.op[cur][0], sm.op[cur][1], wy, wx, lane, acc);
+        mma_slab<AK, BK>(s0.a, s0.b, wy, wx, lane, acc);
         __builtin_amdgcn_s_setprio(0);
-        if (more) {
-            store_slab<AK>(sm.op[cur ^ 1][0], ra);
-            store_slab<BK>(sm.op[cur ^ 1][1], rb);
-        }
-        __syncthreads();
+        finish_slab<BK>(s1, rb);
+        if (kt + 2 < nk) issue_slab<BK>(p, row0, col0, k0 + (kt + 2) * kSlab, s0, rb);
+        __builtin_amdgcn_s_setprio(1);
+        mma_slab<AK, BK>(s1.a, s1.b, wy, wx, lane, acc);
+        __builtin_amdgcn_s_setprio(0);
+        finish_slab<BK>(s0, rb);
     }
+    if (kt < nk) {  // odd slab count: the last slab is in s0
+        __builtin_amdgcn_s_setprio(1);
+        mma_slab<AK, BK>(s0.a, s0.b, wy, wx, lane, acc);
+        __builtin_amdgcn_s_setprio(0);
+    }
+    __syncthreads();  // every wave is done with both stages
 }
 
 // Partial products of split tiles: thread t keeps its 64 accumulators as 16
@@ -329,12 +393,13 @@ template <bool AK, bool BK>
 __global__ __launch_bounds__(kGemmThreads, 2) void gemm_grouped(const GemmProblem* __restrict__ probs,
                                                                 const TileDesc* __restrict__ tiles,
                                                                 float beta1, float* __restrict__ ws) {
-    __shared__ __attribute__((aligned(16))) GemmLds sm;
+    __shared__ __attribute__((aligned(16))) GemmStageLds s0;
+    __shared__ __attribute__((aligned(16))) GemmStageLds s1;
     __shared__ double red[4];
     const TileDesc td = tiles[blockIdx.x];
     const GemmProblem p = probs[td.prob];
     f32x16 acc[2][2];
-    gemm_mainloop<AK, BK>(p, td.tm, td.tn, td.k0, td.k1, sm, acc);
+    gemm_mainloop<AK, BK>(p, td.tm, td.tn, td.k0, td.k1, s0, s1, acc);
     if (td.part >= 0)
         store_partial(ws + (size_t)td.part * kSplitBlock, acc);
     else
