@@ -291,38 +291,65 @@ __device__ __forceinline__ void add_partial(const float* __restrict__ blk, f32x1
             }
 }
 
-// The epilogue of tile (tm, tn) of problem p for the product in acc; beta1
-// is the momentum of EF_MOMENTUM. All threads of the workgroup call it.
-//
-// Symmetric results (p.upper): only tiles with tm <= tn are computed. An
-// element (row, col) with row <= col is written at (row, col) and at
-// (col, row), elements below the diagonal of a diagonal tile are skipped,
-// so the stored matrix is bitwise symmetric whatever the product's rounding.
-// The epilogue reads X only at the positions it is about to write, by the
-// same thread, so X may alias C (an in-place update).
-__device__ __forceinline__ void gemm_epilogue(const GemmProblem& p, int tm, int tn, int slot, float beta1,
-                                              const f32x16 (&acc)[2][2], double* red) {
+typedef __attribute__((address_space(1))) float gfloat;
+typedef __attribute__((address_space(1))) f32x4 gfloat4;
+typedef __attribute__((address_space(1))) char gchar;
+
+// Global accesses at a 32-bit byte offset from a uniform base: they compile to
+// the base-in-SGPR, offset-in-VGPR form with no 64-bit address arithmetic.
+// Every matrix here spans at most 32768^2 floats, so byte offsets fit in 32 bits.
+__device__ __forceinline__ float ld_at(const float* base, unsigned byte_off) {
+    return *(const gfloat*)((const gchar*)base + byte_off);
+}
+__device__ __forceinline__ void st_at(float* base, unsigned byte_off, float v) {
+    *(gfloat*)((gchar*)base + byte_off) = v;
+}
+__device__ __forceinline__ void st4_at(float* base, unsigned byte_off, f32x4 v) {
+    *(gfloat4*)((gchar*)base + byte_off) = v;
+}
+
+// The epilogue body for one combination of flags F and symmetry UP, known
+// at compile time. value = ci [row == col < valid_m] + cx X + cc acc.
+// Offsets are 32-bit (every matrix has fewer than 2^32 elements) from
+// uniform base pointers; per-element masks are only evaluated on edge tiles
+// and on diagonal tiles of symmetric results.
+template <int F, bool UP, bool MASKED>
+__device__ __forceinline__ double epilogue_body(const GemmProblem& p, int tm, int tn, const f32x16 (&acc)[2][2],
+                                                float ci, float cx, float cc) {
+    constexpr bool kReadX = (F & EF_READX) != 0;
+    constexpr bool kRead = (F & (EF_READX | EF_DOT)) != 0;
     const int row0 = tm * kTile, col0 = tn * kTile;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int wy = wave >> 1, wx = wave & 1;
-    // Accumulator register e of block (i, j) holds
-    // C[row0 + wy*64 + i*32 + 8*(e/4) + 4*(lane/32) + e%4][col0 + wx*64 + j*32 + lane%32].
-    const int flags = p.flags;
-    const bool upper = p.upper != 0;
-    const bool diag = upper && tm == tn;
-    float ci = 0.f, cx = 0.f, cc = 1.f;
-    if (p.coef != CO_ONE) {
-        const FactorScalars* s = p.sc;
-        switch (p.coef) {
-            case CO_POLY: ci = 1.f; cx = -s->a; cc = s->b; break;
-            case CO_SCALE: cc = s->sf; break;
-            case CO_WMIX: cx = s->a; cc = -s->b; break;
-            case CO_SYR2K: cx = s->sf; cc = -0.5f * s->sf; break;
-            case CO_LITUPD: cx = s->sf; cc = -s->sf; break;
-            default: break;
-        }
+    const int wy = wave >> 1, wx = wave & 1, h = lane >> 5;
+    const bool diag = MASKED && UP && tm == tn;
+    const bool ident = kReadX && ci != 0.f && tm == tn;
+    constexpr double w_off = UP ? 2.0 : 1.0;   // off-diagonal tiles of a symmetric result
+    float* C = p.C;
+    float* C2 = p.C2;
+    const float* X = p.X;
+    // Row strides in bytes.
+    const unsigned sc = 4u * p.ldc, sc2 = 4u * p.ldc2, sx = 4u * p.ldx;
+
+    // Unmasked tiles (every element inside M x N, not a diagonal tile of a
+    // symmetric result) load all their X values before anything is stored, so
+    // one memory round trip serves the whole tile (X may be C itself, and the
+    // compiler keeps loads after earlier stores it cannot tell apart).
+    f32x16 xv[2][2];
+    if constexpr (kRead && !MASKED) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const int col = col0 + wx * 64 + j * 32 + (lane & 31);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const unsigned ox = (unsigned)(row0 + wy * 64 + i * 32 + q * 8 + h * 4) * sx + 4u * (unsigned)col;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) xv[i][j][q * 4 + e] = ld_at(X, ox + e * sx);
+                }
+            }
     }
-    const int h = lane >> 5;
+
     double part = 0.0;
 #pragma unroll
     for (int i = 0; i < 2; ++i)
@@ -332,52 +359,219 @@ __device__ __forceinline__ void gemm_epilogue(const GemmProblem& p, int tm, int 
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
                 const int rowb = row0 + wy * 64 + i * 32 + q * 8 + h * 4;
-                if (flags & EF_MOMENTUM) {
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const int row = rowb + e;
-                        if (row < p.valid_m && col < p.valid_n) {
-                            float* mp = p.mom + (size_t)row * p.ldmom + col;
-                            const float mn = beta1 * *mp + (1.0f - beta1) * acc[i][j][q * 4 + e];
-                            *mp = mn;
-                            part += (double)mn * (double)mn;
-                        }
-                    }
-                    continue;
-                }
                 // rowb .. rowb+3 are all inside M when rowb is (M is a multiple of 4).
-                if (rowb >= p.M || col >= p.N) continue;
+                if (MASKED && (rowb >= p.M || col >= p.N)) continue;
+                // Masked tiles read X per group of 4 rows; within a diagonal tile
+                // only positions on or above the diagonal, each read and written
+                // by the same thread.
+                f32x4 x;
+                if constexpr (kRead && MASKED) {
+                    const unsigned ox = (unsigned)rowb * sx + 4u * (unsigned)col;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) x[e] = (!diag || rowb + e <= col) ? ld_at(X, ox + e * sx) : 0.0f;
+                }
                 f32x4 out;
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    const int row = rowb + e;
                     const float v = acc[i][j][q * 4 + e];
-                    out[e] = 0.f;
-                    if (upper && row > col) continue;   // lower half of a diagonal tile
                     float o = cc * v;
-                    if (flags & EF_READX) {
-                        const float x = *(global_f32*)(p.X + (size_t)row * p.ldx + col);
-                        const float id = (row == col && row < p.valid_m) ? ci : 0.0f;
-                        o = (id + cx * x) + o;
+                    if constexpr (kRead && !MASKED) x[e] = xv[i][j][q * 4 + e];
+                    if constexpr (kReadX) {
+                        const float id = (ident && rowb + e == col && col < p.valid_m) ? ci : 0.0f;
+                        o = (id + cx * x[e]) + o;
                     }
                     out[e] = o;
-                    const double w = (upper && row != col) ? 2.0 : 1.0;
-                    if (flags & EF_NORM) part += w * (double)o * (double)o;
-                    if (flags & EF_DOT)
-                        part += w * (double)v * (double)*(global_f32*)(p.X + (size_t)row * p.ldx + col);
-                    if ((flags & EF_STORE) && diag) {
-                        p.C[(size_t)row * p.ldc + col] = o;
-                        if (row != col) p.C[(size_t)col * p.ldc + row] = o;
+                }
+                if (!diag) {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        if constexpr ((F & EF_NORM) != 0) part += w_off * (double)out[e] * (double)out[e];
+                        if constexpr ((F & EF_DOT) != 0) part += w_off * (double)acc[i][j][q * 4 + e] * (double)x[e];
+                    }
+                    if constexpr ((F & EF_STORE) != 0) {
+                        const unsigned oc = (unsigned)rowb * sc + 4u * (unsigned)col;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) st_at(C, oc + e * sc, out[e]);
+                        if constexpr (UP) st4_at(C, (unsigned)col * sc + 4u * (unsigned)rowb, out);
+                    }
+                    if constexpr ((F & EF_STORE_T) != 0) st4_at(C2, (unsigned)col * sc2 + 4u * (unsigned)rowb, out);
+                } else {
+                    // Diagonal tile of a symmetric result: element (row, col) with
+                    // row <= col is written at both positions.
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int row = rowb + e;
+                        if (row > col) continue;
+                        const double w = row != col ? 2.0 : 1.0;
+                        if constexpr ((F & EF_NORM) != 0) part += w * (double)out[e] * (double)out[e];
+                        if constexpr ((F & EF_DOT) != 0) part += w * (double)acc[i][j][q * 4 + e] * (double)x[e];
+                        if constexpr ((F & EF_STORE) != 0) {
+                            st_at(C, (unsigned)row * sc + 4u * (unsigned)col, out[e]);
+                            if (row != col) st_at(C, (unsigned)col * sc + 4u * (unsigned)row, out[e]);
+                        }
                     }
                 }
-                if ((flags & EF_STORE) && !diag) {
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) p.C[(size_t)(rowb + e) * p.ldc + col] = out[e];
-                    if (upper) *reinterpret_cast<f32x4*>(p.C + (size_t)col * p.ldc + rowb) = out;
-                }
-                if (flags & EF_STORE_T) *reinterpret_cast<f32x4*>(p.C2 + (size_t)col * p.ldc2 + rowb) = out;
             }
         }
+    return part;
+}
+
+// The epilogue for a flag combination without a compiled body (not used by
+// the launch tables the library builds; kept so every combination works).
+__device__ __forceinline__ double epilogue_generic(const GemmProblem& p, int tm, int tn, const f32x16 (&acc)[2][2],
+                                                float ci, float cx, float cc) {
+    double part = 0.0;
+    const int F = p.flags;
+    const bool up = p.upper != 0;
+    const int row0 = tm * kTile, col0 = tn * kTile;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wy = wave >> 1, wx = wave & 1, h = lane >> 5;
+    float* C = p.C;
+    float* C2 = p.C2;
+    const float* X = p.X;
+    const unsigned sc = 4u * p.ldc, sc2 = 4u * p.ldc2, sx = 4u * p.ldx;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int col = col0 + wx * 64 + j * 32 + (lane & 31);
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int row = row0 + wy * 64 + i * 32 + q * 8 + h * 4 + e;
+                    if (row >= p.M || col >= p.N || (up && row > col)) continue;
+                    const float v = acc[i][j][q * 4 + e];
+                    const float xe = (F & (EF_READX | EF_DOT)) ? ld_at(X, (unsigned)row * sx + 4u * (unsigned)col) : 0.f;
+                    float o = cc * v;
+                    if (F & EF_READX) o = (((row == col && row < p.valid_m) ? ci : 0.0f) + cx * xe) + o;
+                    const double w = (up && row != col) ? 2.0 : 1.0;
+                    if (F & EF_NORM) part += w * (double)o * (double)o;
+                    if (F & EF_DOT) part += w * (double)v * (double)xe;
+                    if (F & EF_STORE) {
+                        st_at(C, (unsigned)row * sc + 4u * (unsigned)col, o);
+                        if (up && row != col) st_at(C, (unsigned)col * sc + 4u * (unsigned)row, o);
+                    }
+                    if (F & EF_STORE_T) st_at(C2, (unsigned)col * sc2 + 4u * (unsigned)row, o);
+                }
+        }
+    return part;
+}
+
+// m = beta1 m + (1 - beta1) acc on the dense valid_m x valid_n momentum.
+template <bool MASKED>
+__device__ __forceinline__ double epilogue_momentum(const GemmProblem& p, int tm, int tn,
+                                                    const f32x16 (&acc)[2][2], float beta1) {
+    const int row0 = tm * kTile, col0 = tn * kTile;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wy = wave >> 1, wx = wave & 1, h = lane >> 5;
+    float* mom = p.mom;
+    const unsigned sm = 4u * p.ldmom;
+    // Unmasked (interior) tiles load all of this thread's momentum values
+    // before any is stored; masked tiles go element by element.
+    f32x16 mv[2][2];
+    if constexpr (!MASKED) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const int col = col0 + wx * 64 + j * 32 + (lane & 31);
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int row = row0 + wy * 64 + i * 32 + q * 8 + h * 4 + e;
+                        mv[i][j][q * 4 + e] = ld_at(mom, (unsigned)row * sm + 4u * (unsigned)col);
+                    }
+            }
+    }
+    double part = 0.0;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int col = col0 + wx * 64 + j * 32 + (lane & 31);
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int row = row0 + wy * 64 + i * 32 + q * 8 + h * 4 + e;
+                    if (MASKED && !(row < p.valid_m && col < p.valid_n)) continue;
+                    const unsigned o = (unsigned)row * sm + 4u * (unsigned)col;
+                    const float old = MASKED ? ld_at(mom, o) : mv[i][j][q * 4 + e];
+                    const float mn = beta1 * old + (1.0f - beta1) * acc[i][j][q * 4 + e];
+                    st_at(mom, o, mn);
+                    part += (double)mn * (double)mn;
+                }
+        }
+    return part;
+}
+
+// The epilogue of tile (tm, tn) of problem p for the product in acc; beta1
+// is the momentum of EF_MOMENTUM. All threads of the workgroup call it.
+// One uniform switch picks the compiled body for the problem's flags.
+//
+// Symmetric results (p.upper): only tiles with tm <= tn are computed. An
+// element (row, col) with row <= col is written at (row, col) and at
+// (col, row), elements below the diagonal of a diagonal tile are skipped,
+// so the stored matrix is bitwise symmetric whatever the product's rounding.
+// The epilogue reads X only at the positions it is about to write, by the
+// same thread, so X may alias C (an in-place update).
+__device__ __forceinline__ void gemm_epilogue(const GemmProblem& p, int tm, int tn, int slot, float beta1,
+                                              const f32x16 (&acc)[2][2], double* red) {
+    const int flags = p.flags;
+    double part = 0.0;
+    if (flags & EF_MOMENTUM) {
+        // Interior tiles of the dense valid_m x valid_n momentum need no masks.
+        if ((tm + 1) * kTile <= p.valid_m && (tn + 1) * kTile <= p.valid_n)
+            part = epilogue_momentum<false>(p, tm, tn, acc, beta1);
+        else
+            part = epilogue_momentum<true>(p, tm, tn, acc, beta1);
+    } else {
+        float ci = 0.f, cx = 0.f, cc = 1.f;
+        if (p.coef != CO_ONE) {
+            const FactorScalars* sc = p.sc;
+            switch (p.coef) {
+                case CO_POLY: ci = 1.f; cx = -sc->a; cc = sc->b; break;
+                case CO_SCALE: cc = sc->sf; break;
+                case CO_WMIX: cx = sc->a; cc = -sc->b; break;
+                case CO_SYR2K: cx = sc->sf; cc = -0.5f * sc->sf; break;
+                case CO_LITUPD: cx = sc->sf; cc = -sc->sf; break;
+                default: break;
+            }
+        }
+        const int key = flags | (p.upper ? 256 : 0);
+        const bool masked = (tm + 1) * kTile > p.M || (tn + 1) * kTile > p.N || (p.upper && tm == tn);
+        switch (key) {
+            case EF_STORE: part = masked ? epilogue_body<EF_STORE, false, true>(p, tm, tn, acc, ci, cx, cc)
+                            : epilogue_body<EF_STORE, false, false>(p, tm, tn, acc, ci, cx, cc); break;
+            case EF_STORE | 256: part = masked ? epilogue_body<EF_STORE, true, true>(p, tm, tn, acc, ci, cx, cc)
+                            : epilogue_body<EF_STORE, true, false>(p, tm, tn, acc, ci, cx, cc); break;
+            case EF_STORE_T: part = masked ? epilogue_body<EF_STORE_T, false, true>(p, tm, tn, acc, ci, cx, cc)
+                            : epilogue_body<EF_STORE_T, false, false>(p, tm, tn, acc, ci, cx, cc); break;
+            case EF_DOT | 256: part = masked ? epilogue_body<EF_DOT, true, true>(p, tm, tn, acc, ci, cx, cc)
+                            : epilogue_body<EF_DOT, true, false>(p, tm, tn, acc, ci, cx, cc); break;
+            case EF_STORE | EF_STORE_T | EF_NORM:
+                part = masked ? epilogue_body<EF_STORE | EF_STORE_T | EF_NORM, false, true>(p, tm, tn, acc, ci, cx, cc)
+                            : epilogue_body<EF_STORE | EF_STORE_T | EF_NORM, false, false>(p, tm, tn, acc, ci, cx, cc);
+                break;
+            case EF_STORE_T | EF_READX:
+                part = masked ? epilogue_body<EF_STORE_T | EF_READX, false, true>(p, tm, tn, acc, ci, cx, cc)
+                            : epilogue_body<EF_STORE_T | EF_READX, false, false>(p, tm, tn, acc, ci, cx, cc);
+                break;
+            case EF_STORE | EF_READX:
+                part = masked ? epilogue_body<EF_STORE | EF_READX, false, true>(p, tm, tn, acc, ci, cx, cc)
+                            : epilogue_body<EF_STORE | EF_READX, false, false>(p, tm, tn, acc, ci, cx, cc);
+                break;
+            case EF_STORE | EF_READX | 256:
+                part = masked ? epilogue_body<EF_STORE | EF_READX, true, true>(p, tm, tn, acc, ci, cx, cc)
+                            : epilogue_body<EF_STORE | EF_READX, true, false>(p, tm, tn, acc, ci, cx, cc);
+                break;
+            default:  // any other combination: every flag tested at run time
+                part = epilogue_generic(p, tm, tn, acc, ci, cx, cc);
+                break;
+        }
+    }
     if (flags & (EF_NORM | EF_DOT | EF_MOMENTUM)) {
         const double total = block_sum_256(part, red);
         if (threadIdx.x == 0) p.partials[slot] = total;
