@@ -461,7 +461,11 @@ void add_explicit(jorge_ctx* c, const FactorHost& F, const FactorDev& fd, const 
 
 // The products of one factor's update in the factored order (through H).
 // Hr: H row-major (dp x kp, ld kp); Ht: H^T row-major (kp x dp, ld dp).
-int add_factored(jorge_ctx* c, const FactorHost& F, const FactorDev& fd, const float* Hr, const float* Ht) {
+// Mo: the other factor's statistic when that factor is in the explicit order
+// (H^T H is exactly it: G^T G for L_hat, G G^T for R_hat; kp x kp, ld kp,
+// computed in the gram level and kept until poly), or null.
+int add_factored(jorge_ctx* c, const FactorHost& F, const FactorDev& fd, const float* Hr, const float* Ht,
+                 const float* Mo) {
     const bool sym = c->hp.symmetrize != 0;
     const int dp = F.dp, kp = F.kp;
     const double d = F.d, k = F.k;
@@ -470,10 +474,14 @@ int add_factored(jorge_ctx* c, const FactorHost& F, const FactorDev& fd, const f
     float* P1 = at<float>(c, F.off_w[1]);
     float* Q = at<float>(c, F.off_w[2]);
     float* S = at<float>(c, F.off_w[3]);
-    // Q = H^T H
-    GemmProblem q = product(Ht, dp, Ht, dp, kp, kp, dp);
-    q.C = Q; q.ldc = kp; q.flags = EF_STORE; q.upper = 1;
-    add_problem(c->nt[ST_GRAM], q, k * k * d);
+    // Q = H^T H, unless the other factor's statistic already is.
+    if (Mo) {
+        Q = const_cast<float*>(Mo);
+    } else {
+        GemmProblem q = product(Ht, dp, Ht, dp, kp, kp, dp);
+        q.C = Q; q.ldc = kp; q.flags = EF_STORE; q.upper = 1;
+        add_problem(c->nt[ST_GRAM], q, k * k * d);
+    }
     // Yt_{j+1} = Yt_j A^T, starting from Yt_0 = H^T: P0, P1, P0, P1.
     const float* src = Ht;
     float* dst[4] = {P0, P1, P0, P1};
@@ -586,7 +594,10 @@ void build_tables(jorge_ctx* c, std::vector<LayerDev>& ld, std::vector<FactorDev
         if (F.expl) {
             add_explicit(c, F, fd[fi], Hr);
         } else {
-            F.nparts = add_factored(c, F, fd[fi], Hr, Ht);
+            const auto& L = c->layers[F.layer];
+            const FactorHost& O = c->factors[F.side == 0 ? L.fR : L.fL];
+            const float* Mo = O.expl ? at<float>(c, O.off_w[0]) : nullptr;
+            F.nparts = add_factored(c, F, fd[fi], Hr, Ht, Mo);
             fd[fi].nparts = F.nparts;
         }
     }
