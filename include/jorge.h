@@ -102,6 +102,10 @@ typedef struct jorge_hparams {
                                  order: deterministic, but rounded differently from an
                                  unsplit tile, and the split plan depends on every layer of
                                  the context); 0: never. Default 1. */
+    int32_t lds_chain_max;    /* factors whose size rounded up to 32 is at most this take the
+                                 explicit order in one workgroup with every matrix in LDS
+                                 (one launch for all of them) instead of the grouped levels;
+                                 0 disables. In [0, 64]. Default 64. */
 } jorge_hparams;
 
 /* Largest rows or cols of a layer the library accepts. */

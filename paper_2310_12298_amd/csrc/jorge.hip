@@ -37,6 +37,10 @@
 //   precond   T = L_hat G, then G~ = T R_hat fused with m <- beta1 m + (1-beta1) G~
 //   lfinal    ||m||, ||m_SGD||, grafted step g
 //   weight    theta <- theta (1 - lr wd) - g m
+// Factors of padded size up to hp.lds_chain_max (at most 64) skip the levels:
+// lds_chain_kernel runs each one's whole explicit-order update in one
+// workgroup with every matrix in LDS, on a second stream concurrent with the
+// levels (forked after stage-in, joined before preconditioning).
 // Non-update steps run stage-in, precond, lfinal and weight only.
 #include <hip/hip_runtime.h>
 
@@ -60,11 +64,11 @@ namespace {
 // Timed stages: one per dependency level of the update (see above).
 enum Stage : int {
     ST_STAGEIN = 0, ST_GRAM, ST_POW4, ST_XFORM, ST_CHAIN4, ST_CHAIN5, ST_FFINAL, ST_POLY, ST_UPDATE,
-    ST_SYMM, ST_PRECOND_L, ST_PRECOND_R, ST_LFINAL, ST_WEIGHT, ST_FIXUP, ST_COUNT
+    ST_SYMM, ST_PRECOND_L, ST_PRECOND_R, ST_LFINAL, ST_WEIGHT, ST_FIXUP, ST_LDS_CHAIN, ST_COUNT
 };
 const char* const kStageNames[ST_COUNT] = {
     "stage_in", "gram", "pow4", "xform", "chain4", "chain5", "factor_finalize", "poly", "update",
-    "symmetrize", "precond_L", "precond_R", "layer_finalize", "weight", "split_fixup"};
+    "symmetrize", "precond_L", "precond_R", "layer_finalize", "weight", "split_fixup", "lds_chain"};
 // The GEMM levels of an update step, in launch order.
 constexpr int kLevels[] = {ST_GRAM, ST_POW4, ST_XFORM, ST_CHAIN4, ST_CHAIN5, ST_POLY, ST_UPDATE};
 
@@ -100,6 +104,7 @@ struct LayerHost {
 struct FactorHost {
     int layer, side, d, dp, k, kp;
     bool expl = true;
+    bool chain = false;  // small: the whole update in one workgroup (lds_chain_kernel), explicit order
     size_t off_A, off_part, off_sc;
     size_t off_w[4];
     int nparts = 0;
@@ -132,6 +137,13 @@ struct jorge_ctx {
     std::vector<FlatChunk> flat_chunks;
     std::vector<int> stage_batch_start, flat_batch_start;  // first block of each layer batch
     std::vector<SymTile> sym_tiles;
+    std::vector<int> grouped, chain;   // factors of the grouped levels / of the LDS chain
+    int* dgrouped = nullptr;
+    int* dchain = nullptr;
+    // The LDS chain runs on a library-owned stream (default priority), forked
+    // from the context's stream after stage-in and joined before preconditioning.
+    hipStream_t side = nullptr;
+    hipEvent_t ev_fork = nullptr, ev_join = nullptr;
     float* splitws = nullptr;     // partial products of split tiles (shared by the stages, in turn)
     int64_t splitws_blocks = 0;
     // Per stage: products with both operands K-major, and (literal mode only)
@@ -179,16 +191,18 @@ hipEvent_t take_event(jorge_ctx* c) {
 struct TimedLaunch {
     jorge_ctx* c;
     int stage;
+    hipStream_t stream;
     hipEvent_t start = nullptr, stop = nullptr;
-    TimedLaunch(jorge_ctx* ctx, int st) : c(ctx), stage(st) {
+    TimedLaunch(jorge_ctx* ctx, int st) : TimedLaunch(ctx, st, ctx->stream) {}
+    TimedLaunch(jorge_ctx* ctx, int st, hipStream_t s) : c(ctx), stage(st), stream(s) {
         if (!c->timing) return;
         start = take_event(c);
         stop = take_event(c);
-        if (start) (void)hipEventRecord(start, c->stream);
+        if (start) (void)hipEventRecord(start, stream);
     }
     void finish() {
         if (!c->timing || !start || !stop) return;
-        (void)hipEventRecord(stop, c->stream);
+        (void)hipEventRecord(stop, stream);
         c->pending.push_back({stage, start, stop});
     }
 };
@@ -339,6 +353,7 @@ jorge_status validate_hparams(const jorge_hparams* hp) {
     if (hp->factor_form < JORGE_FORM_AUTO || hp->factor_form > JORGE_FORM_FACTORED)
         return JORGE_ERR_INVALID_ARGUMENT;
     if (hp->split_k != 0 && hp->split_k != 1) return JORGE_ERR_INVALID_ARGUMENT;
+    if (hp->lds_chain_max < 0 || hp->lds_chain_max > kChainMax) return JORGE_ERR_INVALID_ARGUMENT;
     return JORGE_OK;
 }
 
@@ -379,12 +394,15 @@ size_t plan(jorge_ctx* c) {
             F.dp = side == 0 ? L.mp : L.np;
             F.k = side == 0 ? L.n : L.m;
             F.kp = side == 0 ? L.np : L.mp;
-            if (c->hp.factor_form == JORGE_FORM_EXPLICIT) F.expl = true;
+            F.chain = F.dp <= c->hp.lds_chain_max;
+            if (F.chain || c->hp.factor_form == JORGE_FORM_EXPLICIT) F.expl = true;
             else if (c->hp.factor_form == JORGE_FORM_FACTORED) F.expl = false;
             else F.expl = explicit_is_cheaper(F.dp, F.kp, sym);
             const size_t dd = (size_t)F.dp * F.dp * sizeof(float);
             F.off_A = take(dd);
-            if (F.expl) {
+            if (F.chain) {
+                F.nparts = 1;  // unused: the chain kernel reduces ||X|| itself
+            } else if (F.expl) {
                 for (int w = 0; w < 4; ++w) F.off_w[w] = take(dd);
                 F.nparts = tile_count(F.dp, F.dp);
             } else {
@@ -540,9 +558,13 @@ void build_tables(jorge_ctx* c, std::vector<LayerDev>& ld, std::vector<FactorDev
         d.A = at<float>(c, F.off_A);
         d.sc = at<FactorScalars>(c, F.off_sc);
         d.partials = at<double>(c, F.off_part);
-        d.Z = F.expl ? at<float>(c, F.off_w[2]) : nullptr;
+        d.Z = (F.expl && !F.chain) ? at<float>(c, F.off_w[2]) : nullptr;
+        const auto& L = c->layers[F.layer];
+        d.H = at<float>(c, F.side == 0 ? L.off_Gp : L.off_Gpt);
         d.d = F.d;
         d.dp = F.dp;
+        d.k = F.k;
+        d.kp = F.kp;
         d.nparts = F.nparts;
         d.explicit_form = F.expl ? 1 : 0;
         fd.push_back(d);
@@ -591,12 +613,17 @@ void build_tables(jorge_ctx* c, std::vector<LayerDev>& ld, std::vector<FactorDev
         // H row-major (d x k) and H^T row-major (k x d): G and G^T for L, the reverse for R.
         const float* Hr = F.side == 0 ? l.Gp : l.Gpt;
         const float* Ht = F.side == 0 ? l.Gpt : l.Gp;
+        if (F.chain) {
+            c->chain.push_back(fi);
+            continue;
+        }
+        c->grouped.push_back(fi);
         if (F.expl) {
             add_explicit(c, F, fd[fi], Hr);
         } else {
             const auto& L = c->layers[F.layer];
             const FactorHost& O = c->factors[F.side == 0 ? L.fR : L.fL];
-            const float* Mo = O.expl ? at<float>(c, O.off_w[0]) : nullptr;
+            const float* Mo = (O.expl && !O.chain) ? at<float>(c, O.off_w[0]) : nullptr;
             F.nparts = add_factored(c, F, fd[fi], Hr, Ht, Mo);
             fd[fi].nparts = F.nparts;
         }
@@ -749,6 +776,15 @@ std::string check_tables(const jorge_ctx* c, const std::vector<FactorDev>& fd) {
     for (const FactorDev& F : fd)
         if (!in_buffer(c, F.partials, (int64_t)F.nparts * (int64_t)sizeof(double)) || F.nparts < 1)
             return "factor partials";
+    for (int fi : c->chain) {  // lds_chain_kernel: A (dp x dp), H (dp x kp), scalars
+        const FactorDev& F = fd[fi];
+        if (F.dp > kChainMax || F.dp % 32 || F.kp % kSlab || F.kp < kSlab ||
+            !in_buffer(c, F.A, (int64_t)F.dp * F.dp * (int64_t)sizeof(float)) ||
+            !in_buffer(c, F.H, (int64_t)F.dp * F.kp * (int64_t)sizeof(float)) ||
+            !in_buffer(c, F.sc, (int64_t)sizeof(FactorScalars)))
+            return "lds chain factor";
+    }
+    if (c->grouped.size() + c->chain.size() != fd.size()) return "factor lists";
     return "";
 }
 
@@ -832,6 +868,11 @@ void free_ctx(jorge_ctx* c) {
     if (c->dstage) (void)hipFree(c->dstage);
     if (c->dflat) (void)hipFree(c->dflat);
     if (c->dsym) (void)hipFree(c->dsym);
+    if (c->dgrouped) (void)hipFree(c->dgrouped);
+    if (c->dchain) (void)hipFree(c->dchain);
+    if (c->ev_fork) (void)hipEventDestroy(c->ev_fork);
+    if (c->ev_join) (void)hipEventDestroy(c->ev_join);
+    if (c->side) (void)hipStreamDestroy(c->side);
     if (c->arena) (void)hipFree(c->arena);
     for (auto& l : c->pending) {
         (void)hipEventDestroy(l.start);
@@ -849,11 +890,21 @@ jorge_status launch_stage(jorge_ctx* c, int stage, float beta1) {
 
 jorge_status run_update(jorge_ctx* c, double beta2) {
     jorge_status s;
+    if (!c->chain.empty()) {  // concurrent with the levels: they touch none of its factors
+        JORGE_HIP(c, hipEventRecord(c->ev_fork, c->stream));
+        JORGE_HIP(c, hipStreamWaitEvent(c->side, c->ev_fork, 0));
+        TimedLaunch tl(c, ST_LDS_CHAIN, c->side);
+        hipLaunchKernelGGL(lds_chain_kernel, dim3((unsigned)c->chain.size()), dim3(kGemmThreads), 0, c->side,
+                           c->dfactors, c->dchain, beta2, (int)c->hp.beta_mode, (int)c->hp.symmetrize);
+        tl.finish();
+        JORGE_HIP(c, hipGetLastError());
+        JORGE_HIP(c, hipEventRecord(c->ev_join, c->side));
+    }
     for (int lv : kLevels) {
-        if (lv == ST_POLY) {  // every factor's nu is complete after chain5
+        if (lv == ST_POLY && !c->grouped.empty()) {  // every grouped factor's nu is complete after chain5
             TimedLaunch tl(c, ST_FFINAL);
-            hipLaunchKernelGGL(factor_finalize_kernel, dim3((unsigned)c->factors.size()), dim3(64), 0,
-                               c->stream, c->dfactors, beta2, (int)c->hp.beta_mode);
+            hipLaunchKernelGGL(factor_finalize_kernel, dim3((unsigned)c->grouped.size()), dim3(64), 0,
+                               c->stream, c->dfactors, c->dgrouped, beta2, (int)c->hp.beta_mode);
             tl.finish();
             JORGE_HIP(c, hipGetLastError());
         }
@@ -866,6 +917,7 @@ jorge_status run_update(jorge_ctx* c, double beta2) {
         tl.finish();
         JORGE_HIP(c, hipGetLastError());
     }
+    if (!c->chain.empty()) JORGE_HIP(c, hipStreamWaitEvent(c->stream, c->ev_join, 0));
     return JORGE_OK;
 }
 
@@ -904,6 +956,7 @@ jorge_status jorge_hparams_default(jorge_hparams* hp) {
     hp->symmetrize = 1;
     hp->factor_form = JORGE_FORM_AUTO;
     hp->split_k = 1;
+    hp->lds_chain_max = kChainMax;
     return JORGE_OK;
 }
 
@@ -939,6 +992,14 @@ jorge_status jorge_create(const jorge_shape* shapes, int32_t num_layers, const j
     if ((st = upload(c, c->stage_tiles, &c->dstage)) != JORGE_OK) return bail(st);
     if ((st = upload(c, c->flat_chunks, &c->dflat)) != JORGE_OK) return bail(st);
     if ((st = upload(c, c->sym_tiles, &c->dsym)) != JORGE_OK) return bail(st);
+    if ((st = upload(c, c->grouped, &c->dgrouped)) != JORGE_OK) return bail(st);
+    if ((st = upload(c, c->chain, &c->dchain)) != JORGE_OK) return bail(st);
+    if (!c->chain.empty()) {
+        if (hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking) != hipSuccess ||
+            hipEventCreateWithFlags(&c->ev_fork, hipEventDisableTiming) != hipSuccess ||
+            hipEventCreateWithFlags(&c->ev_join, hipEventDisableTiming) != hipSuccess)
+            return bail(JORGE_ERR_HIP);
+    }
     for (int i = 0; i < ST_COUNT; ++i)
         for (GemmStage* s : {&c->nt[i], &c->nn[i]})
             if ((st = upload_stage(c, *s)) != JORGE_OK) return bail(st);

@@ -93,11 +93,12 @@ __device__ __forceinline__ FactorScalars factor_scalars(double nu, double beta2,
 }
 
 // nu = ||X||_F from the per-tile partial sums, then the factor's scalars.
-// One wave per factor. The factored form's partials are terms of an inner
+// One wave per factor of the list (the factors of the grouped levels). The factored form's partials are terms of an inner
 // product of two positive semidefinite matrices whose exact sum is ||X||_F^2;
 // a sum that rounding left below zero is read as zero.
-__global__ void factor_finalize_kernel(const FactorDev* __restrict__ f, double beta2, int mode) {
-    const FactorDev F = f[blockIdx.x];
+__global__ void factor_finalize_kernel(const FactorDev* __restrict__ f, const int* __restrict__ list,
+                                       double beta2, int mode) {
+    const FactorDev F = f[list[blockIdx.x]];
     const double nu = sqrt(fmax(0.0, wave_sum_array(F.partials, F.nparts)));
     if (threadIdx.x == 0) *F.sc = factor_scalars(nu, beta2, mode);
 }
@@ -152,6 +153,168 @@ __global__ __launch_bounds__(kEwThreads) void symmetrize_kernel(const FactorDev*
     __shared__ float zb[64][65];
     const SymTile st = tiles[blockIdx.x];
     symmetrize_pair(f[st.factor], st.ti, st.tj, symmetrize, za, zb);
+}
+
+// ---------------------------------------------------------------- LDS chain
+// The whole update of a small factor (padded size dp <= 64) by one
+// workgroup, in the explicit order of Algorithm 2 with every matrix resident
+// in LDS: M = H H^T (H streamed from global memory in 32-column slabs),
+// A^2, A^4, X = A^4 M with ||X||_F, (beta, c, s) (Appendix A.1, Eq. 8-9),
+// P = I - (c/4) X + (5c^2/32) X X (Eq. 6), Z = s A P and A <- (Z + Z^T)/2
+// (or Z). One launch replaces the five grouped levels for these factors.
+// Each of the four waves owns one 32 x 32 block of a 64 x 64 product
+// (v_mfma_f32_32x32x2_f32); blocks outside dp are skipped.
+constexpr int kChainMax = 64;
+constexpr int kChainLd = kChainMax + 1;          // LDS row stride: column reads hit 32 distinct banks
+constexpr int kChainMat = kChainMax * kChainLd;  // floats per LDS matrix
+constexpr int kChainSlabLd = kSlab + 1;
+
+struct ChainLds {
+    float A[kChainMat];
+    float M[kChainMat];
+    float T1[kChainMat];
+    float T2[kChainMat];
+    float H[kChainMax * kChainSlabLd];
+    double red[4];
+    float coef[3];  // a, b, s
+};
+
+// acc += A (rows wy*32.., lda) x B (cols wx*32.., ldb) over k in [0, K): both
+// operands in LDS; BT reads B transposed (B[k][col] = Bm[col][k]).
+// K is a multiple of 32; each group of 16 k has all its LDS reads issued
+// before its 8 MFMAs.
+template <bool BT>
+__device__ __forceinline__ void chain_mma(const float* a, int lda, const float* b, int ldb, int K, int wy, int wx,
+                                          f32x16& acc) {
+    const int lane = threadIdx.x & 63, r = lane & 31, h = lane >> 5;
+    for (int t0 = 0; t0 < K; t0 += 16) {
+        float av[8], bv[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int t = t0 + 2 * u + h;
+            av[u] = a[(wy * 32 + r) * lda + t];
+            bv[u] = BT ? b[(wx * 32 + r) * ldb + t] : b[t * ldb + wx * 32 + r];
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av[u], bv[u], acc, 0, 0, 0);
+    }
+}
+
+// C (LDS) = the wave's accumulator block; f(row, col, value) gives the stored value.
+template <typename Fn>
+__device__ __forceinline__ void chain_store(float* c, int wy, int wx, const f32x16& acc, Fn f) {
+    const int lane = threadIdx.x & 63, h = lane >> 5;
+    const int col = wx * 32 + (lane & 31);
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+        const int row = wy * 32 + 8 * (e >> 2) + 4 * h + (e & 3);
+        c[row * kChainLd + col] = f(row, col, acc[e]);
+    }
+}
+
+__global__ __launch_bounds__(kGemmThreads) void lds_chain_kernel(const FactorDev* __restrict__ f,
+                                                                 const int* __restrict__ list, double beta2,
+                                                                 int mode, int symmetrize) {
+    __shared__ __attribute__((aligned(16))) ChainLds sm;
+    const FactorDev F = f[list[blockIdx.x]];
+    const int dp = F.dp, tid = threadIdx.x;
+    const int wave = tid >> 6, wy = wave >> 1, wx = wave & 1;
+    const bool active = wy * 32 < dp && wx * 32 < dp;  // this wave's block lies inside dp x dp
+    auto zero = [](f32x16& a) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) a[e] = 0.0f;
+    };
+
+    for (int e = tid; e < dp * dp; e += kGemmThreads) sm.A[(e / dp) * kChainLd + e % dp] = F.A[e];
+
+    // M = H H^T, H streamed in slabs of 32 columns: each thread holds its
+    // (up to) 8 floats of the next slab in registers while the current one is
+    // multiplied. Thread t covers rows t/8 and 32 + t/8, columns 4 (t%8) .. +3.
+    f32x16 acc;
+    zero(acc);
+    const int hr = tid >> 3, hc = (tid & 7) * 4;
+    f32x4 hv[2];
+    auto load_h = [&](int k0) {
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+            const int r = hr + 32 * q;
+            if (r < dp) hv[q] = *(const f32x4*)(F.H + (size_t)r * F.kp + k0 + hc);
+        }
+    };
+    load_h(0);
+    for (int k0 = 0; k0 < F.kp; k0 += kSlab) {
+        __syncthreads();  // the previous slab's products are done with sm.H
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+            const int r = hr + 32 * q;
+            if (r < dp) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) sm.H[r * kChainSlabLd + hc + e] = hv[q][e];
+            }
+        }
+        __syncthreads();
+        if (k0 + kSlab < F.kp) load_h(k0 + kSlab);
+        if (active) chain_mma<true>(sm.H, kChainSlabLd, sm.H, kChainSlabLd, kSlab, wy, wx, acc);
+    }
+    if (active) chain_store(sm.M, wy, wx, acc, [](int, int, float v) { return v; });
+    __syncthreads();
+    // A^2 -> T1, A^4 -> T2
+    zero(acc);
+    if (active) {
+        chain_mma<false>(sm.A, kChainLd, sm.A, kChainLd, dp, wy, wx, acc);
+        chain_store(sm.T1, wy, wx, acc, [](int, int, float v) { return v; });
+    }
+    __syncthreads();
+    zero(acc);
+    if (active) {
+        chain_mma<false>(sm.T1, kChainLd, sm.T1, kChainLd, dp, wy, wx, acc);
+        chain_store(sm.T2, wy, wx, acc, [](int, int, float v) { return v; });
+    }
+    __syncthreads();
+    // X = A^4 M -> T1, with ||X||_F^2
+    zero(acc);
+    double part = 0.0;
+    if (active) {
+        chain_mma<false>(sm.T2, kChainLd, sm.M, kChainLd, dp, wy, wx, acc);
+        chain_store(sm.T1, wy, wx, acc, [&](int, int, float v) {
+            part += (double)v * (double)v;
+            return v;
+        });
+    }
+    const double nu2 = block_sum_256(part, sm.red);
+    if (tid == 0) {
+        const FactorScalars fs = factor_scalars(sqrt(nu2), beta2, mode);
+        *F.sc = fs;
+        sm.coef[0] = fs.a;
+        sm.coef[1] = fs.b;
+        sm.coef[2] = fs.sf;
+    }
+    __syncthreads();
+    const float a = sm.coef[0], b = sm.coef[1], sf = sm.coef[2];
+    // P = I - a X + b X X -> T2
+    zero(acc);
+    if (active) {
+        chain_mma<false>(sm.T1, kChainLd, sm.T1, kChainLd, dp, wy, wx, acc);
+        const int d = F.d;
+        chain_store(sm.T2, wy, wx, acc, [&](int row, int col, float v) {
+            const float id = (row == col && row < d) ? 1.0f : 0.0f;
+            return (id - a * sm.T1[row * kChainLd + col]) + b * v;
+        });
+    }
+    __syncthreads();
+    // Z = s A P -> M
+    zero(acc);
+    if (active) {
+        chain_mma<false>(sm.A, kChainLd, sm.T2, kChainLd, dp, wy, wx, acc);
+        chain_store(sm.M, wy, wx, acc, [&](int, int, float v) { return sf * v; });
+    }
+    __syncthreads();
+    // A <- (Z + Z^T)/2 or Z; fp32 addition commutes, so the result is bitwise symmetric.
+    for (int e = tid; e < dp * dp; e += kGemmThreads) {
+        const int r = e / dp, c = e % dp;
+        const float z = sm.M[r * kChainLd + c];
+        F.A[e] = symmetrize ? 0.5f * (z + sm.M[c * kChainLd + r]) : z;
+    }
 }
 
 // Per-layer norms of m and m_SGD from their partial sums, and the grafted

@@ -113,7 +113,9 @@ struct FactorDev {
     FactorScalars* sc;
     double* partials;      // per-tile partial sums of ||X||_F^2
     float* Z;              // explicit form: the unsymmetrized product s A P (dp x dp)
+    const float* H;        // the statistic's factor, row-major d x k (ld kp, zero padded)
     int d, dp;
+    int k, kp;
     int nparts;
     int explicit_form;     // 1: explicit powers; 0: factored through the statistic's factor
 };

@@ -21,8 +21,13 @@ pytestmark = pytest.mark.gpu
 STEP_TOL = 1e-5
 TRAJ_TOL = 1e-3
 # Evaluation orders of the factor update: the paper's explicit powers, the
-# factored order through the statistic's factor H, and the per-factor choice.
+# factored order through the statistic's factor H (both through the grouped
+# levels only), and the default per-factor choice, where factors of padded
+# size <= 64 take the one-workgroup LDS chain.
 FORMS = ("explicit", "factored", "auto")
+FORM_KW = {"explicit": dict(factor_form="explicit", lds_chain_max=0),
+           "factored": dict(factor_form="factored", lds_chain_max=0),
+           "auto": dict(factor_form="auto")}
 HP = dict(lr=0.1, beta2=0.9, beta1=0.9, weight_decay=5e-5)
 KINDS = ("L", "R", "mom", "mom_sgd")
 
@@ -94,24 +99,24 @@ def run_pair(shapes, steps, sigma, seed=0, check_every=None, tol=TRAJ_TOL, gpu_k
 ])
 def test_first_step_parity(shapes, form):
     say("first step", shapes, form)
-    _, _, _, _, worst = run_pair(shapes, 1, 1e-2, gpu_kw=dict(factor_form=form))
+    _, _, _, _, worst = run_pair(shapes, 1, 1e-2, gpu_kw=FORM_KW[form])
     say("  worst rel err", worst)
 
 
 @pytest.mark.parametrize("form", FORMS)
 def test_trajectory_64x576_100_steps(form):
     say("trajectory 64x576 x 100", form)
-    _, _, _, _, worst = run_pair([(64, 576)], 100, 1e-2, check_every=10, gpu_kw=dict(factor_form=form))
+    _, _, _, _, worst = run_pair([(64, 576)], 100, 1e-2, check_every=10, gpu_kw=FORM_KW[form])
     say("  worst rel err", worst)
 
 
 @pytest.mark.parametrize("form", FORMS)
 def test_trajectory_multitile_30_steps(form):
     say("trajectory (256x1152, 300x200) x 30", form)
-    run_pair([(256, 1152), (300, 200)], 30, 1e-3, check_every=15, gpu_kw=dict(factor_form=form))
+    run_pair([(256, 1152), (300, 200)], 30, 1e-3, check_every=15, gpu_kw=FORM_KW[form])
 
 
-@pytest.mark.parametrize("form", ["explicit", "factored"])
+@pytest.mark.parametrize("form", FORMS)
 @pytest.mark.parametrize("t_inject", [2, 5, 20, 50])
 def test_per_step_parity_from_injected_state(t_inject, form):
     """Oracle state after t-1 steps (rounded to fp32) is injected; one step on both."""
@@ -125,7 +130,7 @@ def test_per_step_parity_from_injected_state(t_inject, form):
     for k in ("L", "R", "m", "m_sgd"):
         setattr(st, k, getattr(st, k).astype(np.float32).astype(np.float64))
     po = [po[0].astype(np.float32).astype(np.float64)]
-    opt = Jorge(shapes, factor_form=form)
+    opt = Jorge(shapes, **FORM_KW[form])
     for k, v in oracle_state(orc, 0).items():
         opt.set_state(0, k, to_dev(v))
     opt.t = t_inject - 1
@@ -136,13 +141,13 @@ def test_per_step_parity_from_injected_state(t_inject, form):
     compare(opt, orc, pg, po, STEP_TOL, f"injected step {t_inject}")
 
 
-@pytest.mark.parametrize("form", ["explicit", "factored"])
+@pytest.mark.parametrize("form", FORMS)
 @pytest.mark.parametrize("mode,sigma,beta2", [("fixed", 1e-4, 0.9), ("dynamic", 1e-2, 0.9),
                                               ("clamped", 3e-4, 0.9)])
 def test_beta_modes(mode, sigma, beta2, form):
     say("mode", mode, form)
     code = {"fixed": 0, "dynamic": 1, "clamped": 2}[mode]
-    run_pair([(48, 96), (70, 40)], 6, sigma, check_every=3, gpu_kw=dict(beta_mode=mode, factor_form=form),
+    run_pair([(48, 96), (70, 40)], 6, sigma, check_every=3, gpu_kw=dict(FORM_KW[form], beta_mode=mode),
              orc_kw=dict(beta_mode=code), hp=dict(HP, beta2=beta2))
 
 
@@ -150,7 +155,7 @@ def test_beta_modes(mode, sigma, beta2, form):
 def test_literal_mode_without_symmetrization(form):
     say("literal mode", form)
     run_pair([(48, 96), (160, 40), (300, 130)], 6, 1e-2, check_every=3,
-             gpu_kw=dict(symmetrize=False, factor_form=form), orc_kw=dict(symmetrize=False))
+             gpu_kw=dict(FORM_KW[form], symmetrize=False), orc_kw=dict(symmetrize=False))
 
 
 def test_without_grafting():
@@ -181,8 +186,8 @@ def test_update_interval_parity_and_frozen_factors():
 def test_factors_bitwise_symmetric_and_deterministic(form):
     shapes = [(200, 300), (64, 147), (130, 600)]
     say("symmetry + determinism", form)
-    a = run_pair(shapes, 4, 1e-2, gpu_kw=dict(factor_form=form))
-    b = run_pair(shapes, 4, 1e-2, gpu_kw=dict(factor_form=form))
+    a = run_pair(shapes, 4, 1e-2, gpu_kw=FORM_KW[form])
+    b = run_pair(shapes, 4, 1e-2, gpu_kw=FORM_KW[form])
     for l in range(len(shapes)):
         for k in ("L", "R"):
             A = a[0].get_state(l, k)
@@ -214,11 +219,11 @@ def test_grouping_invariance():
         assert torch.equal(pg[l], ps[l])
 
 
-@pytest.mark.parametrize("form", ["explicit", "factored"])
+@pytest.mark.parametrize("form", FORMS)
 def test_zero_gradient_is_exact_beta_scaling(form):
     shapes = [(64, 96)]
     say("G = 0", form)
-    opt, _, pg, _, _ = run_pair(shapes, 3, 1e-2, gpu_kw=dict(factor_form=form))
+    opt, _, pg, _, _ = run_pair(shapes, 3, 1e-2, gpu_kw=FORM_KW[form])
     before = {k: opt.get_state(0, k) for k in KINDS}
     theta = pg[0].clone()
     opt.step(pg, [torch.zeros(shapes[0], device="cuda")], 0.1, 0.8, 0.9, 1e-3)
@@ -337,17 +342,44 @@ def test_split_k_parity_and_determinism(form):
     """Levels with few, long tiles split K; the fixup sums the parts in a fixed order."""
     shapes = [(128, 2048), (64, 4096)]
     say("split-K", form)
-    probe = Jorge(shapes, factor_form=form)
+    probe = Jorge(shapes, **FORM_KW[form])
     probe.set_timing(True)
     probe.step([torch.zeros(s, device="cuda") for s in shapes],
                [to_dev(gradient(0, l, 1, s, 1e-2)) for l, s in enumerate(shapes)], **HP)
     assert probe.read_timing()["split_fixup"][1] >= 1          # the plan does split
-    a = run_pair(shapes, 3, 1e-2, gpu_kw=dict(factor_form=form))                 # vs the oracle
-    b = run_pair(shapes, 3, 1e-2, gpu_kw=dict(factor_form=form))
-    c = run_pair(shapes, 3, 1e-2, gpu_kw=dict(factor_form=form, split_k=False))
+    a = run_pair(shapes, 3, 1e-2, gpu_kw=FORM_KW[form])                 # vs the oracle
+    b = run_pair(shapes, 3, 1e-2, gpu_kw=FORM_KW[form])
+    c = run_pair(shapes, 3, 1e-2, gpu_kw=dict(FORM_KW[form], split_k=False))
     for l in range(len(shapes)):
         assert torch.equal(a[2][l], b[2][l])
         for k in KINDS:
             x, y, z = (r[0].get_state(l, k) for r in (a, b, c))
             assert torch.equal(x, y), (l, k)                     # deterministic
             assert rel(x.cpu().numpy(), z.cpu().numpy()) < 1e-5, (l, k)   # split vs unsplit rounding
+
+
+@pytest.mark.parametrize("symmetrize", [True, False])
+def test_lds_chain_small_factors(symmetrize):
+    """Factors of padded size <= 64 run their whole update in one workgroup, in LDS."""
+    shapes = [(64, 576), (32, 256), (5, 3), (64, 64), (40, 1), (33, 200), (200, 48), (64, 4608)]
+    say("LDS chain, symmetrize", symmetrize)
+    opt = Jorge(shapes, symmetrize=symmetrize)
+    opt.set_timing(True)
+    opt.step([torch.zeros(s, device="cuda") for s in shapes],
+             [to_dev(gradient(0, l, 1, s, 1e-2)) for l, s in enumerate(shapes)], **HP)
+    assert opt.read_timing()["lds_chain"][1] == 1
+    a = run_pair(shapes, 6, 1e-2, check_every=3, gpu_kw=dict(symmetrize=symmetrize),
+                 orc_kw=dict(symmetrize=symmetrize))
+    b = run_pair(shapes, 6, 1e-2, gpu_kw=dict(symmetrize=symmetrize, lds_chain_max=0),
+                 orc_kw=dict(symmetrize=symmetrize))
+    for l in range(len(shapes)):
+        for k in KINDS:
+            x, y = a[0].get_state(l, k), b[0].get_state(l, k)
+            assert rel(x.cpu().numpy(), y.cpu().numpy()) < 1e-5, (l, k)
+        if symmetrize:
+            for k in ("L", "R"):
+                A = a[0].get_state(l, k)
+                assert torch.equal(A, A.T), (l, k)
+        d = a[0].read_diag(l)
+        assert d["nu_L"] == pytest.approx(a[1].last_diag[l]["nu_L"], rel=1e-5)
+        assert d["nu_R"] == pytest.approx(a[1].last_diag[l]["nu_R"], rel=1e-5)
