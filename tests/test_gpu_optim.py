@@ -1,0 +1,119 @@
+"""GPU checks of the torch.optim front end: it is exactly the library's grouped
+step on the matrix parameters, column order does not matter (channels-last
+weights are used in place), vectors follow heavy-ball SGD, and its state
+round-trips."""
+import io
+
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from paper_2310_12298_amd.jorge import Jorge  # noqa: E402
+from paper_2310_12298_amd.optim import JorgeOptimizer  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+HP = dict(lr=0.1, beta1=0.9, beta2=0.9, weight_decay=5e-4)
+
+
+def model(seed=0):
+    torch.manual_seed(seed)
+    nn = torch.nn
+    return nn.Sequential(nn.Conv2d(3, 16, 3, bias=False), nn.BatchNorm2d(16), nn.ReLU(), nn.Conv2d(16, 32, 3),
+                         nn.AdaptiveAvgPool2d(1), nn.Flatten(), nn.Linear(32, 10)).cuda()
+
+
+def grads_for(m, t):
+    gen = torch.Generator(device="cuda").manual_seed(1000 + t)
+    for p in m.parameters():
+        p.grad = torch.randn(p.shape, generator=gen, device="cuda").mul_(1e-2).to(memory_format=torch.contiguous_format)
+
+
+def test_matches_direct_library_steps_bitwise():
+    m = model()
+    ref = [p.detach().clone() for p in m.parameters() if p.dim() >= 2]
+    opt = JorgeOptimizer(m.parameters(), **HP)
+    jr = Jorge([(p.shape[0], p.numel() // p.shape[0]) for p in ref])
+    for t in range(1, 5):
+        grads_for(m, t)
+        g2 = [p.grad.clone() for p in m.parameters() if p.dim() >= 2]
+        opt.step()
+        jr.step([r.view(r.shape[0], -1) for r in ref], [g.view(g.shape[0], -1) for g in g2], HP["lr"],
+                HP["beta2"], HP["beta1"], HP["weight_decay"])
+    torch.cuda.synchronize()
+    for p, r in zip([p for p in m.parameters() if p.dim() >= 2], ref):
+        assert torch.equal(p.detach(), r)
+
+
+def test_vectors_follow_heavy_ball_sgd():
+    m = model()
+    vec0 = [p.detach().clone() for p in m.parameters() if p.dim() < 2]
+    opt = JorgeOptimizer(m.parameters(), vector_weight_decay=1e-4, **HP)
+    bufs = None
+    for t in range(1, 4):
+        grads_for(m, t)
+        gv = [p.grad.clone() for p in m.parameters() if p.dim() < 2]
+        opt.step()
+        gv = [g + 1e-4 * v for g, v in zip(gv, vec0)]
+        bufs = gv if bufs is None else [0.9 * b + g for b, g in zip(bufs, gv)]
+        vec0 = [v - 0.1 * b for v, b in zip(vec0, bufs)]
+    for p, v in zip([p for p in m.parameters() if p.dim() < 2], vec0):
+        assert torch.allclose(p.detach(), v, rtol=1e-6, atol=1e-7)
+
+
+def test_channels_last_weights_give_the_same_update():
+    """Permuting a matrix's columns permutes R_hat alike: the update is the same up to rounding."""
+    a, b = model(), model()
+    b = b.to(memory_format=torch.channels_last)
+    oa, ob = JorgeOptimizer(a.parameters(), **HP), JorgeOptimizer(b.parameters(), **HP)
+    for t in range(1, 4):
+        grads_for(a, t)
+        for pa, pb in zip(a.parameters(), b.parameters()):
+            pb.grad = pa.grad.clone().to(memory_format=torch.channels_last if pa.dim() == 4 else torch.preserve_format)
+        oa.step()
+        ob.step()
+    for pa, pb in zip(a.parameters(), b.parameters()):
+        x, y = pa.detach().double(), pb.detach().double()
+        assert (torch.linalg.norm(x - y) / torch.linalg.norm(x)).item() < 1e-5
+
+
+def test_state_dict_round_trip_resumes_bitwise():
+    a = model()
+    oa = JorgeOptimizer(a.parameters(), **HP)
+    for t in range(1, 3):
+        grads_for(a, t)
+        oa.step()
+    # Through a serialized copy, as a checkpoint would be (a live state_dict
+    # shares the momentum buffers of the optimizer it came from).
+    buf = io.BytesIO()
+    torch.save(oa.state_dict(), buf)
+    buf.seek(0)
+    sd = torch.load(buf, weights_only=True)
+    b = model()
+    b.load_state_dict(a.state_dict())
+    ob = JorgeOptimizer(b.parameters(), **HP)
+    ob.load_state_dict(sd)
+    for t in range(3, 6):
+        grads_for(a, t)
+        for pa, pb in zip(a.parameters(), b.parameters()):
+            pb.grad = pa.grad.clone()
+        oa.step()
+        ob.step()
+    for pa, pb in zip(a.parameters(), b.parameters()):
+        assert torch.equal(pa.detach(), pb.detach())
+
+
+def test_learning_rate_scheduler_drives_the_step():
+    a, b = model(), model()
+    oa = JorgeOptimizer(a.parameters(), **HP)
+    sched = torch.optim.lr_scheduler.MultiStepLR(oa, milestones=[2], gamma=0.1)
+    ob = JorgeOptimizer(b.parameters(), **HP)
+    for t in range(1, 5):
+        grads_for(a, t)
+        for pa, pb in zip(a.parameters(), b.parameters()):
+            pb.grad = pa.grad.clone()
+        oa.step()
+        sched.step()
+        ob.param_groups[0]["lr"] = 0.1 if t <= 2 else 0.01   # MultiStepLR drops after two scheduler steps
+        ob.step()
+    for pa, pb in zip(a.parameters(), b.parameters()):
+        assert torch.equal(pa.detach(), pb.detach())

@@ -1,0 +1,46 @@
+"""Host logic of the torch.optim front end (no GPU): single-shot tuning rules
+of Section 4 and how parameters map onto the library's matrices."""
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from paper_2310_12298_amd.optim import matrix_view, sgd_to_jorge, split_params, step_decay_milestones  # noqa: E402
+
+
+def test_weight_decay_transfer_is_ten_times_sgd_at_momentum_0_9():
+    # Section 4: lambda_Jorge = lambda_SGD / (1 - beta_SGD); the paper uses 10x SGD's at beta 0.9.
+    hp = sgd_to_jorge(lr=0.1, momentum=0.9, weight_decay=5e-5)
+    assert hp["weight_decay"] == pytest.approx(5e-4, rel=1e-12)
+    assert hp["lr"] == 0.1 and hp["beta1"] == 0.9
+    assert sgd_to_jorge(0.2, 0.0, 1e-4)["weight_decay"] == pytest.approx(1e-4)
+    assert sgd_to_jorge(0.2, 0.5, 1e-4)["weight_decay"] == pytest.approx(2e-4)
+    with pytest.raises(ValueError):
+        sgd_to_jorge(0.1, 1.0, 1e-4)
+
+
+def test_step_decay_at_one_and_two_thirds():
+    assert step_decay_milestones(90) == [30, 60]
+    assert step_decay_milestones(100) == [33, 66]
+    with pytest.raises(ValueError):
+        step_decay_milestones(2)
+
+
+def test_matrix_view_of_weights_and_layouts():
+    w = torch.empty(64, 3, 7, 7)
+    assert matrix_view(w) == (64, 147)
+    cl = w.to(memory_format=torch.channels_last)      # (out, kh, kw, in) in memory
+    assert matrix_view(cl) == (64, 147)
+    assert matrix_view(torch.empty(1000, 2048)) == (1000, 2048)
+    with pytest.raises(ValueError):
+        matrix_view(torch.empty(64, 128)[:, ::2])      # not dense
+    with pytest.raises(ValueError):
+        matrix_view(torch.empty(128, 64).t())          # dimension 0 not outermost
+    with pytest.raises(ValueError):
+        matrix_view(torch.empty(10))
+
+
+def test_split_params_by_dimension():
+    ps = [torch.empty(4, 3, 3, 3), torch.empty(4), torch.empty(10, 4), torch.empty(10), torch.empty(())]
+    mats, vecs = split_params(ps)
+    assert [tuple(p.shape) for p in mats] == [(4, 3, 3, 3), (10, 4)]
+    assert [tuple(p.shape) for p in vecs] == [(4,), (10,), ()]
