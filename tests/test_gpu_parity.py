@@ -383,3 +383,47 @@ def test_lds_chain_small_factors(symmetrize):
         d = a[0].read_diag(l)
         assert d["nu_L"] == pytest.approx(a[1].last_diag[l]["nu_L"], rel=1e-5)
         assert d["nu_R"] == pytest.approx(a[1].last_diag[l]["nu_R"], rel=1e-5)
+
+
+# ---------------------------------------------------------------- full-size workloads
+# The bench's workloads in the bench's launch configuration (one context over
+# all layers, default options), after two steps, against the fp64 oracle on
+# every layer (ResNet-50, many-small) or on sampled layers (large dense).
+
+def _workload_parity(name, sample=None, steps=2):
+    from paper_2310_12298_amd.workloads import CONFIGS
+    shapes, sigma, _ = CONFIGS[name]
+    layers = range(len(shapes)) if sample is None else sample
+    say("workload", name, "layers checked", len(list(layers)))
+    opt = Jorge(shapes)
+    pg = [to_dev(initial_params(0, l, s)) for l, s in enumerate(shapes)]
+    orcs = {l: JorgeOracle([shapes[l]]) for l in layers}
+    po = {l: [initial_params(0, l, shapes[l]).astype(np.float64)] for l in layers}
+    for t in range(1, steps + 1):
+        G = {l: gradient(0, l, t, s, sigma) for l, s in enumerate(shapes)}
+        opt.step(pg, [to_dev(G[l]) for l in range(len(shapes))], **HP)
+        for l in layers:
+            po[l] = orcs[l].step(po[l], [G[l]], **HP)
+    worst = 0.0
+    for l in layers:
+        st = orcs[l].layers[0]
+        errs = {k: rel(opt.get_state(l, k).cpu().numpy(), v)
+                for k, v in (("L", st.L), ("R", st.R), ("mom", st.m), ("mom_sgd", st.m_sgd))}
+        errs["theta"] = rel(pg[l].cpu().numpy(), po[l][0])
+        worst = max(worst, max(errs.values()))
+        assert max(errs.values()) <= TRAJ_TOL, (name, l, shapes[l], errs)
+    say("  worst rel err", worst)
+    return worst
+
+
+def test_workload_resnet50_all_layers():
+    assert _workload_parity("resnet50") < 1e-4
+
+
+def test_workload_many_small_all_layers():
+    assert _workload_parity("many_small") < 1e-4
+
+
+def test_workload_large_dense_sampled_layers():
+    # one 4096 x 4096 and one 4096 x 1024 layer of the 16 (the oracle step of each takes seconds)
+    assert _workload_parity("large_dense", sample=[3, 12], steps=1) < 1e-4
