@@ -80,7 +80,10 @@ def measured_traffic(config):
     return float(vals["traffic_bytes_per_launch"]) if "traffic_bytes_per_launch" in vals else None
 
 
-GEMM_STAGES = ("gram", "pow4", "xform", "chain4", "chain5", "poly", "update", "precond_L", "precond_R")
+GEMM_STAGES = ("gram", "pow4", "xform", "chain4", "chain5", "poly", "update", "uprecond_L", "uprecond_R",
+               "precond_L", "precond_R")
+# Preconditioning of steps that do not update the factors; every other GEMM stage runs on update steps.
+NON_UPDATE_STAGES = ("precond_L", "precond_R")
 # Launches of the grouped GEMM's split-tile fixup: their time is part of the GEMM stages' time.
 FIXUP_STAGE = "split_fixup"
 
@@ -201,7 +204,7 @@ def main():
         raise SystemExit("no factor update in the timed steps; use more steps or a smaller interval")
     # Algorithmic flops of each stage in one factor-updating step, from the library's launch tables.
     flops = opt.stage_flops()
-    ran = {k: (updates if k not in ("precond_L", "precond_R") else steps) for k in GEMM_STAGES}
+    ran = {k: (steps - updates if k in NON_UPDATE_STAGES else updates) for k in GEMM_STAGES}
     per_stage = {}
     for k, (ms, n) in timing.items():
         e = {"ms_per_launch": ms / n if n else 0.0, "launches": n}

@@ -106,6 +106,11 @@ typedef struct jorge_hparams {
                                  explicit order in one workgroup with every matrix in LDS
                                  (one launch for all of them) instead of the grouped levels;
                                  0 disables. In [0, 64]. Default 64. */
+    int32_t precond_lowrank;  /* 1: on update steps, a factored factor A with d > 3k preconditions
+                                 through A_new H = s A H - (s/2)(W H^T H + H W^T H), built from
+                                 the update's own terms (about 6 k^2 d flops instead of a d x d
+                                 product; the same result up to fp32 rounding); needs
+                                 symmetrize = 1. 0: always the direct products. Default 1. */
 } jorge_hparams;
 
 /* Largest rows or cols of a layer the library accepts. */

@@ -64,11 +64,13 @@ namespace {
 // Timed stages: one per dependency level of the update (see above).
 enum Stage : int {
     ST_STAGEIN = 0, ST_GRAM, ST_POW4, ST_XFORM, ST_CHAIN4, ST_CHAIN5, ST_FFINAL, ST_POLY, ST_UPDATE,
-    ST_SYMM, ST_PRECOND_L, ST_PRECOND_R, ST_LFINAL, ST_WEIGHT, ST_FIXUP, ST_LDS_CHAIN, ST_COUNT
+    ST_SYMM, ST_PRECOND_L, ST_PRECOND_R, ST_LFINAL, ST_WEIGHT, ST_FIXUP, ST_LDS_CHAIN, ST_UPRECOND_L,
+    ST_UPRECOND_R, ST_COUNT
 };
 const char* const kStageNames[ST_COUNT] = {
     "stage_in", "gram", "pow4", "xform", "chain4", "chain5", "factor_finalize", "poly", "update",
-    "symmetrize", "precond_L", "precond_R", "layer_finalize", "weight", "split_fixup", "lds_chain"};
+    "symmetrize", "precond_L", "precond_R", "layer_finalize", "weight", "split_fixup", "lds_chain",
+    "uprecond_L", "uprecond_R"};
 // The GEMM levels of an update step, in launch order.
 constexpr int kLevels[] = {ST_GRAM, ST_POW4, ST_XFORM, ST_CHAIN4, ST_CHAIN5, ST_POLY, ST_UPDATE};
 
@@ -105,6 +107,10 @@ struct FactorHost {
     int layer, side, d, dp, k, kp;
     bool expl = true;
     bool chain = false;  // small: the whole update in one workgroup (lds_chain_kernel), explicit order
+    // Low-rank preconditioning on update steps (factored, symmetric, d > 3k): the
+    // layer's A_new H comes from the chain's A H, W, Q and H^T W (see add_factored).
+    bool lrp = false;
+    size_t off_y1 = 0, off_wt = 0, off_v2t = 0, off_xa = 0;
     size_t off_A, off_part, off_sc;
     size_t off_w[4];
     int nparts = 0;
@@ -354,6 +360,7 @@ jorge_status validate_hparams(const jorge_hparams* hp) {
         return JORGE_ERR_INVALID_ARGUMENT;
     if (hp->split_k != 0 && hp->split_k != 1) return JORGE_ERR_INVALID_ARGUMENT;
     if (hp->lds_chain_max < 0 || hp->lds_chain_max > kChainMax) return JORGE_ERR_INVALID_ARGUMENT;
+    if (hp->precond_lowrank != 0 && hp->precond_lowrank != 1) return JORGE_ERR_INVALID_ARGUMENT;
     return JORGE_OK;
 }
 
@@ -412,6 +419,16 @@ size_t plan(jorge_ctx* c) {
                 F.off_w[2] = take(kk);
                 F.off_w[3] = take(kk);
                 F.nparts = tile_count(F.kp, F.kp);
+            }
+            // A_new H (d x k) replaces a d x d product in the preconditioning when
+            // 6 k^2 d < 2 d^2 k, i.e. d > 3 k (both orders then cost 2 k^2 d more).
+            F.lrp = !F.expl && sym && c->hp.precond_lowrank && (int64_t)F.d > 3 * (int64_t)F.k;
+            if (F.lrp) {
+                const size_t kd = (size_t)F.kp * F.dp * sizeof(float), kk = (size_t)F.kp * F.kp * sizeof(float);
+                F.off_y1 = take(kd);   // A H, d x k
+                F.off_wt = take(kd);   // W^T, k x d
+                F.off_v2t = take(kk);  // H^T W, k x k
+                F.off_xa = take(kd);   // A_new H, d x k
             }
             F.off_part = take((size_t)F.nparts * sizeof(double));
             F.off_sc = take(sizeof(FactorScalars));
@@ -507,6 +524,9 @@ int add_factored(jorge_ctx* c, const FactorHost& F, const FactorDev& fd, const f
     for (int j = 0; j < 4; ++j) {
         GemmProblem y = product(src, dp, A, dp, kp, dp, dp);
         y.C = dst[j]; y.ldc = dp; y.flags = EF_STORE;
+        if (j == 0 && F.lrp) {  // keep A H (= Yt_1^T) for the preconditioning
+            y.C2 = at<float>(c, F.off_y1); y.ldc2 = kp; y.flags |= EF_STORE_T;
+        }
         add_problem(c->nt[lvl[j]], y, 2 * k * d * d);
         src = dst[j];
     }
@@ -533,7 +553,24 @@ int add_factored(jorge_ctx* c, const FactorHost& F, const FactorDev& fd, const f
     GemmProblem w = product(P0, kp, S, kp, dp, kp, kp);
     w.C = P1; w.ldc = kp; w.X = P0; w.ldx = kp; w.sc = fd.sc;
     w.flags = EF_STORE | EF_READX; w.coef = CO_WMIX;
+    if (F.lrp) {  // and W^T for H^T W
+        w.C2 = at<float>(c, F.off_wt); w.ldc2 = dp; w.flags |= EF_STORE_T;
+    }
     add_problem(c->nt[ST_POLY], w, 2 * d * k * k);
+    if (F.lrp) {
+        // H^T W (k x k) in the update level, beside the SYR2K.
+        GemmProblem v = product(Ht, dp, at<float>(c, F.off_wt), dp, kp, kp, dp);
+        v.C = at<float>(c, F.off_v2t); v.ldc = kp; v.flags = EF_STORE;
+        add_problem(c->nt[ST_UPDATE], v, 2 * k * k * d);
+        // A_new H = s A H - (s/2)(W H^T H + H W^T H), in the first preconditioning level:
+        // K segments [W | H] x [Q | (H^T W)^T]^T (Q is symmetric), coefficients of the SYR2K.
+        GemmProblem x = product(P1, kp, Q, kp, dp, kp, kp);
+        x.A2 = Hr; x.lda2 = kp; x.B2 = at<float>(c, F.off_v2t); x.ldb2 = kp; x.K = 2 * kp;
+        x.C = at<float>(c, F.off_xa); x.ldc = kp;
+        x.X = at<float>(c, F.off_y1); x.ldx = kp; x.sc = fd.sc;
+        x.flags = EF_STORE | EF_READX; x.coef = CO_SYR2K;
+        add_problem(c->nt[ST_UPRECOND_L], x, 2 * d * k * 2 * k);
+    }
     // A <- s A - (s/2)(W H^T + H W^T) (symmetric, in place) or s A - s W H^T.
     GemmProblem u = product(P1, kp, Hr, kp, dp, dp, kp);
     u.C = A; u.ldc = dp; u.X = A; u.ldx = dp; u.sc = fd.sc; u.flags = EF_STORE | EF_READX;
@@ -623,7 +660,9 @@ void build_tables(jorge_ctx* c, std::vector<LayerDev>& ld, std::vector<FactorDev
         } else {
             const auto& L = c->layers[F.layer];
             const FactorHost& O = c->factors[F.side == 0 ? L.fR : L.fL];
-            const float* Mo = (O.expl && !O.chain) ? at<float>(c, O.off_w[0]) : nullptr;
+            // (Not for a low-rank-preconditioning factor: it reads Q after the poly level,
+            // where the explicit factor's statistic buffer receives P^T.)
+            const float* Mo = (O.expl && !O.chain && !F.lrp) ? at<float>(c, O.off_w[0]) : nullptr;
             F.nparts = add_factored(c, F, fd[fi], Hr, Ht, Mo);
             fd[fi].nparts = F.nparts;
         }
@@ -640,15 +679,34 @@ void build_tables(jorge_ctx* c, std::vector<LayerDev>& ld, std::vector<FactorDev
         const auto& L = c->layers[li];
         const LayerDev& l = ld[li];
         const double m = L.m, n = L.n;
-        // T = L_hat G: B^T = Gpt (both K-major)
+        const FactorHost& FL = c->factors[L.fL];
+        const FactorHost& FR = c->factors[L.fR];
+        // Non-update steps (and update steps of layers without a low-rank factor):
+        // T = L_hat G (B^T = Gpt, both K-major), then G~ = T R_hat fused with the
+        // momentum (R_hat is its own K-major B when symmetric).
         GemmProblem a = product(fd[L.fL].A, L.mp, l.Gpt, L.mp, L.mp, L.np, L.mp);
         a.C = l.T; a.ldc = L.np; a.flags = EF_STORE;
-        add_problem(c->nt[ST_PRECOND_L], a, 2 * m * m * n);
-        // G~ = T R_hat fused with the momentum: R_hat is its own K-major B when symmetric.
         GemmProblem b = product(l.T, L.np, fd[L.fR].A, L.np, L.mp, L.np, L.np);
         b.mom = l.mom; b.ldmom = L.n; b.partials = l.part_m;
         b.valid_m = L.m; b.valid_n = L.n; b.flags = EF_MOMENTUM;
+        add_problem(c->nt[ST_PRECOND_L], a, 2 * m * m * n);
         add_problem(sym ? c->nt[ST_PRECOND_R] : c->nn[ST_PRECOND_R], b, 2 * m * n * n);
+        if (FR.lrp) {
+            // G R_new = (R_new G^T)^T is in the factor's x buffer (n x m); G~ = L_hat (G R_new).
+            GemmProblem g = product(fd[L.fL].A, L.mp, at<float>(c, FR.off_xa), L.mp, L.mp, L.np, L.mp);
+            g.mom = l.mom; g.ldmom = L.n; g.partials = l.part_m;
+            g.valid_m = L.m; g.valid_n = L.n; g.flags = EF_MOMENTUM;
+            add_problem(c->nt[ST_UPRECOND_R], g, 2 * m * m * n);
+        } else if (FL.lrp) {
+            // L_new G is in the factor's x buffer (m x n); G~ = (L_new G) R_hat.
+            GemmProblem g = product(at<float>(c, FL.off_xa), L.np, fd[L.fR].A, L.np, L.mp, L.np, L.np);
+            g.mom = l.mom; g.ldmom = L.n; g.partials = l.part_m;
+            g.valid_m = L.m; g.valid_n = L.n; g.flags = EF_MOMENTUM;
+            add_problem(c->nt[ST_UPRECOND_R], g, 2 * m * n * n);
+        } else {
+            add_problem(c->nt[ST_UPRECOND_L], a, 2 * m * m * n);
+            add_problem(sym ? c->nt[ST_UPRECOND_R] : c->nn[ST_UPRECOND_R], b, 2 * m * n * n);
+        }
     }
 }
 
@@ -957,6 +1015,7 @@ jorge_status jorge_hparams_default(jorge_hparams* hp) {
     hp->factor_form = JORGE_FORM_AUTO;
     hp->split_k = 1;
     hp->lds_chain_max = kChainMax;
+    hp->precond_lowrank = 1;
     return JORGE_OK;
 }
 
@@ -1057,8 +1116,9 @@ jorge_status jorge_step(jorge_ctx* c, float* const* params, const float* const* 
     }
     jorge_status s;
     if (update && (s = run_update(c, beta2)) != JORGE_OK) return s;
-    if ((s = launch_stage(c, ST_PRECOND_L, 0.f)) != JORGE_OK) return s;
-    if ((s = launch_stage(c, ST_PRECOND_R, (float)beta1)) != JORGE_OK) return s;
+    // Update steps take the preconditioning tables that reuse the update's low-rank terms.
+    if ((s = launch_stage(c, update ? ST_UPRECOND_L : ST_PRECOND_L, 0.f)) != JORGE_OK) return s;
+    if ((s = launch_stage(c, update ? ST_UPRECOND_R : ST_PRECOND_R, (float)beta1)) != JORGE_OK) return s;
     {
         TimedLaunch tl(c, ST_LFINAL);
         hipLaunchKernelGGL(layer_finalize_kernel, dim3(nl), dim3(64), 0, c->stream, c->dlayers, lr,

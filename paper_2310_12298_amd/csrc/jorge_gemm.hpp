@@ -563,6 +563,15 @@ __device__ __forceinline__ void gemm_epilogue(const GemmProblem& p, int tm, int 
                 part = masked ? epilogue_body<EF_STORE | EF_READX, false, true>(p, tm, tn, acc, ci, cx, cc)
                             : epilogue_body<EF_STORE | EF_READX, false, false>(p, tm, tn, acc, ci, cx, cc);
                 break;
+            case EF_STORE | EF_STORE_T:
+                part = masked ? epilogue_body<EF_STORE | EF_STORE_T, false, true>(p, tm, tn, acc, ci, cx, cc)
+                              : epilogue_body<EF_STORE | EF_STORE_T, false, false>(p, tm, tn, acc, ci, cx, cc);
+                break;
+            case EF_STORE | EF_STORE_T | EF_READX:
+                part = masked ? epilogue_body<EF_STORE | EF_STORE_T | EF_READX, false, true>(p, tm, tn, acc, ci, cx, cc)
+                              : epilogue_body<EF_STORE | EF_STORE_T | EF_READX, false, false>(p, tm, tn, acc, ci, cx,
+                                                                                              cc);
+                break;
             case EF_STORE | EF_READX | 256:
                 part = masked ? epilogue_body<EF_STORE | EF_READX, true, true>(p, tm, tn, acc, ci, cx, cc)
                             : epilogue_body<EF_STORE | EF_READX, true, false>(p, tm, tn, acc, ci, cx, cc);

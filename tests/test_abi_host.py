@@ -46,7 +46,7 @@ def test_hparams_default(lib):
     hp = J.HParams()
     assert lib.jorge_hparams_default(ctypes.byref(hp)) == 0
     assert (hp.eps, hp.precond_interval, hp.beta_mode, hp.graft, hp.symmetrize,
-            hp.factor_form, hp.split_k, hp.lds_chain_max) == (1e-6, 1, 2, 1, 1, 0, 1, 64)
+            hp.factor_form, hp.split_k, hp.lds_chain_max, hp.precond_lowrank) == (1e-6, 1, 2, 1, 1, 0, 1, 64, 1)
     assert lib.jorge_hparams_default(None) == ERR_INVALID
 
 
@@ -73,7 +73,8 @@ def test_create_rejects_oversize(lib):
                                          ("beta_mode", 3), ("beta_mode", -1), ("graft", 2),
                                          ("symmetrize", -1), ("factor_form", -1),
                                          ("factor_form", 3), ("split_k", 2), ("split_k", -1),
-                                         ("lds_chain_max", -1), ("lds_chain_max", 65)])
+                                         ("lds_chain_max", -1), ("lds_chain_max", 65),
+                                         ("precond_lowrank", 2)])
 def test_create_rejects_bad_hparams(lib, field, value):
     hp = J.HParams()
     lib.jorge_hparams_default(ctypes.byref(hp))
@@ -168,6 +169,7 @@ def test_plan_tables_of_edge_shapes(lib, form, symmetrize):
         assert J.Jorge.plan([s], symmetrize=symmetrize, factor_form=form, split_k=False) > 0
         for lds in (0, 32):
             assert J.Jorge.plan([s], symmetrize=symmetrize, factor_form=form, lds_chain_max=lds) > 0
+        assert J.Jorge.plan([s], symmetrize=symmetrize, factor_form=form, precond_lowrank=False) > 0
 
 
 def test_plan_tables_of_random_shapes(lib):

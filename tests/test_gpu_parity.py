@@ -319,11 +319,12 @@ def test_stage_timing_reports_every_update_stage():
     opt.set_timing(True)
     opt.step(p, g, 0.1)
     tm = opt.read_timing()
-    # L_hat (256) is explicit and R_hat (512, rank 256) factored, so every stage runs once.
+    # L_hat (256) is explicit and R_hat (512, rank 256) factored, so every update stage runs once.
     assert (opt.factor_form(0, 0), opt.factor_form(0, 1)) == ("explicit", "factored")
     for name in ("stage_in", "gram", "pow4", "xform", "chain4", "chain5", "factor_finalize", "poly",
-                 "update", "symmetrize", "precond_L", "precond_R", "layer_finalize", "weight"):
+                 "update", "symmetrize", "uprecond_L", "uprecond_R", "layer_finalize", "weight"):
         assert tm[name][1] == 1 and tm[name][0] > 0, name
+    assert tm["precond_L"][1] == 0      # the non-update steps' preconditioning
     fl = opt.stage_flops()
     m, n = 256, 512
     assert fl["precond_L"] == 2 * m * m * n and fl["precond_R"] == 2 * m * n * n
@@ -427,3 +428,21 @@ def test_workload_many_small_all_layers():
 def test_workload_large_dense_sampled_layers():
     # one 4096 x 4096 and one 4096 x 1024 layer of the 16 (the oracle step of each takes seconds)
     assert _workload_parity("large_dense", sample=[3, 12], steps=1) < 1e-4
+
+
+@pytest.mark.parametrize("interval", [1, 2])
+def test_lowrank_preconditioning(interval):
+    """A factored factor with d > 3k preconditions through A_new H on update steps."""
+    shapes = [(64, 576), (256, 1152), (512, 128), (100, 1000), (300, 200)]
+    say("low-rank preconditioning, interval", interval)
+    a = run_pair(shapes, 6, 1e-2, check_every=2, gpu_kw=dict(precond_interval=interval),
+                 orc_kw=dict(precond_interval=interval))
+    b = run_pair(shapes, 6, 1e-2, gpu_kw=dict(precond_interval=interval, precond_lowrank=False),
+                 orc_kw=dict(precond_interval=interval))
+    for l in range(len(shapes)):
+        for k in KINDS:
+            x, y = a[0].get_state(l, k), b[0].get_state(l, k)
+            assert rel(x.cpu().numpy(), y.cpu().numpy()) < 1e-5, (l, k)
+        assert rel(a[2][l].cpu().numpy(), b[2][l].cpu().numpy()) < 1e-5
+    fl_a, fl_b = a[0].stage_flops(), b[0].stage_flops()
+    assert fl_a["uprecond_L"] + fl_a["uprecond_R"] < fl_b["uprecond_L"] + fl_b["uprecond_R"]
