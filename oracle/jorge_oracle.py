@@ -13,8 +13,10 @@ for GPU-efficient Second-order Optimization", arXiv 2310.12298):
   gradient preconditioned as L_hat G R_hat; momentum on the preconditioned
   gradient; weight update.
 * Eq. 5-7 (Section 3): the binomial series of (I + A)^(-p) with p = 1/4,
-  truncated after the quadratic term. The two coefficients are computed here
-  from the general term of Eq. 5 rather than typed in.
+  truncated after the quadratic term. The coefficients are computed here
+  from the general term of Eq. 5 rather than typed in. Section 3 drops the
+  cubic and higher terms; series_order=3 keeps the cubic one (the ablation of
+  that choice).
 * Appendix A.1, Eq. 8-9: the dynamic beta_2 = ||X||_F / (||X||_F + 1), which
   turns the update into ((nu+1)/nu)^(1/4) A_hat (I - X/(4 nu) + 5 X^2/(32 nu^2)).
 * Appendix A.2, Algorithm 3: SGD grafting (step magnitude from the heavy-ball
@@ -68,9 +70,11 @@ def binomial_series_coefficient(p: float, r: int) -> float:
     return (-1.0) ** r * coef
 
 
-# Eq. 6 with p = 1/4: the linear and the quadratic coefficient (-1/4 and 5/32).
+# Eq. 6 with p = 1/4: the linear and the quadratic coefficient (-1/4 and 5/32),
+# and the cubic one of Eq. 5 (-15/128) that Section 3 drops.
 SERIES_C1 = binomial_series_coefficient(0.25, 1)
 SERIES_C2 = binomial_series_coefficient(0.25, 2)
+SERIES_C3 = binomial_series_coefficient(0.25, 3)
 
 
 def init_factor(d: int, eps: float) -> np.ndarray:
@@ -109,12 +113,16 @@ def beta_select(nu: float, beta2: float, mode: int) -> tuple[float, float, float
 
 
 def update_factor(A_hat: np.ndarray, M: np.ndarray, beta2: float,
-                  mode: int = BETA_CLAMPED, symmetrize: bool = True):
+                  mode: int = BETA_CLAMPED, symmetrize: bool = True, series_order: int = 2):
     """One preconditioner update of Algorithm 2 (lines 5-6 for L, 7-8 for R).
 
     A_hat is the previous factor (L_hat or R_hat), M the matching statistic
-    (G G^T or G^T G). Returns the new factor and a dict of intermediates.
+    (G G^T or G^T G). series_order is the last power of X kept from the
+    series of Eq. 5: 2 as in Eq. 6-7, or 3. Returns the new factor and a dict
+    of intermediates.
     """
+    if series_order not in (2, 3):
+        raise ValueError("series_order must be 2 or 3")
     A_hat = np.asarray(A_hat, dtype=np.float64)
     M = np.asarray(M, dtype=np.float64)
     d = A_hat.shape[0]
@@ -124,7 +132,10 @@ def update_factor(A_hat: np.ndarray, M: np.ndarray, beta2: float,
     nu = float(np.sqrt(np.sum(X * X)))           # Frobenius norm (Appendix A.1)
     c, s, beta_eff = beta_select(nu, beta2, mode)
     # Truncated series of (I + c X)^(-1/4) (Eq. 6-7, line 6)
-    P = np.eye(d) + SERIES_C1 * c * X + SERIES_C2 * (c * c) * (X @ X)
+    X2 = X @ X
+    P = np.eye(d) + SERIES_C1 * c * X + SERIES_C2 * (c * c) * X2
+    if series_order == 3:                        # the next term of Eq. 5
+        P = P + SERIES_C3 * (c * c * c) * (X2 @ X)
     Z = s * (A_hat @ P)
     A_new = 0.5 * (Z + Z.T) if symmetrize else Z
     return A_new, {"X": X, "nu": nu, "c": c, "s": s, "beta_eff": beta_eff,
@@ -174,6 +185,7 @@ class JorgeOracle:
     beta_mode: int = BETA_CLAMPED
     graft: bool = True
     symmetrize: bool = True
+    series_order: int = 2
     t: int = 0                                   # steps taken so far
     layers: list = field(default_factory=list)
     last_diag: list = field(default_factory=list)
@@ -197,8 +209,10 @@ class JorgeOracle:
             diag = {}
             if update:
                 ML, MR = gram_factors(G)
-                st.L, dL = update_factor(st.L, ML, beta2, self.beta_mode, self.symmetrize)
-                st.R, dR = update_factor(st.R, MR, beta2, self.beta_mode, self.symmetrize)
+                st.L, dL = update_factor(st.L, ML, beta2, self.beta_mode, self.symmetrize,
+                                         self.series_order)
+                st.R, dR = update_factor(st.R, MR, beta2, self.beta_mode, self.symmetrize,
+                                         self.series_order)
                 diag.update(nu_L=dL["nu"], nu_R=dR["nu"], beta_L=dL["beta_eff"],
                             beta_R=dR["beta_eff"])
             Gt = precondition(st.L, G, st.R)

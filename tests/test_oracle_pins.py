@@ -15,8 +15,9 @@ import mpmath
 import numpy as np
 import pytest
 
-from oracle import (BETA_CLAMPED, BETA_DYNAMIC, BETA_FIXED, SERIES_C1, SERIES_C2, JorgeOracle,
-                    beta_select, gram_factors, init_factor, update_factor, update_weights)
+from oracle import (BETA_CLAMPED, BETA_DYNAMIC, BETA_FIXED, SERIES_C1, SERIES_C2, SERIES_C3,
+                    JorgeOracle, beta_select, gram_factors, init_factor, update_factor,
+                    update_weights)
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
@@ -46,13 +47,16 @@ def test_series_coefficients_match_paper_and_taylor():
                 vals[name] = Fraction(int(num), int(den))
     assert SERIES_C1 == float(vals["linear"]) == _TAYLOR[1]
     assert SERIES_C2 == float(vals["quadratic"]) == _TAYLOR[2]
+    # The cubic term that Section 3 drops (kept by series_order=3): Eq. 5's general term.
+    assert SERIES_C3 == _TAYLOR[3] == -15.0 / 128.0
 
 
 # ---------------------------------------------------------------- step 1 vs exact
-def _first_step_case(rng, m, n, sigma, beta2, mode, eps=1e-6):
+def _first_step_case(rng, m, n, sigma, beta2, mode, eps=1e-6, series_order=2):
     G = rng.standard_normal((m, n)) * sigma
     M = G @ G.T
-    L1, diag = update_factor(init_factor(m, eps), M, beta2, mode, symmetrize=True)
+    L1, diag = update_factor(init_factor(m, eps), M, beta2, mode, symmetrize=True,
+                             series_order=series_order)
     lam, U = np.linalg.eigh(M)
     lam = np.clip(lam, 0.0, None)
     l0 = eps ** -0.25
@@ -98,6 +102,37 @@ def test_step1_within_truncation_bound_of_exact_inverse_root(mode, sigma, beta2,
     np.testing.assert_allclose(np.diag(D), series, rtol=1e-12, atol=1e-12 * scale)
 
 
+@pytest.mark.parametrize("mode,sigma,beta2", [
+    (BETA_DYNAMIC, 1e-2, 0.9),          # c X normalised: eigenvalues of c X up to 1
+    (BETA_CLAMPED, 1e-2, 0.9),
+    (BETA_FIXED, 3e-4, 0.9),
+])
+def test_step1_cubic_series_within_quartic_bound(mode, sigma, beta2):
+    """series_order=3 keeps Eq. 5's cubic term: the error against the exact
+    inverse fourth root then has the sign of the quartic term and at most its
+    size, and it is smaller than the quadratic truncation's wherever a > 0."""
+    rng = np.random.default_rng(1)
+    m, n, eps = 7, 11, 1e-6
+    G, M, L3, diag, lam, U, l0, nu, beta = _first_step_case(rng, m, n, sigma, beta2, mode, eps,
+                                                           series_order=3)
+    L2, _ = update_factor(init_factor(m, eps), M, beta2, mode, symmetrize=True)
+    L_exact_eigs = (beta * eps + (1 - beta) * lam) ** -0.25
+    s = beta ** -0.25
+    a = (1 - beta) / beta * l0 ** 4 * lam
+    assert np.all(a <= 1 + 1e-12) and a.max() > 0.05
+    D3, D2 = U.T @ L3 @ U, U.T @ L2 @ U
+    scale = np.abs(np.diag(D3)).max()
+    assert np.abs(D3 - np.diag(np.diag(D3))).max() <= 1e-12 * scale
+    err3 = np.diag(D3) - L_exact_eigs
+    err2 = np.diag(D2) - L_exact_eigs
+    assert np.all(err3 <= 1e-12 * scale)
+    assert np.all(err3 >= -s * l0 * _TAYLOR[4] * a ** 4 * (1 + 1e-9) - 1e-12 * scale)
+    big = a > 0.05
+    assert np.all(np.abs(err3[big]) < np.abs(err2[big]))
+    series = s * l0 * (1 + _TAYLOR[1] * a + _TAYLOR[2] * a ** 2 + _TAYLOR[3] * a ** 3)
+    np.testing.assert_allclose(np.diag(D3), series, rtol=1e-12, atol=1e-12 * scale)
+
+
 # ---------------------------------------------------------------- commuting closed form
 def _beta_paper(nu, beta2, mode):
     if mode == BETA_FIXED or nu == 0:
@@ -107,15 +142,16 @@ def _beta_paper(nu, beta2, mode):
     return 1.0 / nu, ((nu + 1.0) / nu) ** 0.25          # Eq. 9
 
 
+@pytest.mark.parametrize("series_order", [2, 3])
 @pytest.mark.parametrize("mode,sigma,beta2", [(BETA_FIXED, 3e-4, 0.99),
                                               (BETA_CLAMPED, 1e-2, 0.9),
                                               (BETA_DYNAMIC, 1e-3, 0.9)])
-def test_commuting_gradients_follow_scalar_recurrence(mode, sigma, beta2):
+def test_commuting_gradients_follow_scalar_recurrence(mode, sigma, beta2, series_order):
     """G_t = U diag(sigma_t) V^T with fixed U, V: each factor stays diagonal in U (V)."""
     rng = np.random.default_rng(2)
     m, n, eps, steps = 5, 8, 1e-6, 6
     U, V = rand_orth(rng, m), rand_orth(rng, n)
-    orc = JorgeOracle([(m, n)], eps=eps, beta_mode=mode)
+    orc = JorgeOracle([(m, n)], eps=eps, beta_mode=mode, series_order=series_order)
     lL = np.full(m, eps ** -0.25)
     lR = np.full(n, eps ** -0.25)
     for t in range(steps):
@@ -126,15 +162,17 @@ def test_commuting_gradients_follow_scalar_recurrence(mode, sigma, beta2):
                             (np.concatenate([sig ** 2, np.zeros(n - m)]), lR)):
             x = l ** 4 * lam_vals
             c, s = _beta_paper(np.sqrt(np.sum(x ** 2)), beta2, mode)
-            l *= s * (1 - c * x / 4 + 5 * c * c * x * x / 32)
+            cubic = -15 * (c * x) ** 3 / 128 if series_order == 3 else 0.0
+            l *= s * (1 - c * x / 4 + 5 * c * c * x * x / 32 + cubic)
         st = orc.layers[0]
         np.testing.assert_allclose(st.L, (U * lL) @ U.T, rtol=0, atol=1e-12 * lL.max())
         np.testing.assert_allclose(st.R, (V * lR) @ V.T, rtol=0, atol=1e-12 * lR.max())
 
 
 # ---------------------------------------------------------------- any state: similarity
+@pytest.mark.parametrize("series_order", [2, 3])
 @pytest.mark.parametrize("mode", [BETA_FIXED, BETA_CLAMPED])
-def test_update_similarity_identity_noncommuting(mode):
+def test_update_similarity_identity_noncommuting(mode, series_order):
     """For X = A^4 M: A^-3 Z A^2 = s P(K) with K = A^2 M A^2 symmetric.
 
     X = A^2 K A^-2, so the literal update Z = s A P(X) satisfies the identity;
@@ -146,7 +184,7 @@ def test_update_similarity_identity_noncommuting(mode):
     A = rand_spd(rng, d, 0.6, 1.4)
     Gm = rng.standard_normal((d, 9)) * 0.05
     M = Gm @ Gm.T
-    Z, diag = update_factor(A, M, 0.9, mode, symmetrize=False)
+    Z, diag = update_factor(A, M, 0.9, mode, symmetrize=False, series_order=series_order)
     l, U = np.linalg.eigh(A)
     nu_spec = np.sqrt(np.sum(l ** 8 * np.sum((U.T @ M) ** 2, axis=1)))
     assert diag["nu"] == pytest.approx(nu_spec, rel=1e-12)
@@ -154,20 +192,23 @@ def test_update_similarity_identity_noncommuting(mode):
     K = A2 @ M @ A2
     c, s = diag["c"], diag["s"]
     PK = np.eye(d) + _TAYLOR[1] * c * K + _TAYLOR[2] * c * c * (K @ K)
+    if series_order == 3:
+        PK = PK + _TAYLOR[3] * c ** 3 * (K @ K @ K)
     Ainv3 = (U * l ** -3.0) @ U.T
     lhs = Ainv3 @ Z @ A2
     np.testing.assert_allclose(lhs, s * PK, rtol=0, atol=1e-11 * np.abs(PK).max())
     # symmetrize=True is exactly the symmetric part of the literal update.
-    Zs, _ = update_factor(A, M, 0.9, mode, symmetrize=True)
+    Zs, _ = update_factor(A, M, 0.9, mode, symmetrize=True, series_order=series_order)
     np.testing.assert_array_equal(Zs, 0.5 * (Z + Z.T))
 
 
 # ---------------------------------------------------------------- exact special cases
+@pytest.mark.parametrize("series_order", [2, 3])
 @pytest.mark.parametrize("mode", [BETA_FIXED, BETA_CLAMPED])
-def test_zero_gradient_is_pure_beta_scaling(mode):
+def test_zero_gradient_is_pure_beta_scaling(mode, series_order):
     rng = np.random.default_rng(4)
     m, n = 4, 6
-    orc = JorgeOracle([(m, n)], beta_mode=mode)
+    orc = JorgeOracle([(m, n)], beta_mode=mode, series_order=series_order)
     st = orc.layers[0]
     st.L, st.R = rand_spd(rng, m), rand_spd(rng, n)
     st.m, st.m_sgd = rng.standard_normal((m, n)), rng.standard_normal((m, n))
