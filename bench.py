@@ -80,7 +80,7 @@ def measured_traffic(config):
     return float(vals["traffic_bytes_per_launch"]) if "traffic_bytes_per_launch" in vals else None
 
 
-GEMM_STAGES = ("gram", "pow4", "xform", "chain4", "chain5", "poly", "update", "uprecond_L", "uprecond_R",
+GEMM_STAGES = ("gram", "pow4", "xform", "chain4", "chain5", "poly", "poly2", "update", "uprecond_L", "uprecond_R",
                "precond_L", "precond_R")
 # Preconditioning of steps that do not update the factors; every other GEMM stage runs on update steps.
 NON_UPDATE_STAGES = ("precond_L", "precond_R")
@@ -88,7 +88,7 @@ NON_UPDATE_STAGES = ("precond_L", "precond_R")
 FIXUP_STAGE = "split_fixup"
 
 
-def cpu_baseline(shapes, sigma, seed, budget_s):
+def cpu_baseline(shapes, sigma, seed, budget_s, series_order=2):
     """The fp64 oracle timed on the host over a bounded, deterministic sample.
 
     Layers are taken in the workload's order, one oracle step each, until the
@@ -105,7 +105,7 @@ def cpu_baseline(shapes, sigma, seed, budget_s):
     for l, s in enumerate(shapes):
         G = [gradient(seed, l, 1, s, sigma)]
         P = [initial_params(seed, l, s).astype(np.float64)]
-        orc = JorgeOracle([s])
+        orc = JorgeOracle([s], series_order=series_order)
         t0 = time.perf_counter()
         orc.step(P, G, 0.1, 0.9, 0.9, 5e-5)
         spent += time.perf_counter() - t0
@@ -131,6 +131,8 @@ def main():
                     help="evaluation order of the factor updates")
     ap.add_argument("--split-k", type=int, default=1, choices=(0, 1),
                     help="split the K range of long tiles in levels with too few tiles")
+    ap.add_argument("--series-order", type=int, default=2, choices=(2, 3),
+                    help="last power of X kept from the binomial series (Section 3 keeps 2)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time (0 = skip)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -151,7 +153,8 @@ def main():
     shapes, sigma, run_steps = CONFIGS[args.config]
     steps = args.steps if args.steps is not None else run_steps
     hp = DEFAULT_HPARAMS
-    opt = Jorge(shapes, eps=hp["eps"], precond_interval=args.interval, factor_form=args.form, split_k=bool(args.split_k))
+    opt = Jorge(shapes, eps=hp["eps"], precond_interval=args.interval, factor_form=args.form,
+                split_k=bool(args.split_k), series_order=args.series_order)
     params = [device_initial_params(args.seed, l, s) for l, s in enumerate(shapes)]
     grads = [[device_gradient(args.seed, l, t, s, sigma) for l, s in enumerate(shapes)]
              for t in range(1, args.warmup + steps + 1)]
@@ -239,7 +242,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": WORKLOAD_NAMES[args.config], "name": args.config, "layers": len(shapes),
                    "params": sum(m * n for m, n in shapes), "precond_interval": args.interval,
-                   "factor_updates": updates, "factor_form": args.form, "factors": forms, "split_k": args.split_k, "seed": args.seed},
+                   "factor_updates": updates, "factor_form": args.form, "factors": forms, "split_k": args.split_k,
+                   "series_order": args.series_order, "seed": args.seed},
         "roofline": {"bound": "mfma", "kernel": "gemm_grouped<true, true> (every GEMM stage of the step)",
                      "achieved": achieved, "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_FP32_MFMA_TFLOPS, "traffic": measured_traffic(args.config), "traffic_unit": "HBM bytes per launch",
@@ -254,7 +258,7 @@ def main():
         "stages": per_stage,
     }
     if args.cpu_budget > 0:
-        out["cpu_baseline"] = cpu_baseline(shapes, sigma, args.seed, args.cpu_budget)
+        out["cpu_baseline"] = cpu_baseline(shapes, sigma, args.seed, args.cpu_budget, args.series_order)
     print(json.dumps(out), flush=True)
     return 0
 

@@ -111,6 +111,13 @@ typedef struct jorge_hparams {
                                  the update's own terms (about 6 k^2 d flops instead of a d x d
                                  product; the same result up to fp32 rounding); needs
                                  symmetrize = 1. 0: always the direct products. Default 1. */
+    int32_t series_order;     /* last power of X kept from the binomial series of
+                                 (I + c X)^(-1/4) (Section 3, Eq. 5): 2 gives Eq. 6-7,
+                                 P = I - (c/4) X + (5c^2/32) X^2, as in Algorithm 2; 3 also
+                                 keeps -(15c^3/128) X^3, the term Section 3 drops. Order 3
+                                 costs one more product per factor (2 d^3 in the explicit
+                                 order, k^3 in the factored one) and one more GEMM launch per
+                                 update. 2 or 3. Default 2. */
 } jorge_hparams;
 
 /* Largest rows or cols of a layer the library accepts. */

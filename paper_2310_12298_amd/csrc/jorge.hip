@@ -65,14 +65,15 @@ namespace {
 enum Stage : int {
     ST_STAGEIN = 0, ST_GRAM, ST_POW4, ST_XFORM, ST_CHAIN4, ST_CHAIN5, ST_FFINAL, ST_POLY, ST_UPDATE,
     ST_SYMM, ST_PRECOND_L, ST_PRECOND_R, ST_LFINAL, ST_WEIGHT, ST_FIXUP, ST_LDS_CHAIN, ST_UPRECOND_L,
-    ST_UPRECOND_R, ST_COUNT
+    ST_UPRECOND_R, ST_POLY2, ST_COUNT
 };
 const char* const kStageNames[ST_COUNT] = {
     "stage_in", "gram", "pow4", "xform", "chain4", "chain5", "factor_finalize", "poly", "update",
     "symmetrize", "precond_L", "precond_R", "layer_finalize", "weight", "split_fixup", "lds_chain",
-    "uprecond_L", "uprecond_R"};
-// The GEMM levels of an update step, in launch order.
-constexpr int kLevels[] = {ST_GRAM, ST_POW4, ST_XFORM, ST_CHAIN4, ST_CHAIN5, ST_POLY, ST_UPDATE};
+    "uprecond_L", "uprecond_R", "poly2"};
+// The GEMM levels of an update step, in launch order (poly2 is empty unless
+// the series keeps its cubic term).
+constexpr int kLevels[] = {ST_GRAM, ST_POW4, ST_XFORM, ST_CHAIN4, ST_CHAIN5, ST_POLY, ST_POLY2, ST_UPDATE};
 
 constexpr size_t kAlign = 256;
 constexpr int kFlatChunkElems = 16384;
@@ -102,7 +103,8 @@ struct LayerHost {
 
 // One factor: A (d x d) with statistic H H^T, H being d x k.
 //   explicit workspace: w[0] M then P^T, w[1] A^2 then X, w[2] A^4 then Z, w[3] X^T (dp x dp each)
-//   factored workspace: w[0], w[1] kp x dp (Yt_j, A^5 H, W), w[2] Q = H^T H, w[3] S (kp x kp)
+//   factored workspace: w[0], w[1] kp x dp (Yt_j, A^5 H, W), w[2] Q = H^T H, w[3] S (kp x kp),
+//   and with series order 3 s2: b S - e S^2 (kp x kp)
 struct FactorHost {
     int layer, side, d, dp, k, kp;
     bool expl = true;
@@ -113,6 +115,7 @@ struct FactorHost {
     size_t off_y1 = 0, off_wt = 0, off_v2t = 0, off_xa = 0;
     size_t off_A, off_part, off_sc;
     size_t off_w[4];
+    size_t off_s2 = 0;
     int nparts = 0;
 };
 
@@ -361,6 +364,7 @@ jorge_status validate_hparams(const jorge_hparams* hp) {
     if (hp->split_k != 0 && hp->split_k != 1) return JORGE_ERR_INVALID_ARGUMENT;
     if (hp->lds_chain_max < 0 || hp->lds_chain_max > kChainMax) return JORGE_ERR_INVALID_ARGUMENT;
     if (hp->precond_lowrank != 0 && hp->precond_lowrank != 1) return JORGE_ERR_INVALID_ARGUMENT;
+    if (hp->series_order != 2 && hp->series_order != 3) return JORGE_ERR_INVALID_ARGUMENT;
     return JORGE_OK;
 }
 
@@ -372,13 +376,15 @@ int64_t tile_work(int64_t M, int64_t N, int64_t K, bool upper) {
 
 // Whether a factor of padded size dp with statistic rank kp is cheaper in the
 // explicit order than in the factored one (same product list as build_tables).
-bool explicit_is_cheaper(int64_t dp, int64_t kp, bool sym) {
-    const int64_t e = tile_work(dp, dp, kp, true) + 2 * tile_work(dp, dp, dp, sym) +
-                      3 * tile_work(dp, dp, dp, false);
-    const int64_t f = tile_work(kp, kp, dp, true) + 5 * tile_work(kp, dp, dp, false) +
-                      tile_work(kp, kp, dp, sym) + tile_work(kp, kp, dp, true) +
-                      tile_work(dp, kp, kp, false) + (sym ? tile_work(dp, dp, 2 * kp, true)
-                                                          : tile_work(dp, dp, kp, false));
+bool explicit_is_cheaper(int64_t dp, int64_t kp, bool sym, int order) {
+    int64_t e = tile_work(dp, dp, kp, true) + 2 * tile_work(dp, dp, dp, sym) + 3 * tile_work(dp, dp, dp, false);
+    int64_t f = tile_work(kp, kp, dp, true) + 5 * tile_work(kp, dp, dp, false) + tile_work(kp, kp, dp, sym) +
+                tile_work(kp, kp, dp, true) + tile_work(dp, kp, kp, false) +
+                (sym ? tile_work(dp, dp, 2 * kp, true) : tile_work(dp, dp, kp, false));
+    if (order == 3) {  // X V, and S S
+        e += tile_work(dp, dp, dp, false);
+        f += tile_work(kp, kp, kp, sym);
+    }
     return e <= f;
 }
 
@@ -404,7 +410,7 @@ size_t plan(jorge_ctx* c) {
             F.chain = F.dp <= c->hp.lds_chain_max;
             if (F.chain || c->hp.factor_form == JORGE_FORM_EXPLICIT) F.expl = true;
             else if (c->hp.factor_form == JORGE_FORM_FACTORED) F.expl = false;
-            else F.expl = explicit_is_cheaper(F.dp, F.kp, sym);
+            else F.expl = explicit_is_cheaper(F.dp, F.kp, sym, c->hp.series_order);
             const size_t dd = (size_t)F.dp * F.dp * sizeof(float);
             F.off_A = take(dd);
             if (F.chain) {
@@ -418,6 +424,7 @@ size_t plan(jorge_ctx* c) {
                 F.off_w[1] = take(kd);
                 F.off_w[2] = take(kk);
                 F.off_w[3] = take(kk);
+                if (c->hp.series_order == 3) F.off_s2 = take(kk);
                 F.nparts = tile_count(F.kp, F.kp);
             }
             // A_new H (d x k) replaces a d x d product in the preconditioning when
@@ -480,11 +487,24 @@ void add_explicit(jorge_ctx* c, const FactorHost& F, const FactorDev& fd, const 
     x.C = W1; x.ldc = dp; x.C2 = W3; x.ldc2 = dp;
     x.flags = EF_STORE | EF_STORE_T | EF_NORM; x.partials = fd.partials;
     add_problem(c->nt[ST_XFORM], x, 2 * d * d * d);
-    // P = I - a X + b X X, stored transposed (the K-major B of the next product).
-    GemmProblem p = product(W1, dp, W3, dp, dp, dp, dp);
-    p.C2 = W0; p.ldc2 = dp; p.X = W1; p.ldx = dp; p.sc = fd.sc;
-    p.flags = EF_STORE_T | EF_READX; p.coef = CO_POLY; p.valid_m = p.valid_n = F.d;
-    add_problem(c->nt[ST_POLY], p, 2 * d * d * d);
+    if (c->hp.series_order == 3) {
+        // V = b X - e X X, stored transposed over A^4 (the K-major B of X V) ...
+        GemmProblem v = product(W1, dp, W3, dp, dp, dp, dp);
+        v.C2 = W2; v.ldc2 = dp; v.X = W1; v.ldx = dp; v.sc = fd.sc;
+        v.flags = EF_STORE_T | EF_READX; v.coef = CO_VSER;
+        add_problem(c->nt[ST_POLY], v, 2 * d * d * d);
+        // ... then P = I - a X + X V, stored transposed.
+        GemmProblem p = product(W1, dp, W2, dp, dp, dp, dp);
+        p.C2 = W0; p.ldc2 = dp; p.X = W1; p.ldx = dp; p.sc = fd.sc;
+        p.flags = EF_STORE_T | EF_READX; p.coef = CO_POLY3; p.valid_m = p.valid_n = F.d;
+        add_problem(c->nt[ST_POLY2], p, 2 * d * d * d);
+    } else {
+        // P = I - a X + b X X, stored transposed (the K-major B of the next product).
+        GemmProblem p = product(W1, dp, W3, dp, dp, dp, dp);
+        p.C2 = W0; p.ldc2 = dp; p.X = W1; p.ldx = dp; p.sc = fd.sc;
+        p.flags = EF_STORE_T | EF_READX; p.coef = CO_POLY; p.valid_m = p.valid_n = F.d;
+        add_problem(c->nt[ST_POLY], p, 2 * d * d * d);
+    }
     // Z = s A P
     GemmProblem z = product(A, dp, W0, dp, dp, dp, dp);
     z.C = W2; z.ldc = dp; z.sc = fd.sc; z.flags = EF_STORE; z.coef = CO_SCALE;
@@ -549,14 +569,27 @@ int add_factored(jorge_ctx* c, const FactorHost& F, const FactorDev& fd, const f
         s.C = S; s.ldc = kp; s.flags = EF_STORE;
         add_problem(c->nt[ST_CHAIN5], s, 2 * k * k * d);
     }
-    // W = a A^5 H - b A^5 H S (B = S^T row-major), into P1.
-    GemmProblem w = product(P0, kp, S, kp, dp, kp, kp);
+    // W = a A^5 H - b A^5 H S (B = S^T row-major), into P1. With the cubic
+    // term, W = a A^5 H - A^5 H V with V = b S - e S S (X^r = U S^(r-1) H^T),
+    // one level later: V^T = b S^T - e S^T S^T (S^T symmetric, or the literal
+    // mode's S^T as an MN-major B), then W.
+    const bool cubic = c->hp.series_order == 3;
+    const float* wb = S;
+    if (cubic) {
+        float* V = at<float>(c, F.off_s2);
+        GemmProblem v = product(S, kp, S, kp, kp, kp, kp);
+        v.C = V; v.ldc = kp; v.X = S; v.ldx = kp; v.sc = fd.sc;
+        v.flags = EF_STORE | EF_READX; v.coef = CO_VSER; v.upper = sym;
+        add_problem(sym ? c->nt[ST_POLY] : c->nn[ST_POLY], v, (sym ? 1 : 2) * k * k * k);
+        wb = V;
+    }
+    GemmProblem w = product(P0, kp, wb, kp, dp, kp, kp);
     w.C = P1; w.ldc = kp; w.X = P0; w.ldx = kp; w.sc = fd.sc;
-    w.flags = EF_STORE | EF_READX; w.coef = CO_WMIX;
+    w.flags = EF_STORE | EF_READX; w.coef = cubic ? CO_WMIX3 : CO_WMIX;
     if (F.lrp) {  // and W^T for H^T W
         w.C2 = at<float>(c, F.off_wt); w.ldc2 = dp; w.flags |= EF_STORE_T;
     }
-    add_problem(c->nt[ST_POLY], w, 2 * d * k * k);
+    add_problem(c->nt[cubic ? ST_POLY2 : ST_POLY], w, 2 * d * k * k);
     if (F.lrp) {
         // H^T W (k x k) in the update level, beside the SYR2K.
         GemmProblem v = product(Ht, dp, at<float>(c, F.off_wt), dp, kp, kp, dp);
@@ -757,7 +790,8 @@ std::string check_stage(const jorge_ctx* c, const GemmStage& st, bool bk, const 
             return where + "C2";
         if ((p.flags & (EF_READX | EF_DOT)) && !in_buffer(c, p.X, fl((int64_t)(p.M - 1) * p.ldx + p.N - 1)))
             return where + "X";
-        if ((p.flags & EF_READX) && p.coef == CO_POLY && (p.valid_m > p.M || p.valid_m > p.N))
+        if ((p.flags & EF_READX) && (p.coef == CO_POLY || p.coef == CO_POLY3) &&
+            (p.valid_m > p.M || p.valid_m > p.N))
             return where + "identity extent";
         if ((p.flags & EF_MOMENTUM) &&
             (p.valid_m > p.M || p.valid_n > p.N ||
@@ -953,7 +987,8 @@ jorge_status run_update(jorge_ctx* c, double beta2) {
         JORGE_HIP(c, hipStreamWaitEvent(c->side, c->ev_fork, 0));
         TimedLaunch tl(c, ST_LDS_CHAIN, c->side);
         hipLaunchKernelGGL(lds_chain_kernel, dim3((unsigned)c->chain.size()), dim3(kGemmThreads), 0, c->side,
-                           c->dfactors, c->dchain, beta2, (int)c->hp.beta_mode, (int)c->hp.symmetrize);
+                           c->dfactors, c->dchain, beta2, (int)c->hp.beta_mode, (int)c->hp.symmetrize,
+                           (int)c->hp.series_order);
         tl.finish();
         JORGE_HIP(c, hipGetLastError());
         JORGE_HIP(c, hipEventRecord(c->ev_join, c->side));
@@ -1016,6 +1051,7 @@ jorge_status jorge_hparams_default(jorge_hparams* hp) {
     hp->split_k = 1;
     hp->lds_chain_max = kChainMax;
     hp->precond_lowrank = 1;
+    hp->series_order = 2;
     return JORGE_OK;
 }
 

@@ -537,6 +537,9 @@ __device__ __forceinline__ void gemm_epilogue(const GemmProblem& p, int tm, int 
                 case CO_WMIX: cx = sc->a; cc = -sc->b; break;
                 case CO_SYR2K: cx = sc->sf; cc = -0.5f * sc->sf; break;
                 case CO_LITUPD: cx = sc->sf; cc = -sc->sf; break;
+                case CO_VSER: cx = sc->b; cc = -sc->e; break;
+                case CO_POLY3: ci = 1.f; cx = -sc->a; break;
+                case CO_WMIX3: cx = sc->a; cc = -1.f; break;
                 default: break;
             }
         }

@@ -88,7 +88,7 @@ __device__ __forceinline__ FactorScalars factor_scalars(double nu, double beta2,
     out.a = (float)(0.25 * out.c);
     out.b = (float)(0.15625 * out.c * out.c);
     out.sf = (float)out.s;
-    out.pad = 0.f;
+    out.e = (float)(0.1171875 * out.c * out.c * out.c);
     return out;
 }
 
@@ -161,7 +161,9 @@ __global__ __launch_bounds__(kEwThreads) void symmetrize_kernel(const FactorDev*
 // in LDS: M = H H^T (H streamed from global memory in 32-column slabs),
 // A^2, A^4, X = A^4 M with ||X||_F, (beta, c, s) (Appendix A.1, Eq. 8-9),
 // P = I - (c/4) X + (5c^2/32) X X (Eq. 6), Z = s A P and A <- (Z + Z^T)/2
-// (or Z). One launch replaces the five grouped levels for these factors.
+// (or Z). With series order 3, P = I - a X + X V with V = b X - e X X keeps
+// the cubic term of Eq. 5. One launch replaces the grouped levels for these
+// factors.
 // Each of the four waves owns one 32 x 32 block of a 64 x 64 product
 // (v_mfma_f32_32x32x2_f32); blocks outside dp are skipped.
 constexpr int kChainMax = 64;
@@ -176,7 +178,7 @@ struct ChainLds {
     float T2[kChainMat];
     float H[kChainMax * kChainSlabLd];
     double red[4];
-    float coef[3];  // a, b, s
+    float coef[4];  // a, b, s, e
 };
 
 // acc += A (rows wy*32.., lda) x B (cols wx*32.., ldb) over k in [0, K): both
@@ -214,7 +216,7 @@ __device__ __forceinline__ void chain_store(float* c, int wy, int wx, const f32x
 
 __global__ __launch_bounds__(kGemmThreads) void lds_chain_kernel(const FactorDev* __restrict__ f,
                                                                  const int* __restrict__ list, double beta2,
-                                                                 int mode, int symmetrize) {
+                                                                 int mode, int symmetrize, int order) {
     __shared__ __attribute__((aligned(16))) ChainLds sm;
     const FactorDev F = f[list[blockIdx.x]];
     const int dp = F.dp, tid = threadIdx.x;
@@ -288,32 +290,57 @@ __global__ __launch_bounds__(kGemmThreads) void lds_chain_kernel(const FactorDev
         sm.coef[0] = fs.a;
         sm.coef[1] = fs.b;
         sm.coef[2] = fs.sf;
+        sm.coef[3] = fs.e;
     }
     __syncthreads();
-    const float a = sm.coef[0], b = sm.coef[1], sf = sm.coef[2];
-    // P = I - a X + b X X -> T2
-    zero(acc);
-    if (active) {
-        chain_mma<false>(sm.T1, kChainLd, sm.T1, kChainLd, dp, wy, wx, acc);
-        const int d = F.d;
-        chain_store(sm.T2, wy, wx, acc, [&](int row, int col, float v) {
-            const float id = (row == col && row < d) ? 1.0f : 0.0f;
-            return (id - a * sm.T1[row * kChainLd + col]) + b * v;
-        });
+    const float a = sm.coef[0], b = sm.coef[1], sf = sm.coef[2], ce = sm.coef[3];
+    const int d = F.d;
+    // P (the matrix the product with A reads) and Z, in buffers free at that point.
+    float* P = sm.T2;
+    float* Z = sm.M;
+    if (order == 3) {
+        // V = b X - e X X -> T2, then P = I - a X + X V -> M
+        zero(acc);
+        if (active) {
+            chain_mma<false>(sm.T1, kChainLd, sm.T1, kChainLd, dp, wy, wx, acc);
+            chain_store(sm.T2, wy, wx, acc,
+                        [&](int row, int col, float v) { return b * sm.T1[row * kChainLd + col] - ce * v; });
+        }
+        __syncthreads();
+        zero(acc);
+        if (active) {
+            chain_mma<false>(sm.T1, kChainLd, sm.T2, kChainLd, dp, wy, wx, acc);
+            chain_store(sm.M, wy, wx, acc, [&](int row, int col, float v) {
+                const float id = (row == col && row < d) ? 1.0f : 0.0f;
+                return (id - a * sm.T1[row * kChainLd + col]) + v;
+            });
+        }
+        P = sm.M;
+        Z = sm.T1;
+    } else {
+        // P = I - a X + b X X -> T2
+        zero(acc);
+        if (active) {
+            chain_mma<false>(sm.T1, kChainLd, sm.T1, kChainLd, dp, wy, wx, acc);
+            chain_store(sm.T2, wy, wx, acc, [&](int row, int col, float v) {
+                const float id = (row == col && row < d) ? 1.0f : 0.0f;
+                return (id - a * sm.T1[row * kChainLd + col]) + b * v;
+            });
+        }
     }
     __syncthreads();
-    // Z = s A P -> M
+    // Z = s A P
     zero(acc);
     if (active) {
-        chain_mma<false>(sm.A, kChainLd, sm.T2, kChainLd, dp, wy, wx, acc);
-        chain_store(sm.M, wy, wx, acc, [&](int, int, float v) { return sf * v; });
+        chain_mma<false>(sm.A, kChainLd, P, kChainLd, dp, wy, wx, acc);
+        chain_store(Z, wy, wx, acc, [&](int, int, float v) { return sf * v; });
     }
     __syncthreads();
     // A <- (Z + Z^T)/2 or Z; fp32 addition commutes, so the result is bitwise symmetric.
     for (int e = tid; e < dp * dp; e += kGemmThreads) {
         const int r = e / dp, c = e % dp;
-        const float z = sm.M[r * kChainLd + c];
-        F.A[e] = symmetrize ? 0.5f * (z + sm.M[c * kChainLd + r]) : z;
+        const float z = Z[r * kChainLd + c];
+        F.A[e] = symmetrize ? 0.5f * (z + Z[c * kChainLd + r]) : z;
     }
 }
 

@@ -17,7 +17,8 @@ enum EpiFlags : int {
 };
 
 // Coefficient sets: value = ci [row == col < valid_m] + cx X[row][col] + cc acc,
-// with (a, b, s) = (c/4, 5c^2/32, beta^(-1/4)) of the factor being updated.
+// with (a, b, e, s) = (c/4, 5c^2/32, 15c^3/128, beta^(-1/4)) of the factor
+// being updated (e: the cubic term of Eq. 5, kept only with series order 3).
 enum Coef : int {
     CO_ONE = 0,     // (0, 0, 1)          plain product
     CO_POLY = 1,    // (1, -a, b)         P = I - (c/4) X + (5c^2/32) X X      (Eq. 6)
@@ -25,6 +26,9 @@ enum Coef : int {
     CO_WMIX = 3,    // (0, a, -b)         W = A^5 H (a I - b S)
     CO_SYR2K = 4,   // (0, s, -s/2)       A <- s A - (s/2) (W H^T + H W^T)
     CO_LITUPD = 5,  // (0, s, -s)         A <- s A - s W H^T
+    CO_VSER = 6,    // (0, b, -e)         V = b X - e X X        (series order 3)
+    CO_POLY3 = 7,   // (1, -a, 1)         P = I - a X + X V  = I - a X + b X^2 - e X^3
+    CO_WMIX3 = 8,   // (0, a, -1)         W = a A^5 H - A^5 H V(S) = A^5 H (a I - b S + e S^2)
 };
 
 // Scalars of one factor update, written on the device by the finalize kernel.
@@ -36,7 +40,7 @@ struct FactorScalars {
     float a;      // c / 4            (fp32 copy for the epilogue)
     float b;      // 5 c^2 / 32
     float sf;     // s
-    float pad;
+    float e;      // 15 c^3 / 128
 };
 
 // Scalars of one layer's weight update, written by the layer finalize kernel.

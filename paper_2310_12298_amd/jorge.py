@@ -35,7 +35,7 @@ class HParams(ctypes.Structure):
                 ("beta_mode", ctypes.c_int32), ("graft", ctypes.c_int32),
                 ("symmetrize", ctypes.c_int32), ("factor_form", ctypes.c_int32),
                 ("split_k", ctypes.c_int32), ("lds_chain_max", ctypes.c_int32),
-                ("precond_lowrank", ctypes.c_int32)]
+                ("precond_lowrank", ctypes.c_int32), ("series_order", ctypes.c_int32)]
 
 
 _LIB = None
@@ -114,11 +114,11 @@ class Jorge:
 
     def __init__(self, shapes, eps=1e-6, precond_interval=1, beta_mode="clamped", graft=True,
                  symmetrize=True, factor_form="auto", split_k=True, lds_chain_max=64, precond_lowrank=True,
-                 stream=None):
+                 series_order=2, stream=None):
         self.lib = load_library()
         self.shapes = [(int(m), int(n)) for m, n in shapes]
         hp = self.hparams(eps, precond_interval, beta_mode, graft, symmetrize, factor_form, split_k,
-                          lds_chain_max, precond_lowrank)
+                          lds_chain_max, precond_lowrank, series_order)
         arr = (Shape * len(self.shapes))(*[Shape(m, n) for m, n in self.shapes])
         ctx = _P()
         s = _current_stream() if stream is None else int(stream)
@@ -128,7 +128,7 @@ class Jorge:
 
     @staticmethod
     def hparams(eps=1e-6, precond_interval=1, beta_mode="clamped", graft=True, symmetrize=True,
-                factor_form="auto", split_k=True, lds_chain_max=64, precond_lowrank=True):
+                factor_form="auto", split_k=True, lds_chain_max=64, precond_lowrank=True, series_order=2):
         lib = load_library()
         hp = HParams()
         _check(lib, lib.jorge_hparams_default(ctypes.byref(hp)))
@@ -141,6 +141,7 @@ class Jorge:
         hp.split_k = int(split_k)
         hp.lds_chain_max = int(lds_chain_max)
         hp.precond_lowrank = int(bool(precond_lowrank))
+        hp.series_order = int(series_order)
         return hp
 
     @staticmethod

@@ -46,7 +46,8 @@ def test_hparams_default(lib):
     hp = J.HParams()
     assert lib.jorge_hparams_default(ctypes.byref(hp)) == 0
     assert (hp.eps, hp.precond_interval, hp.beta_mode, hp.graft, hp.symmetrize,
-            hp.factor_form, hp.split_k, hp.lds_chain_max, hp.precond_lowrank) == (1e-6, 1, 2, 1, 1, 0, 1, 64, 1)
+            hp.factor_form, hp.split_k, hp.lds_chain_max, hp.precond_lowrank,
+            hp.series_order) == (1e-6, 1, 2, 1, 1, 0, 1, 64, 1, 2)
     assert lib.jorge_hparams_default(None) == ERR_INVALID
 
 
@@ -74,7 +75,8 @@ def test_create_rejects_oversize(lib):
                                          ("symmetrize", -1), ("factor_form", -1),
                                          ("factor_form", 3), ("split_k", 2), ("split_k", -1),
                                          ("lds_chain_max", -1), ("lds_chain_max", 65),
-                                         ("precond_lowrank", 2)])
+                                         ("precond_lowrank", 2), ("series_order", 1),
+                                         ("series_order", 4), ("series_order", 0)])
 def test_create_rejects_bad_hparams(lib, field, value):
     hp = J.HParams()
     lib.jorge_hparams_default(ctypes.byref(hp))
@@ -147,6 +149,8 @@ def test_plan_tables_of_every_workload(lib, name, symmetrize):
     assert sizes["auto"] <= max(sizes["explicit"], sizes["factored"])
     for f in FORMS:   # split plans are checked too; they only add their workspace
         assert J.Jorge.plan(shapes, symmetrize=symmetrize, factor_form=f) >= sizes[f]
+        # The cubic series term adds products (and, factored, one k x k buffer per factor).
+        assert J.Jorge.plan(shapes, symmetrize=symmetrize, factor_form=f, series_order=3) > 0
 
 
 def test_plan_splits_long_tiles_of_sparse_levels(lib):
@@ -170,6 +174,7 @@ def test_plan_tables_of_edge_shapes(lib, form, symmetrize):
         for lds in (0, 32):
             assert J.Jorge.plan([s], symmetrize=symmetrize, factor_form=form, lds_chain_max=lds) > 0
         assert J.Jorge.plan([s], symmetrize=symmetrize, factor_form=form, precond_lowrank=False) > 0
+        assert J.Jorge.plan([s], symmetrize=symmetrize, factor_form=form, series_order=3) > 0
 
 
 def test_plan_tables_of_random_shapes(lib):
@@ -179,6 +184,7 @@ def test_plan_tables_of_random_shapes(lib):
         shapes = [tuple(int(x) for x in rng.integers(1, 700, size=2)) for _ in range(int(rng.integers(1, 6)))]
         for form in FORMS:
             assert J.Jorge.plan(shapes, factor_form=form) > 0, shapes
+            assert J.Jorge.plan(shapes, factor_form=form, series_order=3, symmetrize=bool(rng.integers(2))) > 0
 
 
 def test_plan_rejects_what_create_rejects(lib):

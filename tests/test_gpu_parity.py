@@ -446,3 +446,55 @@ def test_lowrank_preconditioning(interval):
         assert rel(a[2][l].cpu().numpy(), b[2][l].cpu().numpy()) < 1e-5
     fl_a, fl_b = a[0].stage_flops(), b[0].stage_flops()
     assert fl_a["uprecond_L"] + fl_a["uprecond_R"] < fl_b["uprecond_L"] + fl_b["uprecond_R"]
+
+
+# ---------------------------------------------------------------- cubic series term
+# series_order=3 keeps the cubic term of Eq. 5 that Section 3 drops: the
+# explicit order forms V = b X - e X X and then P = I - a X + X V, the factored
+# order V = b S - e S S and W = a A^5 H - A^5 H V, the LDS chain the explicit
+# steps in LDS. The shapes put factors in every path: LDS chain (d <= 64),
+# explicit, factored, low-rank preconditioning (factored with d > 3k), and a
+# long-K layer whose sparse levels split.
+CUBIC_SHAPES = [(64, 576), (48, 96), (300, 130), (256, 1152), (512, 128), (128, 2048)]
+
+
+@pytest.mark.parametrize("symmetrize", [True, False])
+@pytest.mark.parametrize("form", FORMS)
+def test_cubic_series_term(form, symmetrize):
+    say("cubic series term", form, "symmetrize", symmetrize)
+    kw = dict(series_order=3, symmetrize=symmetrize)
+    opt, orc, pg, po, worst = run_pair(CUBIC_SHAPES, 6, 1e-2, check_every=2,
+                                       gpu_kw=dict(FORM_KW[form], **kw), orc_kw=kw)
+    say("  worst rel err", worst)
+    # The test discriminates: the quadratic truncation is far from the cubic one here.
+    orc2 = JorgeOracle(CUBIC_SHAPES, symmetrize=symmetrize)
+    po2 = [initial_params(0, l, s).astype(np.float64) for l, s in enumerate(CUBIC_SHAPES)]
+    for t in range(1, 7):
+        po2 = orc2.step(po2, [gradient(0, l, t, s, 1e-2) for l, s in enumerate(CUBIC_SHAPES)], **HP)
+    gap = max(rel(orc2.layers[l].R, orc.layers[l].R) for l in range(len(CUBIC_SHAPES)))
+    assert gap > 100 * worst, (gap, worst)
+
+
+@pytest.mark.parametrize("shapes", [[(1, 1)], [(40, 1)], [(33, 65)], [(200, 300)], [(130, 260)]])
+@pytest.mark.parametrize("form", FORMS)
+def test_cubic_series_first_step(shapes, form):
+    say("cubic first step", shapes, form)
+    run_pair(shapes, 1, 1e-2, gpu_kw=dict(FORM_KW[form], series_order=3), orc_kw=dict(series_order=3))
+
+
+def test_cubic_series_launches_and_flops():
+    shapes = [(256, 512)]     # L_hat explicit, R_hat factored
+    g = [to_dev(gradient(0, 0, 1, shapes[0], 1e-2))]
+    runs = {}
+    for order in (2, 3):
+        opt = Jorge(shapes, series_order=order)
+        opt.set_timing(True)
+        opt.step([torch.zeros(shapes[0], device="cuda")], g, 0.1)
+        runs[order] = (opt.read_timing(), opt.stage_flops())
+    assert runs[2][0]["poly2"][1] == 0 and runs[3][0]["poly2"][1] == 1
+    m, n = shapes[0]
+    # Explicit L_hat: X V (2 m^3) one level after V; factored R_hat (k = m): S S (m^3, symmetric).
+    f2, f3 = runs[2][1], runs[3][1]
+    assert f3["poly2"] == 2 * m ** 3 + 2 * n * m * m
+    assert f3["poly"] == 2 * m ** 3 + m ** 3
+    assert f2["poly"] == 2 * m ** 3 + 2 * n * m * m
