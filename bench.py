@@ -220,8 +220,11 @@ def main():
     g_launches = sum(timing[k][1] for k in GEMM_STAGES)
     achieved = g_flops / (g_ms * 1e-3) / 1e12
     f_paper = sum(falg_paper(m, n) for m, n in shapes) * updates_clean / steps
-    hbm = stage_bytes(shapes)
-    w_ms = timing["weight"][0] / max(1, timing["weight"][1])
+    hbm = {}  # the bandwidth-bound kernels: algorithmic bytes / average launch time
+    for k, nbytes in stage_bytes(shapes).items():
+        k_ms = timing[k][0] / max(1, timing[k][1])
+        gbs = nbytes / (k_ms * 1e-3) / 1e9 if k_ms else 0.0
+        hbm[k] = {"achieved": gbs, "frac": gbs / PEAK_HBM_GBS, "bytes_per_launch": nbytes}
     forms = {"explicit": 0, "factored": 0}
     for l in range(len(shapes)):
         for side in (0, 1):
@@ -253,8 +256,7 @@ def main():
         "mfma_util_pct": 100.0 * g_flops / steps / (inst_ms / steps * 1e-3) / (PEAK_FP32_MFMA_TFLOPS * 1e12),
         # the same step's flops counted in the paper's explicit order, per second of step time
         "paper_order_tflops": f_paper / (total_ms / steps * 1e-3) / 1e12,
-        "hbm": {"kernel": "weight", "achieved": hbm["weight"] / (w_ms * 1e-3) / 1e9 if w_ms else 0.0,
-                "peak": PEAK_HBM_GBS, "unit": "GB/s"},
+        "hbm": dict(hbm, peak=PEAK_HBM_GBS, unit="GB/s"),
         "stages": per_stage,
     }
     if args.cpu_budget > 0:

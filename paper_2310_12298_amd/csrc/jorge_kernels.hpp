@@ -33,8 +33,10 @@ __global__ void init_factors_kernel(const FactorDev* __restrict__ f, float l0) {
 // Gradient stage-in over 64 x 64 blocks: copies G (dense m x n, caller's
 // buffer) into the padded operand Gp and its transpose Gpt, updates
 // m_SGD = beta1 m_SGD + G (Algorithm 3) and writes the block's sum of m_SGD^2.
-// Both the row-major reads and the transposed writes are coalesced; the
-// transpose goes through LDS.
+// Each thread moves groups of four consecutive elements: 16-byte accesses
+// where the layer's rows allow them (n a multiple of 4, G 16-byte aligned),
+// element by element otherwise. Rows are read and the transpose is written
+// in 256-byte runs per 16 threads; the transpose goes through LDS.
 __global__ __launch_bounds__(kEwThreads) void stagein_kernel(const LayerDev* __restrict__ layers,
                                                              const StageTile* __restrict__ tiles,
                                                              int layer_base, PtrBatch grads,
@@ -45,23 +47,53 @@ __global__ __launch_bounds__(kEwThreads) void stagein_kernel(const LayerDev* __r
     const LayerDev& L = layers[st.layer];
     const float* __restrict__ G = grads.p[st.layer - layer_base];
     const int m = L.m, n = L.n;
+    const bool vec = (n & 3) == 0 && (reinterpret_cast<uintptr_t>(G) & 15) == 0;
     double part = 0.0;
-    for (int e = threadIdx.x; e < 64 * 64; e += kEwThreads) {
-        const int r = e >> 6, c = e & 63, gr = st.r0 + r, gc = st.c0 + c;
-        if (gr < m && gc < n) {
-            const float g = G[(size_t)gr * n + gc];
-            L.Gp[(size_t)gr * L.np + gc] = g;
-            float* ms = L.msgd + (size_t)gr * n + gc;
-            const float v = beta1 * *ms + g;
-            *ms = v;
-            part += (double)v * (double)v;
-            blk[r][c] = g;
+    // Row r, columns c .. c+3 of the block.
+    for (int q = threadIdx.x; q < 64 * 16; q += kEwThreads) {
+        const int r = q >> 4, c = (q & 15) * 4, gr = st.r0 + r, gc = st.c0 + c;
+        if (gr >= m || gc >= n) continue;
+        const size_t gi = (size_t)gr * n + gc;
+        f32x4 g, v;
+        if (vec) {  // gc + 3 < n: n and gc are multiples of 4
+            g = *reinterpret_cast<const f32x4*>(G + gi);
+            const f32x4 ms = *reinterpret_cast<const f32x4*>(L.msgd + gi);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) v[j] = beta1 * ms[j] + g[j];
+            *reinterpret_cast<f32x4*>(L.Gp + (size_t)gr * L.np + gc) = g;
+            *reinterpret_cast<f32x4*>(L.msgd + gi) = v;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) part += (double)v[j] * (double)v[j];
+        } else {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                g[j] = 0.0f;
+                if (gc + j < n) {
+                    g[j] = G[gi + j];
+                    L.Gp[(size_t)gr * L.np + gc + j] = g[j];
+                    const float w = beta1 * L.msgd[gi + j] + g[j];
+                    L.msgd[gi + j] = w;
+                    part += (double)w * (double)w;
+                }
+            }
         }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) blk[r][c + j] = g[j];
     }
     __syncthreads();
-    for (int e = threadIdx.x; e < 64 * 64; e += kEwThreads) {
-        const int c = e >> 6, r = e & 63, gr = st.r0 + r, gc = st.c0 + c;
-        if (gr < m && gc < n) L.Gpt[(size_t)gc * L.mp + gr] = blk[r][c];
+    // Column c, rows r .. r+3 of the block: Gpt[c][r..r+3] (mp is a multiple of 32).
+    for (int q = threadIdx.x; q < 64 * 16; q += kEwThreads) {
+        const int c = q >> 4, r = (q & 15) * 4, gr = st.r0 + r, gc = st.c0 + c;
+        if (gc >= n || gr >= m) continue;
+        float* dst = L.Gpt + (size_t)gc * L.mp + gr;
+        if (gr + 3 < m) {
+            f32x4 t;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) t[j] = blk[r + j][c];
+            *reinterpret_cast<f32x4*>(dst) = t;
+        } else {
+            for (int j = 0; gr + j < m; ++j) dst[j] = blk[r + j][c];
+        }
     }
     const double total = block_sum_256(part, red);
     if (threadIdx.x == 0) L.part_sgd[st.slot] = total;
