@@ -102,10 +102,12 @@ typedef struct jorge_hparams {
                                  order: deterministic, but rounded differently from an
                                  unsplit tile, and the split plan depends on every layer of
                                  the context); 0: never. Default 1. */
-    int32_t lds_chain_max;    /* factors whose size rounded up to 32 is at most this take the
-                                 explicit order in one workgroup with every matrix in LDS
-                                 (one launch for all of them) instead of the grouped levels;
-                                 0 disables. In [0, 64]. Default 64. */
+    int32_t lds_chain_max;    /* when every factor's size rounded up to 32 is at most this, each
+                                 factor update runs in the explicit order in one workgroup with
+                                 every matrix in LDS (one launch for all of them) instead of the
+                                 grouped levels. With any larger factor present the levels run
+                                 anyway and take the small factors too. 0 disables. In [0, 64].
+                                 Default 64. */
     int32_t precond_lowrank;  /* 1: on update steps, a factored factor A with d > 3k preconditions
                                  through A_new H = s A H - (s/2)(W H^T H + H W^T H), built from
                                  the update's own terms (about 6 k^2 d flops instead of a d x d

@@ -32,15 +32,18 @@
 //   chain5                                  factored: A^5 H (stored d x k), <U^T U, Q>
 //   ffinal    nu = ||X||_F, beta, c, s per factor
 //   poly      explicit: P^T                 factored: W = a A^5 H - b A^5 H S
+//             (series order 3: V = b X - e X X   /   V = b S - e S S)
+//   poly2     (series order 3 only) explicit: P^T = (I - a X + X V)^T   factored: W = a A^5 H - A^5 H V
 //   update    explicit: Z = s A P           factored: A <- s A - (s/2)(W H^T + H W^T)
 //   symm      explicit: A <- (Z + Z^T)/2
-//   precond   T = L_hat G, then G~ = T R_hat fused with m <- beta1 m + (1-beta1) G~
+//   precond   T = L_hat G, then G~ = T R_hat fused with m <- beta1 m + (1-beta1) G~;
+//             on update steps a factored factor with d > 3k supplies A_new H from the
+//             update's own terms instead (low-rank preconditioning)
 //   lfinal    ||m||, ||m_SGD||, grafted step g
 //   weight    theta <- theta (1 - lr wd) - g m
-// Factors of padded size up to hp.lds_chain_max (at most 64) skip the levels:
-// lds_chain_kernel runs each one's whole explicit-order update in one
-// workgroup with every matrix in LDS, on a second stream concurrent with the
-// levels (forked after stage-in, joined before preconditioning).
+// When every factor has padded size up to hp.lds_chain_max (at most 64), the
+// levels are replaced by one launch of lds_chain_kernel, which runs each
+// factor's whole explicit-order update in one workgroup with every matrix in LDS.
 // Non-update steps run stage-in, precond, lfinal and weight only.
 #include <hip/hip_runtime.h>
 
@@ -149,10 +152,6 @@ struct jorge_ctx {
     std::vector<int> grouped, chain;   // factors of the grouped levels / of the LDS chain
     int* dgrouped = nullptr;
     int* dchain = nullptr;
-    // The LDS chain runs on a library-owned stream (default priority), forked
-    // from the context's stream after stage-in and joined before preconditioning.
-    hipStream_t side = nullptr;
-    hipEvent_t ev_fork = nullptr, ev_join = nullptr;
     float* splitws = nullptr;     // partial products of split tiles (shared by the stages, in turn)
     int64_t splitws_blocks = 0;
     // Per stage: products with both operands K-major, and (literal mode only)
@@ -250,7 +249,7 @@ int tile_count(int M, int N) { return (int)(tiles_of(M) * tiles_of(N)); }
 
 constexpr int kXcds = 8;  // workgroup b of a launch runs on XCD b % 8, in increasing b
 constexpr int kSlots = 512;   // resident GEMM workgroups: 256 CUs x 2
-constexpr int kMinSplitK = 512;  // shortest K piece of a split tile
+constexpr int kMinSplitK = 64;  // shortest K piece of a split tile
 
 // Splits the K range of long tiles when a stage has too few tiles to keep
 // every workgroup slot busy: with W the stage's total tile work (sum of K)
@@ -398,6 +397,12 @@ size_t plan(jorge_ctx* c) {
         return o;
     };
     const bool sym = c->hp.symmetrize != 0;
+    // The LDS chain takes the factor updates only when it replaces the grouped
+    // levels altogether: with any larger factor present the levels run anyway,
+    // and the small factors' tiles fill slots of theirs that would idle.
+    int max_dp = 0;
+    for (const auto& L : c->layers) max_dp = std::max(max_dp, std::max(L.mp, L.np));
+    const bool use_chain = max_dp <= c->hp.lds_chain_max;
     for (auto& L : c->layers) {
         for (int side = 0; side < 2; ++side) {
             FactorHost F{};
@@ -407,7 +412,7 @@ size_t plan(jorge_ctx* c) {
             F.dp = side == 0 ? L.mp : L.np;
             F.k = side == 0 ? L.n : L.m;
             F.kp = side == 0 ? L.np : L.mp;
-            F.chain = F.dp <= c->hp.lds_chain_max;
+            F.chain = use_chain;
             if (F.chain || c->hp.factor_form == JORGE_FORM_EXPLICIT) F.expl = true;
             else if (c->hp.factor_form == JORGE_FORM_FACTORED) F.expl = false;
             else F.expl = explicit_is_cheaper(F.dp, F.kp, sym, c->hp.series_order);
@@ -962,9 +967,6 @@ void free_ctx(jorge_ctx* c) {
     if (c->dsym) (void)hipFree(c->dsym);
     if (c->dgrouped) (void)hipFree(c->dgrouped);
     if (c->dchain) (void)hipFree(c->dchain);
-    if (c->ev_fork) (void)hipEventDestroy(c->ev_fork);
-    if (c->ev_join) (void)hipEventDestroy(c->ev_join);
-    if (c->side) (void)hipStreamDestroy(c->side);
     if (c->arena) (void)hipFree(c->arena);
     for (auto& l : c->pending) {
         (void)hipEventDestroy(l.start);
@@ -982,16 +984,13 @@ jorge_status launch_stage(jorge_ctx* c, int stage, float beta1) {
 
 jorge_status run_update(jorge_ctx* c, double beta2) {
     jorge_status s;
-    if (!c->chain.empty()) {  // concurrent with the levels: they touch none of its factors
-        JORGE_HIP(c, hipEventRecord(c->ev_fork, c->stream));
-        JORGE_HIP(c, hipStreamWaitEvent(c->side, c->ev_fork, 0));
-        TimedLaunch tl(c, ST_LDS_CHAIN, c->side);
-        hipLaunchKernelGGL(lds_chain_kernel, dim3((unsigned)c->chain.size()), dim3(kGemmThreads), 0, c->side,
+    if (!c->chain.empty()) {  // every factor of the context (the levels below are then empty)
+        TimedLaunch tl(c, ST_LDS_CHAIN);
+        hipLaunchKernelGGL(lds_chain_kernel, dim3((unsigned)c->chain.size()), dim3(kGemmThreads), 0, c->stream,
                            c->dfactors, c->dchain, beta2, (int)c->hp.beta_mode, (int)c->hp.symmetrize,
                            (int)c->hp.series_order);
         tl.finish();
         JORGE_HIP(c, hipGetLastError());
-        JORGE_HIP(c, hipEventRecord(c->ev_join, c->side));
     }
     for (int lv : kLevels) {
         if (lv == ST_POLY && !c->grouped.empty()) {  // every grouped factor's nu is complete after chain5
@@ -1010,7 +1009,6 @@ jorge_status run_update(jorge_ctx* c, double beta2) {
         tl.finish();
         JORGE_HIP(c, hipGetLastError());
     }
-    if (!c->chain.empty()) JORGE_HIP(c, hipStreamWaitEvent(c->stream, c->ev_join, 0));
     return JORGE_OK;
 }
 
@@ -1089,12 +1087,6 @@ jorge_status jorge_create(const jorge_shape* shapes, int32_t num_layers, const j
     if ((st = upload(c, c->sym_tiles, &c->dsym)) != JORGE_OK) return bail(st);
     if ((st = upload(c, c->grouped, &c->dgrouped)) != JORGE_OK) return bail(st);
     if ((st = upload(c, c->chain, &c->dchain)) != JORGE_OK) return bail(st);
-    if (!c->chain.empty()) {
-        if (hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking) != hipSuccess ||
-            hipEventCreateWithFlags(&c->ev_fork, hipEventDisableTiming) != hipSuccess ||
-            hipEventCreateWithFlags(&c->ev_join, hipEventDisableTiming) != hipSuccess)
-            return bail(JORGE_ERR_HIP);
-    }
     for (int i = 0; i < ST_COUNT; ++i)
         for (GemmStage* s : {&c->nt[i], &c->nn[i]})
             if ((st = upload_stage(c, *s)) != JORGE_OK) return bail(st);

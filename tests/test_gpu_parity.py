@@ -22,8 +22,8 @@ STEP_TOL = 1e-5
 TRAJ_TOL = 1e-3
 # Evaluation orders of the factor update: the paper's explicit powers, the
 # factored order through the statistic's factor H (both through the grouped
-# levels only), and the default per-factor choice, where factors of padded
-# size <= 64 take the one-workgroup LDS chain.
+# levels only), and the default per-factor choice, where a context whose
+# factors all have padded size <= 64 runs them in the one-workgroup LDS chain.
 FORMS = ("explicit", "factored", "auto")
 FORM_KW = {"explicit": dict(factor_form="explicit", lds_chain_max=0),
            "factored": dict(factor_form="factored", lds_chain_max=0),
@@ -359,16 +359,27 @@ def test_split_k_parity_and_determinism(form):
             assert rel(x.cpu().numpy(), z.cpu().numpy()) < 1e-5, (l, k)   # split vs unsplit rounding
 
 
+SMALL_SHAPES = [(64, 64), (32, 48), (5, 3), (40, 1), (33, 60), (64, 32), (1, 64), (50, 17)]
+
+
 @pytest.mark.parametrize("symmetrize", [True, False])
 def test_lds_chain_small_factors(symmetrize):
-    """Factors of padded size <= 64 run their whole update in one workgroup, in LDS."""
-    shapes = [(64, 576), (32, 256), (5, 3), (64, 64), (40, 1), (33, 200), (200, 48), (64, 4608)]
+    """A context whose factors all have padded size <= 64 runs each whole update in
+    one workgroup, in LDS, instead of the grouped levels."""
+    shapes = SMALL_SHAPES
     say("LDS chain, symmetrize", symmetrize)
     opt = Jorge(shapes, symmetrize=symmetrize)
     opt.set_timing(True)
     opt.step([torch.zeros(s, device="cuda") for s in shapes],
              [to_dev(gradient(0, l, 1, s, 1e-2)) for l, s in enumerate(shapes)], **HP)
-    assert opt.read_timing()["lds_chain"][1] == 1
+    tm = opt.read_timing()
+    assert tm["lds_chain"][1] == 1 and tm["gram"][1] == 0 and tm["update"][1] == 0
+    # One larger factor brings the levels back, and the small factors join them.
+    mixed = Jorge(shapes + [(64, 576)], symmetrize=symmetrize)
+    mixed.set_timing(True)
+    mixed.step([torch.zeros(s, device="cuda") for s in shapes + [(64, 576)]],
+               [to_dev(gradient(0, l, 1, s, 1e-2)) for l, s in enumerate(shapes + [(64, 576)])], **HP)
+    assert mixed.read_timing()["lds_chain"][1] == 0 and mixed.read_timing()["gram"][1] >= 1
     a = run_pair(shapes, 6, 1e-2, check_every=3, gpu_kw=dict(symmetrize=symmetrize),
                  orc_kw=dict(symmetrize=symmetrize))
     b = run_pair(shapes, 6, 1e-2, gpu_kw=dict(symmetrize=symmetrize, lds_chain_max=0),
@@ -452,9 +463,10 @@ def test_lowrank_preconditioning(interval):
 # series_order=3 keeps the cubic term of Eq. 5 that Section 3 drops: the
 # explicit order forms V = b X - e X X and then P = I - a X + X V, the factored
 # order V = b S - e S S and W = a A^5 H - A^5 H V, the LDS chain the explicit
-# steps in LDS. The shapes put factors in every path: LDS chain (d <= 64),
+# steps in LDS. The shapes put factors in every path of the grouped levels:
 # explicit, factored, low-rank preconditioning (factored with d > 3k), and a
-# long-K layer whose sparse levels split.
+# long-K layer whose sparse levels split; an all-small context takes the LDS
+# chain.
 CUBIC_SHAPES = [(64, 576), (48, 96), (300, 130), (256, 1152), (512, 128), (128, 2048)]
 
 
@@ -473,6 +485,18 @@ def test_cubic_series_term(form, symmetrize):
         po2 = orc2.step(po2, [gradient(0, l, t, s, 1e-2) for l, s in enumerate(CUBIC_SHAPES)], **HP)
     gap = max(rel(orc2.layers[l].R, orc.layers[l].R) for l in range(len(CUBIC_SHAPES)))
     assert gap > 100 * worst, (gap, worst)
+
+
+@pytest.mark.parametrize("symmetrize", [True, False])
+def test_cubic_series_term_lds_chain(symmetrize):
+    say("cubic series term, LDS chain, symmetrize", symmetrize)
+    kw = dict(series_order=3, symmetrize=symmetrize)
+    a = run_pair(SMALL_SHAPES, 6, 1e-2, check_every=2, gpu_kw=kw, orc_kw=kw)
+    b = run_pair(SMALL_SHAPES, 6, 1e-2, gpu_kw=dict(kw, lds_chain_max=0), orc_kw=kw)
+    for l in range(len(SMALL_SHAPES)):
+        for k in KINDS:
+            x, y = a[0].get_state(l, k), b[0].get_state(l, k)
+            assert rel(x.cpu().numpy(), y.cpu().numpy()) < 1e-5, (l, k)
 
 
 @pytest.mark.parametrize("shapes", [[(1, 1)], [(40, 1)], [(33, 65)], [(200, 300)], [(130, 260)]])
