@@ -522,3 +522,43 @@ def test_cubic_series_launches_and_flops():
     assert f3["poly2"] == 2 * m ** 3 + 2 * n * m * m
     assert f3["poly"] == 2 * m ** 3 + m ** 3
     assert f2["poly"] == 2 * m ** 3 + 2 * n * m * m
+
+
+# ---------------------------------------------------------------- HIP graph capture
+def test_graph_capture_replays_match_eager():
+    """jorge_step launches kernels only (no allocation, memset or host sync), so a
+    caller can capture an update step in a HIP graph and replay it with new
+    gradients copied into the captured buffers. Each replay, with unrelated eager
+    work and synchronisations in between, equals an eager step bitwise."""
+    shapes = [(64, 576), (130, 260), (512, 128), (128, 2048)]
+    say("graph capture")
+    grads = [torch.zeros(s, device="cuda") for s in shapes]
+    eager, graphed = Jorge(shapes), Jorge(shapes)
+    pe = [to_dev(initial_params(0, l, s)) for l, s in enumerate(shapes)]
+    pg = [p.clone() for p in pe]
+
+    def load(t):
+        for l, s in enumerate(shapes):
+            grads[l].copy_(to_dev(gradient(0, l, t, s, 1e-2)))
+
+    load(1)
+    eager.step(pe, grads, **HP)
+    graphed.step(pg, grads, **HP)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        graphed.set_stream(torch.cuda.current_stream().cuda_stream)
+        graphed.step(pg, grads, **HP)
+    graphed.set_stream(torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    for t in range(2, 6):
+        load(t)
+        eager.step(pe, grads, **HP)
+        graph.replay()
+        x = torch.randn(1 << 20, device="cuda")
+        (x * x).sum().item()
+        torch.cuda.synchronize()
+        for l in range(len(shapes)):
+            assert torch.equal(pe[l], pg[l]), (t, l)
+            for k in KINDS:
+                assert torch.equal(eager.get_state(l, k), graphed.get_state(l, k)), (t, l, k)
