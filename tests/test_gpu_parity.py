@@ -562,3 +562,52 @@ def test_graph_capture_replays_match_eager():
             assert torch.equal(pe[l], pg[l]), (t, l)
             for k in KINDS:
                 assert torch.equal(eager.get_state(l, k), graphed.get_state(l, k)), (t, l, k)
+
+
+# ---------------------------------------------------------------- maximum size
+# A rank-one statistic at the largest dimension the library accepts. For a
+# 1 x n layer G = g and R_hat_0 = a I: X = a^4 g^T g = nu u u^T with
+# nu = a^4 ||g||^2 and u = g / ||g||, so the series collapses to
+# P = I + q u u^T with q = -(c/4) nu + (5c^2/32) nu^2 (- (15c^3/128) nu^3),
+# R_hat_1 = s a P, L_hat_1 = s a (1 + q), and since g P = (1 + q) g the grafted
+# step is theta_1 = theta_0 (1 - lr wd) - lr g (Eq. 5-7, Alg. 2, Alg. 3). The
+# n x n factor (4.3 GB) is checked on sampled entries against this closed form;
+# its last element sits at the 2^32 - 4 byte offset of the 32-bit epilogue
+# addressing. The n x 1 layer puts the same factor on the L side.
+@pytest.mark.parametrize("series_order", [2, 3])
+@pytest.mark.parametrize("side", ["R", "L"])
+def test_maximum_dimension_rank_one_closed_form(side, series_order):
+    from oracle import BETA_CLAMPED, beta_select, init_factor  # noqa: F401
+    n = 32768
+    shape = (1, n) if side == "R" else (n, 1)
+    say("max dimension", shape, "series order", series_order)
+    eps, sigma = 1e-6, 1e-2
+    g = gradient(0, 0, 1, shape, sigma).astype(np.float64).ravel()
+    theta0 = initial_params(0, 0, shape)
+    opt = Jorge([shape], eps=eps, series_order=series_order)
+    pg = [to_dev(theta0)]
+    opt.step(pg, [to_dev(g.reshape(shape))], **HP)
+    a = eps ** -0.25
+    gg = float(g @ g)
+    nu = a ** 4 * gg
+    c, s, _ = beta_select(nu, HP["beta2"], BETA_CLAMPED)
+    q = -(c / 4) * nu + (5 * c * c / 32) * nu ** 2
+    if series_order == 3:
+        q -= (15 * c ** 3 / 128) * nu ** 3
+    big = opt.get_state(0, side)
+    rng = np.random.default_rng(7)
+    i = rng.integers(0, n, 4096)
+    j = rng.integers(0, n, 4096)
+    i = np.concatenate([i, np.arange(0, n, 128), [n - 1, n - 1, 0]])
+    j = np.concatenate([j, np.arange(0, n, 128), [n - 1, 0, n - 1]])
+    ti, tj = torch.from_numpy(i).cuda(), torch.from_numpy(j).cuda()
+    got = big[ti, tj].double().cpu().numpy()
+    ref = s * a * ((i == j).astype(np.float64) + q * g[i] * g[j] / gg)
+    assert np.abs(got - ref).max() <= 1e-6 * s * a, np.abs(got - ref).max() / (s * a)
+    assert torch.equal(big[ti, tj], big[tj, ti])                       # bitwise symmetric
+    small = opt.get_state(0, "L" if side == "R" else "R").item()
+    assert small == pytest.approx(s * a * (1 + q), rel=1e-6)
+    d = opt.read_diag(0)
+    assert d["nu_L"] == pytest.approx(nu, rel=1e-4) and d["nu_R"] == pytest.approx(nu, rel=1e-4)
+    want = theta0.astype(np.float64).ravel() * (1 - HP["lr"] * HP["weight_decay"]) - HP["lr"] * g
+    assert rel(pg[0].cpu().numpy().ravel(), want) <= 1e-6
