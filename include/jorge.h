@@ -63,8 +63,8 @@ typedef int32_t jorge_status;
 #define JORGE_FORM_FACTORED 2
 
 /* State tensors of one layer (Algorithm 2 and Algorithm 3). */
-#define JORGE_STATE_L       0 /* L_hat, rows x rows, fp32, symmetric        */
-#define JORGE_STATE_R       1 /* R_hat, cols x cols, fp32, symmetric        */
+#define JORGE_STATE_L       0 /* L_hat, rows x rows, fp32 (symmetric unless symmetrize = 0) */
+#define JORGE_STATE_R       1 /* R_hat, cols x cols, fp32 (symmetric unless symmetrize = 0) */
 #define JORGE_STATE_MOM     2 /* Jorge momentum m_t, rows x cols, fp32      */
 #define JORGE_STATE_MOM_SGD 3 /* SGD heavy-ball momentum m_SGD, rows x cols */
 
