@@ -97,11 +97,14 @@ typedef struct jorge_hparams {
                                  Algorithm 2's product; 0: Z itself. Default 1. */
     int32_t factor_form;      /* JORGE_FORM_*: evaluation order of each factor update.
                                  Default JORGE_FORM_AUTO. */
-    int32_t split_k;          /* 1: a GEMM level with too few tiles for the GPU splits its
-                                 long tiles along K (partial products summed in a fixed
-                                 order: deterministic, but rounded differently from an
-                                 unsplit tile, and the split plan depends on every layer of
-                                 the context); 0: never. Default 1. */
+    int32_t split_k;          /* 1: a GEMM level splits some of its tiles along K where the
+                                 library's cost model of the launch says it then finishes
+                                 sooner: a level with too few tiles for the GPU, or one whose
+                                 last round of tiles would leave most workgroups idle
+                                 (partial products summed in a fixed order: deterministic,
+                                 but rounded differently from an unsplit tile, and the split
+                                 plan depends on every layer of the context); 0: never.
+                                 Default 1. */
     int32_t lds_chain_max;    /* when every factor's size rounded up to 32 is at most this, each
                                  factor update runs in the explicit order in one workgroup with
                                  every matrix in LDS (one launch for all of them) instead of the
@@ -152,6 +155,16 @@ jorge_status jorge_create(const jorge_shape* shapes, int32_t num_layers,
  * the check returns JORGE_ERR_HIP (an internal error). */
 jorge_status jorge_plan(const jorge_shape* shapes, int32_t num_layers, const jorge_hparams* hp,
                         int64_t* arena_bytes);
+
+/* The grouped GEMM launches of each stage as jorge_plan builds them, without a
+ * GPU: for min(n, jorge_num_stages()) stages (numbered as for jorge_stage_name),
+ * units[i] receives the work units of the stage's grouped launches (whole
+ * 128 x 128 tiles plus the pieces of tiles split along K) and split_tiles[i]
+ * the number of tiles split along K (0 when split_k = 0). units and
+ * split_tiles are host arrays of n entries; either may be NULL, not both when
+ * n > 0. Same argument rules and errors as jorge_plan. */
+jorge_status jorge_plan_stages(const jorge_shape* shapes, int32_t num_layers, const jorge_hparams* hp,
+                               int64_t* units, int64_t* split_tiles, int32_t n);
 
 /* One Jorge step for every layer (Algorithm 2 with Algorithm 3 and decoupled
  * weight decay). With t the new step number (1 for the first call):

@@ -51,7 +51,9 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <functional>
 #include <new>
+#include <queue>
 #include <string>
 #include <vector>
 
@@ -251,66 +253,32 @@ constexpr int kXcds = 8;  // workgroup b of a launch runs on XCD b % 8, in incre
 constexpr int kSlots = 512;   // resident GEMM workgroups: 256 CUs x 2
 constexpr int kMinSplitK = 64;  // shortest K piece of a split tile
 
-// Splits the K range of long tiles when a stage has too few tiles to keep
-// every workgroup slot busy: with W the stage's total tile work (sum of K)
-// and target = max(W / kSlots, kMinSplitK), a tile of length K >= 2 target
-// is cut into floor(K / target) pieces of equal length (multiples of 32). Each piece leaves a partial product
-// in the split workspace; a fixup unit per split tile sums them in K order
-// and runs the epilogue.
-void split_stage(GemmStage& st) {
-    int64_t W = 0;
-    for (const TileDesc& t : st.tiles) W += t.k1 - t.k0;
-    const int64_t target = std::max<int64_t>(kMinSplitK, round_up((W + kSlots - 1) / kSlots, kSlab));
-    std::vector<TileDesc> out;
-    out.reserve(st.tiles.size());
-    for (const TileDesc& t : st.tiles) {
-        const int64_t K = t.k1 - t.k0;
-        const int64_t ns = K / target;  // pieces no shorter than the target
-        if (ns < 2) {
-            out.push_back(t);
-            continue;
-        }
-        const int chunk = (int)round_up((K + ns - 1) / ns, kSlab);
-        const int n = (int)((K + chunk - 1) / chunk);
-        st.fix.push_back({t.prob, t.tm, t.tn, t.slot, st.nparts, n, 0, 0});
-        for (int q = 0; q < n; ++q) {
-            TileDesc u = t;
-            u.k0 = t.k0 + q * chunk;
-            u.k1 = std::min(t.k1, u.k0 + chunk);
-            u.part = st.nparts + q;
-            out.push_back(u);
-        }
-        st.nparts += n;
-    }
-    st.tiles.swap(out);
-}
-
-// Puts a stage's tiles in dispatch order. The tiles are sorted by K, longest
+// Puts work units in dispatch order. The units are sorted by K, longest
 // first; each problem's tiles stay in bands of kGroupRows tile rows walked
-// column by column. Runs of consecutive tiles of one problem and one column (they
-// share the B panel and neighbouring A panels) are dealt, in that order, to
-// the XCD with the least accumulated work (K of the tile), so every XCD gets
-// a balanced, largest-first share whose tiles reuse panels in its own L2.
-// The shares are then interleaved so that XCD x's i-th tile sits at slot
-// kXcds * i + x; once a share is used up, its slots take the next tile of the
-// longest remaining share.
-void order_for_xcds(GemmStage& st) {
-    const size_t n = st.tiles.size();
+// column by column. Runs of consecutive units of one problem, one column and
+// one K range (they share the B panel and neighbouring A panels) are dealt,
+// in that order, to the XCD with the least accumulated work (K of the unit),
+// so every XCD gets a balanced, largest-first share whose units reuse panels
+// in its own L2. The shares are then interleaved so that XCD x's i-th unit
+// sits at slot kXcds * i + x; once a share is used up, its slots take the
+// next unit of the longest remaining share.
+void order_for_xcds(std::vector<TileDesc>& tiles) {
+    const size_t n = tiles.size();
     if (n == 0) return;
     // Longest K range first (stable: each problem's tiles stay together and in order).
-    std::stable_sort(st.tiles.begin(), st.tiles.end(), [&](const TileDesc& a, const TileDesc& b) {
+    std::stable_sort(tiles.begin(), tiles.end(), [&](const TileDesc& a, const TileDesc& b) {
         return a.k1 - a.k0 > b.k1 - b.k0;
     });
     std::vector<std::vector<TileDesc>> share(kXcds);
     std::vector<int64_t> work(kXcds, 0);
     for (size_t i = 0; i < n;) {
         size_t j = i + 1;
-        while (j < n && st.tiles[j].prob == st.tiles[i].prob && st.tiles[j].tn == st.tiles[i].tn &&
-               st.tiles[j].k0 == st.tiles[i].k0 && st.tiles[j].tm / kGroupRows == st.tiles[i].tm / kGroupRows)
+        while (j < n && tiles[j].prob == tiles[i].prob && tiles[j].tn == tiles[i].tn &&
+               tiles[j].k0 == tiles[i].k0 && tiles[j].tm / kGroupRows == tiles[i].tm / kGroupRows)
             ++j;
         const int x = (int)(std::min_element(work.begin(), work.end()) - work.begin());
-        for (size_t k = i; k < j; ++k) share[x].push_back(st.tiles[k]);
-        work[x] += (int64_t)(j - i) * (st.tiles[i].k1 - st.tiles[i].k0);
+        for (size_t k = i; k < j; ++k) share[x].push_back(tiles[k]);
+        work[x] += (int64_t)(j - i) * (tiles[i].k1 - tiles[i].k0);
         i = j;
     }
     std::vector<size_t> next(kXcds, 0);
@@ -327,6 +295,228 @@ void order_for_xcds(GemmStage& st) {
                 }
         }
         out.push_back(share[x][next[x]++]);
+    }
+    tiles.swap(out);
+}
+
+// Cost model of a grouped launch for the split planner, in units of one k
+// step of a 128 x 128 tile on a whole compute unit (0.058 us). Workgroup b
+// runs on XCD b mod kXcds, on one of that XCD's CUs. A CU holds two work
+// units at a time; two resident units share its throughput, a unit alone on
+// a CU runs at kLoneRate of it. A work unit costs its K plus its own
+// prologue and epilogue; the fixup launch costs a fixed start plus the
+// traffic of all partial products (64 KB each). Fitted on MI355X to the
+// per-level times of 512 x 4608 and 64 x 576 layers with the long tiles cut
+// into 1 .. 8 equal pieces or into pieces of a fixed length (most levels
+// within 5%).
+constexpr int kCus = kSlots / 2;
+constexpr int kCusPerXcd = kCus / kXcds;
+constexpr double kLoneRate = 0.9;
+constexpr int64_t kUnitCost = 64;
+constexpr int64_t kFixupStart = 200;
+constexpr int64_t kFixupPartsPerK = 5;
+// A split plan is kept only if the model puts it this much below the unsplit launch
+// (the partial products' traffic also slows the other units, which the model leaves out).
+constexpr double kSplitGain = 0.97;
+
+// Duration of a list of units (in dispatch order) on ncu CUs: placed one per
+// CU, then a second per CU; later, each unit goes to a CU with a free place,
+// CUs with no resident unit first. Each CU shares its throughput between its
+// resident units.
+double launch_span(const std::vector<int64_t>& work, int ncu) {
+    struct Cu {
+        double rem[2];
+        int n = 0;
+        double last = 0.0;
+        unsigned ver = 0;
+    };
+    std::vector<Cu> cu(ncu);
+    typedef std::pair<double, std::pair<int, unsigned>> Ev;  // (time, (cu, version))
+    std::priority_queue<Ev, std::vector<Ev>, std::greater<Ev>> events;
+    auto rate = [](int n) { return n == 1 ? kLoneRate : 0.5; };  // of each resident unit
+    auto next_done = [&](const Cu& c) {
+        const double m = c.n == 1 ? c.rem[0] : std::min(c.rem[0], c.rem[1]);
+        return c.last + m / rate(c.n);
+    };
+    size_t next = 0;
+    for (int round = 0; round < 2; ++round)
+        for (int i = 0; i < ncu && next < work.size(); ++i) cu[i].rem[cu[i].n++] = (double)work[next++];
+    for (int i = 0; i < ncu; ++i)
+        if (cu[i].n) events.push({next_done(cu[i]), {i, cu[i].ver}});
+    double span = 0.0;
+    std::vector<int> freed;
+    while (!events.empty()) {
+        // Every completion at this time, then the placements.
+        const double now = events.top().first;
+        freed.clear();
+        while (!events.empty() && events.top().first <= now) {
+            const Ev e = events.top();
+            events.pop();
+            Cu& c = cu[e.second.first];
+            if (e.second.second != c.ver) continue;
+            const double done_work = (e.first - c.last) * rate(c.n);
+            for (int j = 0; j < c.n; ++j) c.rem[j] -= done_work;
+            c.last = e.first;
+            const int done = (c.n == 2 && c.rem[1] < c.rem[0]) ? 1 : 0;
+            c.rem[done] = c.rem[c.n - 1];
+            --c.n;
+            ++c.ver;
+            span = std::max(span, e.first);
+            freed.push_back(e.second.first);
+        }
+        std::sort(freed.begin(), freed.end());
+        freed.erase(std::unique(freed.begin(), freed.end()), freed.end());
+        std::stable_sort(freed.begin(), freed.end(), [&](int a, int b) { return cu[a].n < cu[b].n; });
+        for (int pass = 0; pass < 2; ++pass)
+            for (int i : freed)
+                if (next < work.size() && cu[i].n == pass) cu[i].rem[cu[i].n++] = (double)work[next++];
+        for (int i : freed)  // each was brought up to now by its completion
+            if (cu[i].n) events.push({next_done(cu[i]), {i, ++cu[i].ver}});
+    }
+    return span;
+}
+
+// The K lengths of a tile of length K cut into pieces of length P (a multiple
+// of 32): whole pieces of P, and the rest as a last piece of its own when it
+// is at least kMinSplitK long, else added to the last whole piece. A single
+// piece means the tile stays whole.
+std::vector<int64_t> cut_tile(int64_t K, int64_t P) {
+    std::vector<int64_t> out;
+    if (P <= 0 || P >= K) return {K};
+    for (int64_t k = 0; k + P <= K; k += P) out.push_back(P);
+    const int64_t rest = K - P * (int64_t)out.size();
+    if (rest >= kMinSplitK) out.push_back(rest);
+    else out.back() += rest;
+    return out;
+}
+
+// Piece length that cuts K into q pieces of about equal length.
+int64_t piece_len(int64_t K, int q) { return round_up((K + q - 1) / q, kSlab); }
+
+// The work units of tiles cut into pieces of length plen[i] (0: whole), in
+// tile order with each tile's pieces in K order; parts counts the pieces of
+// cut tiles.
+std::vector<TileDesc> cut_units(const std::vector<TileDesc>& tiles, const std::vector<int64_t>& plen,
+                                int64_t* parts) {
+    std::vector<TileDesc> units;
+    units.reserve(tiles.size());
+    *parts = 0;
+    for (size_t i = 0; i < tiles.size(); ++i) {
+        const TileDesc& t = tiles[i];
+        const std::vector<int64_t> pieces = cut_tile(t.k1 - t.k0, plen[i]);
+        if (pieces.size() > 1) *parts += (int64_t)pieces.size();
+        int k = t.k0;
+        for (int64_t len : pieces) {
+            TileDesc u = t;
+            u.k0 = k;
+            u.k1 = k + (int)len;
+            k = u.k1;
+            units.push_back(u);
+        }
+    }
+    return units;
+}
+
+// Modelled duration of a stage whose tiles are cut into pieces of length
+// plen[i] (0: whole): the units in dispatch order, each XCD's share on its CUs,
+// plus the fixup launch.
+double modelled_cost(const std::vector<TileDesc>& tiles, const std::vector<int64_t>& plen) {
+    int64_t parts = 0;
+    std::vector<TileDesc> units = cut_units(tiles, plen, &parts);
+    order_for_xcds(units);
+    std::vector<std::vector<int64_t>> per(kXcds);
+    for (size_t b = 0; b < units.size(); ++b) per[b % kXcds].push_back(units[b].k1 - units[b].k0 + kUnitCost);
+    double cost = 0.0;
+    for (const auto& w : per) cost = std::max(cost, launch_span(w, kCusPerXcd));
+    if (parts) cost += (double)(kFixupStart + parts / kFixupPartsPerK);
+    return cost;
+}
+
+// Splits the K range of some tiles of a stage when the cost model above says
+// the launch then finishes sooner: a level with too few tiles to keep every CU
+// busy, a level held up by a few long tiles, or one whose last round of tiles
+// would leave CUs idle. Candidates, tiles taken longest first: no split;
+// every long tile (more than half the longest) in q = 2 .. 8 equal pieces;
+// every tile longer than P in pieces of P, for P a share of the stage's work
+// per CU (1, 1/2, 1/3, 1/4, 1/6, 1/8) or the longest tile over q; and all but
+// the last one or two rounds of kSlots tiles kept whole with every later tile
+// in 2 .. 6 pieces. Pieces are never shorter than kMinSplitK. Each piece leaves a
+// partial product in the split workspace; a fixup unit per split tile sums
+// them in K order and runs the epilogue, so results do not depend on the
+// schedule.
+void split_stage(GemmStage& st) {
+    const size_t n = st.tiles.size();
+    if (n == 0) return;
+    std::vector<size_t> idx(n);
+    for (size_t i = 0; i < n; ++i) idx[i] = i;
+    std::stable_sort(idx.begin(), idx.end(), [&](size_t a, size_t b) {
+        return st.tiles[a].k1 - st.tiles[a].k0 > st.tiles[b].k1 - st.tiles[b].k0;
+    });
+    std::vector<int64_t> klen(n);
+    int64_t W = 0;
+    for (size_t i = 0; i < n; ++i) {
+        klen[i] = st.tiles[idx[i]].k1 - st.tiles[idx[i]].k0;
+        W += klen[i];
+    }
+    // Candidates give piece lengths in longest-first order; the model takes them in tile order.
+    std::vector<int64_t> in_order(n, 0);
+    auto cost_of = [&](const std::vector<int64_t>& plen) {
+        for (size_t i = 0; i < n; ++i) in_order[idx[i]] = plen[i];
+        return modelled_cost(st.tiles, in_order);
+    };
+    const std::vector<int64_t> none(n, 0);
+    std::vector<int64_t> best = none;
+    const double base = cost_of(none);
+    // No plan finishes before the CUs have shared out all the work (splitting only adds units).
+    if (kSplitGain * base <= (double)(W + (int64_t)n * kUnitCost) / kCus) return;
+    double best_cost = base;
+    auto consider = [&](const std::vector<int64_t>& plen) {
+        const double c = cost_of(plen);
+        if (c < best_cost) {
+            best_cost = c;
+            best = plen;
+        }
+    };
+    for (int q = 2; q <= 8; ++q) {  // the long tiles in q equal pieces
+        std::vector<int64_t> plen(n, 0);
+        for (size_t i = 0; i < n && 2 * klen[i] > klen[0]; ++i)
+            if (klen[i] >= (int64_t)q * kMinSplitK) plen[i] = piece_len(klen[i], q);
+        consider(plen);
+    }
+    std::vector<int64_t> lens;
+    for (int m : {1, 2, 3, 4, 6, 8}) lens.push_back(round_up((W + (int64_t)m * kCus - 1) / ((int64_t)m * kCus), kSlab));
+    for (int q = 2; q <= 8; ++q) lens.push_back(piece_len(klen[0], q));
+    for (int64_t P : lens) {  // pieces of a fixed length
+        P = std::max<int64_t>(P, kMinSplitK);
+        std::vector<int64_t> plen(n, 0);
+        for (size_t i = 0; i < n; ++i)
+            if (klen[i] > P) plen[i] = P;
+        consider(plen);
+    }
+    const size_t rounds = (n - 1) / kSlots;  // whole rounds before the last one
+    for (size_t h = kSlots * (rounds > 2 ? rounds - 1 : 1); h < n; h += kSlots)  // the last rounds cut
+        for (int q = 2; q <= 6; ++q) {
+            std::vector<int64_t> plen(n, 0);
+            for (size_t i = h; i < n; ++i)
+                if (klen[i] >= (int64_t)q * kMinSplitK) plen[i] = piece_len(klen[i], q);
+            consider(plen);
+        }
+    if (!(best_cost < kSplitGain * base)) return;
+    std::vector<int64_t> plen_of(n, 0);
+    for (size_t i = 0; i < n; ++i) plen_of[idx[i]] = best[i];
+    // The same units as the model's, with their workspace blocks and fixups.
+    int64_t parts = 0;
+    std::vector<TileDesc> out = cut_units(st.tiles, plen_of, &parts);
+    for (size_t u = 0; u < out.size();) {
+        size_t v = u + 1;
+        while (v < out.size() && out[v].prob == out[u].prob && out[v].tm == out[u].tm && out[v].tn == out[u].tn &&
+               out[v].k0 == out[v - 1].k1)
+            ++v;
+        if (v - u > 1) {
+            st.fix.push_back({out[u].prob, out[u].tm, out[u].tn, out[u].slot, st.nparts, (int)(v - u), 0, 0});
+            for (size_t q = u; q < v; ++q) out[q].part = st.nparts++;
+        }
+        u = v;
     }
     st.tiles.swap(out);
 }
@@ -910,7 +1100,7 @@ jorge_status tables_context(jorge_ctx* c, std::vector<LayerDev>& ld, std::vector
         for (int i = 0; i < ST_COUNT; ++i)
             for (GemmStage* st : {&c->nt[i], &c->nn[i]}) {
                 if (c->hp.split_k) split_stage(*st);
-                order_for_xcds(*st);
+                order_for_xcds(st->tiles);
                 c->splitws_blocks = std::max<int64_t>(c->splitws_blocks, st->nparts);
             }
         const std::string e = check_tables(c, fd);
@@ -1098,9 +1288,10 @@ jorge_status jorge_create(const jorge_shape* shapes, int32_t num_layers, const j
     return JORGE_OK;
 }
 
-jorge_status jorge_plan(const jorge_shape* shapes, int32_t num_layers, const jorge_hparams* hp,
-                        int64_t* arena_bytes) {
-    if (!arena_bytes) return JORGE_ERR_INVALID_ARGUMENT;
+// Lays out and builds the tables of a context on the host only (jorge_plan,
+// jorge_plan_stages); on success *out owns a context with no device memory.
+jorge_status plan_only(const jorge_shape* shapes, int32_t num_layers, const jorge_hparams* hp, jorge_ctx** out) {
+    *out = nullptr;
     jorge_hparams h;
     jorge_status st = validate_args(shapes, num_layers, hp, &h);
     if (st != JORGE_OK) return st;
@@ -1115,9 +1306,37 @@ jorge_status jorge_plan(const jorge_shape* shapes, int32_t num_layers, const jor
         st = tables_context(c, ld, fd);
         c->arena = nullptr;
     }
-    if (st == JORGE_OK) *arena_bytes = (int64_t)c->arena_bytes + c->splitws_blocks * kSplitBlock * (int64_t)sizeof(float);
+    if (st != JORGE_OK) {
+        delete c;
+        return st;
+    }
+    *out = c;
+    return JORGE_OK;
+}
+
+jorge_status jorge_plan(const jorge_shape* shapes, int32_t num_layers, const jorge_hparams* hp,
+                        int64_t* arena_bytes) {
+    if (!arena_bytes) return JORGE_ERR_INVALID_ARGUMENT;
+    jorge_ctx* c = nullptr;
+    const jorge_status st = plan_only(shapes, num_layers, hp, &c);
+    if (st != JORGE_OK) return st;
+    *arena_bytes = (int64_t)c->arena_bytes + c->splitws_blocks * kSplitBlock * (int64_t)sizeof(float);
     delete c;
-    return st;
+    return JORGE_OK;
+}
+
+jorge_status jorge_plan_stages(const jorge_shape* shapes, int32_t num_layers, const jorge_hparams* hp,
+                               int64_t* units, int64_t* split_tiles, int32_t n) {
+    if (n < 0 || (n > 0 && !units && !split_tiles)) return JORGE_ERR_INVALID_ARGUMENT;
+    jorge_ctx* c = nullptr;
+    const jorge_status st = plan_only(shapes, num_layers, hp, &c);
+    if (st != JORGE_OK) return st;
+    for (int i = 0; i < std::min<int>(n, ST_COUNT); ++i) {
+        if (units) units[i] = (int64_t)c->nt[i].tiles.size() + (int64_t)c->nn[i].tiles.size();
+        if (split_tiles) split_tiles[i] = (int64_t)c->nt[i].fix.size() + (int64_t)c->nn[i].fix.size();
+    }
+    delete c;
+    return JORGE_OK;
 }
 
 jorge_status jorge_step(jorge_ctx* c, float* const* params, const float* const* grads, double lr,

@@ -278,16 +278,22 @@ __device__ __forceinline__ void store_partial(float* __restrict__ blk, const f32
             }
 }
 
-__device__ __forceinline__ void add_partial(const float* __restrict__ blk, f32x16 (&acc)[2][2]) {
+// This thread's 64 values of one partial product.
+__device__ __forceinline__ void load_partial(const float* __restrict__ blk, f32x4 (&v)[16]) {
+#pragma unroll
+    for (int b = 0; b < 16; ++b) v[b] = *(global_f32x4*)(blk + b * 1024 + 4 * threadIdx.x);
+}
+
+__device__ __forceinline__ void add_partial(const f32x4 (&v)[16], f32x16 (&acc)[2][2]) {
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int j = 0; j < 2; ++j)
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-                const f32x4 v = *(global_f32x4*)(blk + ((i * 2 + j) * 4 + q) * 1024 + 4 * threadIdx.x);
-                acc[i][j][q * 4 + 0] += v[0]; acc[i][j][q * 4 + 1] += v[1];
-                acc[i][j][q * 4 + 2] += v[2]; acc[i][j][q * 4 + 3] += v[3];
+                const f32x4 w = v[(i * 2 + j) * 4 + q];
+                acc[i][j][q * 4 + 0] += w[0]; acc[i][j][q * 4 + 1] += w[1];
+                acc[i][j][q * 4 + 2] += w[2]; acc[i][j][q * 4 + 3] += w[3];
             }
 }
 
@@ -627,7 +633,19 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_fixup(const GemmProblem* __
         for (int j = 0; j < 2; ++j)
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
-    for (int s = 0; s < fd.nsplit; ++s) add_partial(ws + (size_t)(fd.part0 + s) * kSplitBlock, acc);
+    // Partials are added in K order; the loads of the next one are in flight
+    // while the current one is added (nsplit >= 2).
+    const float* blk = ws + (size_t)fd.part0 * kSplitBlock;
+    f32x4 v0[16], v1[16];
+    load_partial(blk, v0);
+    int s = 0;
+    for (; s + 2 <= fd.nsplit; s += 2) {
+        load_partial(blk + (size_t)(s + 1) * kSplitBlock, v1);
+        add_partial(v0, acc);
+        if (s + 2 < fd.nsplit) load_partial(blk + (size_t)(s + 2) * kSplitBlock, v0);
+        add_partial(v1, acc);
+    }
+    if (s < fd.nsplit) add_partial(v0, acc);
     gemm_epilogue(p, fd.tm, fd.tn, fd.slot, beta1, acc, red);
 }
 

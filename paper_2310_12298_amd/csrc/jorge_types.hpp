@@ -162,8 +162,9 @@ struct SymTile {
     int pad0;
 };
 
-// User pointers passed by value as kernel arguments, one batch of layers per launch.
-constexpr int kPtrBatch = 128;
+// User pointers passed by value as kernel arguments, one batch of layers per launch
+// (2 KB of pointers, within the 4 KB a kernel's arguments may take).
+constexpr int kPtrBatch = 256;
 struct PtrBatch {
     const float* p[kPtrBatch];
 };

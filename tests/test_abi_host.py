@@ -162,6 +162,39 @@ def test_plan_splits_long_tiles_of_sparse_levels(lib):
     assert J.Jorge.plan(r50) == J.Jorge.plan(r50, split_k=False)
 
 
+def test_plan_stages_split_choices(lib):
+    one = [(512, 4608)]
+    plain = J.Jorge.plan_stages(one, split_k=False)
+    split = J.Jorge.plan_stages(one)
+    assert set(plain) == set(split) and all(v[1] == 0 for v in plain.values())
+    for name, (units, nsplit) in split.items():
+        # A split tile becomes at least two units; an unsplit level keeps its tiles.
+        assert units >= plain[name][0] + nsplit, name
+        assert (units == plain[name][0]) == (nsplit == 0), name
+    # The chain levels hold ~150 tiles of K = 4608 for 512 CUs' worth of slots: split.
+    for name in ("gram", "pow4", "xform", "chain4", "chain5"):
+        assert split[name][1] >= 144, (name, split[name])
+    # The update level's 16 tiles of W^T H (K = 4608) would outlast its 682 short
+    # tiles: they are cut.
+    assert split["update"][1] >= 16
+    # Plans are deterministic.
+    assert J.Jorge.plan_stages(one) == split
+    # Full levels are left whole.
+    r50 = J.Jorge.plan_stages(CONFIGS["resnet50"][0])
+    assert all(v[1] == 0 for v in r50.values()), r50
+
+
+def test_plan_stages_rejects_bad_arguments(lib):
+    arr = (J.Shape * 1)(J.Shape(4, 4))
+    units = (ctypes.c_int64 * 4)()
+    assert lib.jorge_plan_stages(arr, 1, None, None, None, 4) == ERR_INVALID
+    assert lib.jorge_plan_stages(arr, 1, None, units, None, -1) == ERR_INVALID
+    assert lib.jorge_plan_stages(arr, 1, None, None, None, 0) == 0
+    assert lib.jorge_plan_stages(arr, 0, None, units, None, 4) == ERR_INVALID
+    bad = (J.Shape * 1)(J.Shape(4, 0))
+    assert lib.jorge_plan_stages(bad, 1, None, units, None, 4) == ERR_INVALID
+
+
 @pytest.mark.parametrize("form", FORMS)
 @pytest.mark.parametrize("symmetrize", [True, False])
 def test_plan_tables_of_edge_shapes(lib, form, symmetrize):
