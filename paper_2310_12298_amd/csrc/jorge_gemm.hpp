@@ -336,20 +336,26 @@ __device__ __forceinline__ double epilogue_body(const GemmProblem& p, int tm, in
     // Row strides in bytes.
     const unsigned sc = 4u * p.ldc, sc2 = 4u * p.ldc2, sx = 4u * p.ldx;
 
-    // Unmasked tiles (every element inside M x N, not a diagonal tile of a
-    // symmetric result) load all their X values before anything is stored, so
-    // one memory round trip serves the whole tile (X may be C itself, and the
-    // compiler keeps loads after earlier stores it cannot tell apart).
+    // Every X value the thread will use is loaded before anything is stored,
+    // so one memory round trip serves the whole tile (X may be C itself, and
+    // the compiler keeps loads after earlier stores it cannot tell apart).
+    // Masked tiles clamp positions outside M x N to the last row and column
+    // and drop those values; every position the thread uses is also one it
+    // writes, and no other thread writes it.
     f32x16 xv[2][2];
-    if constexpr (kRead && !MASKED) {
+    if constexpr (kRead) {
 #pragma unroll
         for (int i = 0; i < 2; ++i)
 #pragma unroll
             for (int j = 0; j < 2; ++j) {
                 const int col = col0 + wx * 64 + j * 32 + (lane & 31);
+                const int colc = MASKED ? min(col, p.N - 1) : col;
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
-                    const unsigned ox = (unsigned)(row0 + wy * 64 + i * 32 + q * 8 + h * 4) * sx + 4u * (unsigned)col;
+                    // rowb .. rowb+3 are all inside M when rowb is (M is a multiple of 4).
+                    const int rowb = row0 + wy * 64 + i * 32 + q * 8 + h * 4;
+                    const int rowc = MASKED ? min(rowb, p.M - 4) : rowb;
+                    const unsigned ox = (unsigned)rowc * sx + 4u * (unsigned)colc;
 #pragma unroll
                     for (int e = 0; e < 4; ++e) xv[i][j][q * 4 + e] = ld_at(X, ox + e * sx);
                 }
@@ -367,21 +373,14 @@ __device__ __forceinline__ double epilogue_body(const GemmProblem& p, int tm, in
                 const int rowb = row0 + wy * 64 + i * 32 + q * 8 + h * 4;
                 // rowb .. rowb+3 are all inside M when rowb is (M is a multiple of 4).
                 if (MASKED && (rowb >= p.M || col >= p.N)) continue;
-                // Masked tiles read X per group of 4 rows; within a diagonal tile
-                // only positions on or above the diagonal, each read and written
-                // by the same thread.
+                // X at positions this thread writes (read and written by the same thread).
                 f32x4 x;
-                if constexpr (kRead && MASKED) {
-                    const unsigned ox = (unsigned)rowb * sx + 4u * (unsigned)col;
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) x[e] = (!diag || rowb + e <= col) ? ld_at(X, ox + e * sx) : 0.0f;
-                }
                 f32x4 out;
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     const float v = acc[i][j][q * 4 + e];
                     float o = cc * v;
-                    if constexpr (kRead && !MASKED) x[e] = xv[i][j][q * 4 + e];
+                    if constexpr (kRead) x[e] = xv[i][j][q * 4 + e];
                     if constexpr (kReadX) {
                         const float id = (ident && rowb + e == col && col < p.valid_m) ? ci : 0.0f;
                         o = (id + cx * x[e]) + o;
@@ -473,24 +472,26 @@ __device__ __forceinline__ double epilogue_momentum(const GemmProblem& p, int tm
     const int wy = wave >> 1, wx = wave & 1, h = lane >> 5;
     float* mom = p.mom;
     const unsigned sm = 4u * p.ldmom;
-    // Unmasked (interior) tiles load all of this thread's momentum values
-    // before any is stored; masked tiles go element by element.
+    // All of this thread's momentum values are loaded before any is stored
+    // (one memory round trip per tile); masked tiles clamp positions outside
+    // the dense valid_m x valid_n momentum to its last row and column and
+    // drop those values.
     f32x16 mv[2][2];
-    if constexpr (!MASKED) {
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < 2; ++i)
 #pragma unroll
-            for (int j = 0; j < 2; ++j) {
-                const int col = col0 + wx * 64 + j * 32 + (lane & 31);
+        for (int j = 0; j < 2; ++j) {
+            const int col = col0 + wx * 64 + j * 32 + (lane & 31);
+            const int colc = MASKED ? min(col, p.valid_n - 1) : col;
 #pragma unroll
-                for (int q = 0; q < 4; ++q)
+            for (int q = 0; q < 4; ++q)
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const int row = row0 + wy * 64 + i * 32 + q * 8 + h * 4 + e;
-                        mv[i][j][q * 4 + e] = ld_at(mom, (unsigned)row * sm + 4u * (unsigned)col);
-                    }
-            }
-    }
+                for (int e = 0; e < 4; ++e) {
+                    const int row = row0 + wy * 64 + i * 32 + q * 8 + h * 4 + e;
+                    const int rowc = MASKED ? min(row, p.valid_m - 1) : row;
+                    mv[i][j][q * 4 + e] = ld_at(mom, (unsigned)rowc * sm + 4u * (unsigned)colc);
+                }
+        }
     double part = 0.0;
 #pragma unroll
     for (int i = 0; i < 2; ++i)
@@ -504,7 +505,7 @@ __device__ __forceinline__ double epilogue_momentum(const GemmProblem& p, int tm
                     const int row = row0 + wy * 64 + i * 32 + q * 8 + h * 4 + e;
                     if (MASKED && !(row < p.valid_m && col < p.valid_n)) continue;
                     const unsigned o = (unsigned)row * sm + 4u * (unsigned)col;
-                    const float old = MASKED ? ld_at(mom, o) : mv[i][j][q * 4 + e];
+                    const float old = mv[i][j][q * 4 + e];
                     const float mn = beta1 * old + (1.0f - beta1) * acc[i][j][q * 4 + e];
                     st_at(mom, o, mn);
                     part += (double)mn * (double)mn;
