@@ -531,8 +531,8 @@ jorge_status launch_gemm(jorge_ctx* c, const GemmStage& st, int stage, float bet
     JORGE_HIP(c, hipGetLastError());
     if (!st.fix.empty()) {
         TimedLaunch tf(c, ST_FIXUP);
-        hipLaunchKernelGGL(gemm_fixup, dim3((unsigned)st.fix.size()), dim3(kGemmThreads), 0, c->stream,
-                           st.dprobs, st.dfix, beta1, c->splitws);
+        hipLaunchKernelGGL(gemm_fixup, dim3((unsigned)st.fix.size() * kWaveSlots), dim3(kFixupThreads), 0,
+                           c->stream, st.dprobs, st.dfix, beta1, c->splitws);
         tf.finish();
         JORGE_HIP(c, hipGetLastError());
     }
@@ -632,7 +632,7 @@ size_t plan(jorge_ctx* c) {
                 F.off_v2t = take(kk);  // H^T W, k x k
                 F.off_xa = take(kd);   // A_new H, d x k
             }
-            F.off_part = take((size_t)F.nparts * sizeof(double));
+            F.off_part = take((size_t)F.nparts * kWaveSlots * sizeof(double));
             F.off_sc = take(sizeof(FactorScalars));
             (side == 0 ? L.fL : L.fR) = (int)c->factors.size();
             c->factors.push_back(F);
@@ -645,7 +645,7 @@ size_t plan(jorge_ctx* c) {
         L.off_mom = take(dense);
         L.off_msgd = take(dense);
         L.n_part_m = tile_count(L.mp, L.np);
-        L.off_part_m = take((size_t)L.n_part_m * sizeof(double));
+        L.off_part_m = take((size_t)L.n_part_m * kWaveSlots * sizeof(double));
         L.n_part_sgd = ((L.m + 63) / 64) * ((L.n + 63) / 64);
         L.off_part_sgd = take((size_t)L.n_part_sgd * sizeof(double));
         L.off_ls = take(sizeof(LayerScalars));
@@ -1004,7 +1004,7 @@ std::string check_stage(const jorge_ctx* c, const GemmStage& st, bool bk, const 
         if (tm < 0 || tn < 0 || tm >= tiles_of(p.M) || tn >= tiles_of(p.N) || (p.upper && tm > tn))
             return std::string(name) + ": tile index";
         if ((p.flags & (EF_NORM | EF_DOT | EF_MOMENTUM)) &&
-            (slot < 0 || !in_buffer(c, p.partials, (int64_t)(slot + 1) * (int64_t)sizeof(double))))
+            (slot < 0 || !in_buffer(c, p.partials, (int64_t)(slot + 1) * kWaveSlots * (int64_t)sizeof(double))))
             return std::string(name) + ": partial slot";
         return "";
     };
@@ -1061,7 +1061,7 @@ std::string check_tables(const jorge_ctx* c, const std::vector<FactorDev>& fd) {
             return "symmetrize tile";
     }
     for (const FactorDev& F : fd)
-        if (!in_buffer(c, F.partials, (int64_t)F.nparts * (int64_t)sizeof(double)) || F.nparts < 1)
+        if (!in_buffer(c, F.partials, (int64_t)F.nparts * kWaveSlots * (int64_t)sizeof(double)) || F.nparts < 1)
             return "factor partials";
     for (int fi : c->chain) {  // lds_chain_kernel: A (dp x dp), H (dp x kp), scalars
         const FactorDev& F = fd[fi];

@@ -163,6 +163,13 @@ __device__ __forceinline__ void mma_slab(const float* sa, const float* sb, int w
     }
 }
 
+// Sum of one double per lane over a 64-lane wave, in a fixed order.
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+    return v;
+}
+
 // Sum of one double per thread over the workgroup, in a fixed order.
 __device__ __forceinline__ double block_sum_256(double v, double* red) {
 #pragma unroll
@@ -262,8 +269,9 @@ __device__ __forceinline__ void gemm_mainloop(const GemmProblem& p, int tm, int 
     __syncthreads();  // every wave is done with both stages
 }
 
-// Partial products of split tiles: thread t keeps its 64 accumulators as 16
-// float4, float4 q of a block at q * 1024 + 4 t (coalesced across threads).
+// Partial products of split tiles: thread t (= 64 wave + lane) keeps its 64
+// accumulators as 16 float4, float4 q of a block at q * 1024 + 4 t (coalesced
+// across threads).
 __device__ __forceinline__ void store_partial(float* __restrict__ blk, const f32x16 (&acc)[2][2]) {
 #pragma unroll
     for (int i = 0; i < 2; ++i)
@@ -278,10 +286,10 @@ __device__ __forceinline__ void store_partial(float* __restrict__ blk, const f32
             }
 }
 
-// This thread's 64 values of one partial product.
-__device__ __forceinline__ void load_partial(const float* __restrict__ blk, f32x4 (&v)[16]) {
+// The 64 values of one partial product that thread t of the computing workgroup kept.
+__device__ __forceinline__ void load_partial(const float* __restrict__ blk, int t, f32x4 (&v)[16]) {
 #pragma unroll
-    for (int b = 0; b < 16; ++b) v[b] = *(global_f32x4*)(blk + b * 1024 + 4 * threadIdx.x);
+    for (int b = 0; b < 16; ++b) v[b] = *(global_f32x4*)(blk + b * 1024 + 4 * t);
 }
 
 __device__ __forceinline__ void add_partial(const f32x4 (&v)[16], f32x16 (&acc)[2][2]) {
@@ -321,11 +329,10 @@ __device__ __forceinline__ void st4_at(float* base, unsigned byte_off, f32x4 v) 
 // and on diagonal tiles of symmetric results.
 template <int F, bool UP, bool MASKED>
 __device__ __forceinline__ double epilogue_body(const GemmProblem& p, int tm, int tn, const f32x16 (&acc)[2][2],
-                                                float ci, float cx, float cc) {
+                                                float ci, float cx, float cc, int lane, int wave) {
     constexpr bool kReadX = (F & EF_READX) != 0;
     constexpr bool kRead = (F & (EF_READX | EF_DOT)) != 0;
     const int row0 = tm * kTile, col0 = tn * kTile;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int wy = wave >> 1, wx = wave & 1, h = lane >> 5;
     const bool diag = MASKED && UP && tm == tn;
     const bool ident = kReadX && ci != 0.f && tm == tn;
@@ -424,12 +431,11 @@ __device__ __forceinline__ double epilogue_body(const GemmProblem& p, int tm, in
 // The epilogue for a flag combination without a compiled body (not used by
 // the launch tables the library builds; kept so every combination works).
 __device__ __forceinline__ double epilogue_generic(const GemmProblem& p, int tm, int tn, const f32x16 (&acc)[2][2],
-                                                float ci, float cx, float cc) {
+                                                float ci, float cx, float cc, int lane, int wave) {
     double part = 0.0;
     const int F = p.flags;
     const bool up = p.upper != 0;
     const int row0 = tm * kTile, col0 = tn * kTile;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int wy = wave >> 1, wx = wave & 1, h = lane >> 5;
     float* C = p.C;
     float* C2 = p.C2;
@@ -466,9 +472,8 @@ __device__ __forceinline__ double epilogue_generic(const GemmProblem& p, int tm,
 // m = beta1 m + (1 - beta1) acc on the dense valid_m x valid_n momentum.
 template <bool MASKED>
 __device__ __forceinline__ double epilogue_momentum(const GemmProblem& p, int tm, int tn,
-                                                    const f32x16 (&acc)[2][2], float beta1) {
+                                                    const f32x16 (&acc)[2][2], float beta1, int lane, int wave) {
     const int row0 = tm * kTile, col0 = tn * kTile;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int wy = wave >> 1, wx = wave & 1, h = lane >> 5;
     float* mom = p.mom;
     const unsigned sm = 4u * p.ldmom;
@@ -514,9 +519,11 @@ __device__ __forceinline__ double epilogue_momentum(const GemmProblem& p, int tm
     return part;
 }
 
-// The epilogue of tile (tm, tn) of problem p for the product in acc; beta1
-// is the momentum of EF_MOMENTUM. All threads of the workgroup call it.
-// One uniform switch picks the compiled body for the problem's flags.
+// The epilogue of quadrant `wave` of tile (tm, tn) of problem p for the
+// product in acc (this lane's accumulators); beta1 is the momentum of
+// EF_MOMENTUM. One uniform switch picks the compiled body for the problem's
+// flags. The wave's partial sum (norm, dot product) goes to sub-slot `wave`
+// of the tile's slot.
 //
 // Symmetric results (p.upper): only tiles with tm <= tn are computed. An
 // element (row, col) with row <= col is written at (row, col) and at
@@ -525,15 +532,15 @@ __device__ __forceinline__ double epilogue_momentum(const GemmProblem& p, int tm
 // The epilogue reads X only at the positions it is about to write, by the
 // same thread, so X may alias C (an in-place update).
 __device__ __forceinline__ void gemm_epilogue(const GemmProblem& p, int tm, int tn, int slot, float beta1,
-                                              const f32x16 (&acc)[2][2], double* red) {
+                                              const f32x16 (&acc)[2][2], int lane, int wave) {
     const int flags = p.flags;
     double part = 0.0;
     if (flags & EF_MOMENTUM) {
         // Interior tiles of the dense valid_m x valid_n momentum need no masks.
         if ((tm + 1) * kTile <= p.valid_m && (tn + 1) * kTile <= p.valid_n)
-            part = epilogue_momentum<false>(p, tm, tn, acc, beta1);
+            part = epilogue_momentum<false>(p, tm, tn, acc, beta1, lane, wave);
         else
-            part = epilogue_momentum<true>(p, tm, tn, acc, beta1);
+            part = epilogue_momentum<true>(p, tm, tn, acc, beta1, lane, wave);
     } else {
         float ci = 0.f, cx = 0.f, cc = 1.f;
         if (p.coef != CO_ONE) {
@@ -553,47 +560,47 @@ __device__ __forceinline__ void gemm_epilogue(const GemmProblem& p, int tm, int 
         const int key = flags | (p.upper ? 256 : 0);
         const bool masked = (tm + 1) * kTile > p.M || (tn + 1) * kTile > p.N || (p.upper && tm == tn);
         switch (key) {
-            case EF_STORE: part = masked ? epilogue_body<EF_STORE, false, true>(p, tm, tn, acc, ci, cx, cc)
-                            : epilogue_body<EF_STORE, false, false>(p, tm, tn, acc, ci, cx, cc); break;
-            case EF_STORE | 256: part = masked ? epilogue_body<EF_STORE, true, true>(p, tm, tn, acc, ci, cx, cc)
-                            : epilogue_body<EF_STORE, true, false>(p, tm, tn, acc, ci, cx, cc); break;
-            case EF_STORE_T: part = masked ? epilogue_body<EF_STORE_T, false, true>(p, tm, tn, acc, ci, cx, cc)
-                            : epilogue_body<EF_STORE_T, false, false>(p, tm, tn, acc, ci, cx, cc); break;
-            case EF_DOT | 256: part = masked ? epilogue_body<EF_DOT, true, true>(p, tm, tn, acc, ci, cx, cc)
-                            : epilogue_body<EF_DOT, true, false>(p, tm, tn, acc, ci, cx, cc); break;
+            case EF_STORE: part = masked ? epilogue_body<EF_STORE, false, true>(p, tm, tn, acc, ci, cx, cc, lane, wave)
+                            : epilogue_body<EF_STORE, false, false>(p, tm, tn, acc, ci, cx, cc, lane, wave); break;
+            case EF_STORE | 256: part = masked ? epilogue_body<EF_STORE, true, true>(p, tm, tn, acc, ci, cx, cc, lane, wave)
+                            : epilogue_body<EF_STORE, true, false>(p, tm, tn, acc, ci, cx, cc, lane, wave); break;
+            case EF_STORE_T: part = masked ? epilogue_body<EF_STORE_T, false, true>(p, tm, tn, acc, ci, cx, cc, lane, wave)
+                            : epilogue_body<EF_STORE_T, false, false>(p, tm, tn, acc, ci, cx, cc, lane, wave); break;
+            case EF_DOT | 256: part = masked ? epilogue_body<EF_DOT, true, true>(p, tm, tn, acc, ci, cx, cc, lane, wave)
+                            : epilogue_body<EF_DOT, true, false>(p, tm, tn, acc, ci, cx, cc, lane, wave); break;
             case EF_STORE | EF_STORE_T | EF_NORM:
-                part = masked ? epilogue_body<EF_STORE | EF_STORE_T | EF_NORM, false, true>(p, tm, tn, acc, ci, cx, cc)
-                            : epilogue_body<EF_STORE | EF_STORE_T | EF_NORM, false, false>(p, tm, tn, acc, ci, cx, cc);
+                part = masked ? epilogue_body<EF_STORE | EF_STORE_T | EF_NORM, false, true>(p, tm, tn, acc, ci, cx, cc, lane, wave)
+                            : epilogue_body<EF_STORE | EF_STORE_T | EF_NORM, false, false>(p, tm, tn, acc, ci, cx, cc, lane, wave);
                 break;
             case EF_STORE_T | EF_READX:
-                part = masked ? epilogue_body<EF_STORE_T | EF_READX, false, true>(p, tm, tn, acc, ci, cx, cc)
-                            : epilogue_body<EF_STORE_T | EF_READX, false, false>(p, tm, tn, acc, ci, cx, cc);
+                part = masked ? epilogue_body<EF_STORE_T | EF_READX, false, true>(p, tm, tn, acc, ci, cx, cc, lane, wave)
+                            : epilogue_body<EF_STORE_T | EF_READX, false, false>(p, tm, tn, acc, ci, cx, cc, lane, wave);
                 break;
             case EF_STORE | EF_READX:
-                part = masked ? epilogue_body<EF_STORE | EF_READX, false, true>(p, tm, tn, acc, ci, cx, cc)
-                            : epilogue_body<EF_STORE | EF_READX, false, false>(p, tm, tn, acc, ci, cx, cc);
+                part = masked ? epilogue_body<EF_STORE | EF_READX, false, true>(p, tm, tn, acc, ci, cx, cc, lane, wave)
+                            : epilogue_body<EF_STORE | EF_READX, false, false>(p, tm, tn, acc, ci, cx, cc, lane, wave);
                 break;
             case EF_STORE | EF_STORE_T:
-                part = masked ? epilogue_body<EF_STORE | EF_STORE_T, false, true>(p, tm, tn, acc, ci, cx, cc)
-                              : epilogue_body<EF_STORE | EF_STORE_T, false, false>(p, tm, tn, acc, ci, cx, cc);
+                part = masked ? epilogue_body<EF_STORE | EF_STORE_T, false, true>(p, tm, tn, acc, ci, cx, cc, lane, wave)
+                              : epilogue_body<EF_STORE | EF_STORE_T, false, false>(p, tm, tn, acc, ci, cx, cc, lane, wave);
                 break;
             case EF_STORE | EF_STORE_T | EF_READX:
-                part = masked ? epilogue_body<EF_STORE | EF_STORE_T | EF_READX, false, true>(p, tm, tn, acc, ci, cx, cc)
+                part = masked ? epilogue_body<EF_STORE | EF_STORE_T | EF_READX, false, true>(p, tm, tn, acc, ci, cx, cc, lane, wave)
                               : epilogue_body<EF_STORE | EF_STORE_T | EF_READX, false, false>(p, tm, tn, acc, ci, cx,
-                                                                                              cc);
+                                                                                              cc, lane, wave);
                 break;
             case EF_STORE | EF_READX | 256:
-                part = masked ? epilogue_body<EF_STORE | EF_READX, true, true>(p, tm, tn, acc, ci, cx, cc)
-                            : epilogue_body<EF_STORE | EF_READX, true, false>(p, tm, tn, acc, ci, cx, cc);
+                part = masked ? epilogue_body<EF_STORE | EF_READX, true, true>(p, tm, tn, acc, ci, cx, cc, lane, wave)
+                            : epilogue_body<EF_STORE | EF_READX, true, false>(p, tm, tn, acc, ci, cx, cc, lane, wave);
                 break;
             default:  // any other combination: every flag tested at run time
-                part = epilogue_generic(p, tm, tn, acc, ci, cx, cc);
+                part = epilogue_generic(p, tm, tn, acc, ci, cx, cc, lane, wave);
                 break;
         }
     }
     if (flags & (EF_NORM | EF_DOT | EF_MOMENTUM)) {
-        const double total = block_sum_256(part, red);
-        if (threadIdx.x == 0) p.partials[slot] = total;
+        const double total = wave_sum(part);
+        if (lane == 0) p.partials[(size_t)slot * kWaveSlots + wave] = total;
     }
 }
 
@@ -608,7 +615,6 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_grouped(const GemmProble
                                                                 float beta1, float* __restrict__ ws) {
     __shared__ __attribute__((aligned(16))) GemmStageLds s0;
     __shared__ __attribute__((aligned(16))) GemmStageLds s1;
-    __shared__ double red[4];
     const TileDesc td = tiles[blockIdx.x];
     const GemmProblem p = probs[td.prob];
     f32x16 acc[2][2];
@@ -616,16 +622,22 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_grouped(const GemmProble
     if (td.part >= 0)
         store_partial(ws + (size_t)td.part * kSplitBlock, acc);
     else
-        gemm_epilogue(p, td.tm, td.tn, td.slot, beta1, acc, red);
+        gemm_epilogue(p, td.tm, td.tn, td.slot, beta1, acc, threadIdx.x & 63, threadIdx.x >> 6);
 }
 
 // Split tiles of a grouped launch: sums the partial products in K order
-// (a fixed order, so results are deterministic) and runs the epilogue.
-__global__ __launch_bounds__(kGemmThreads) void gemm_fixup(const GemmProblem* __restrict__ probs,
-                                                           const FixupDesc* __restrict__ fix, float beta1,
-                                                           const float* __restrict__ ws) {
-    __shared__ double red[4];
-    const FixupDesc fd = fix[blockIdx.x];
+// (a fixed order, so results are deterministic) and runs the epilogue. One
+// single-wave workgroup per 64 x 64 quadrant of each split tile (workgroup b:
+// tile b / 4, quadrant b % 4), so a tile's pieces are read by four
+// workgroups in parallel; each takes the accumulators that wave b % 4 of the
+// computing workgroups kept.
+constexpr int kFixupThreads = 64;
+__global__ __launch_bounds__(kFixupThreads) void gemm_fixup(const GemmProblem* __restrict__ probs,
+                                                            const FixupDesc* __restrict__ fix, float beta1,
+                                                            const float* __restrict__ ws) {
+    const FixupDesc fd = fix[blockIdx.x / kWaveSlots];
+    const int wave = blockIdx.x % kWaveSlots, lane = threadIdx.x;
+    const int t = wave * 64 + lane;  // thread of the computing workgroup
     const GemmProblem p = probs[fd.prob];
     f32x16 acc[2][2];
 #pragma unroll
@@ -638,16 +650,16 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_fixup(const GemmProblem* __
     // while the current one is added (nsplit >= 2).
     const float* blk = ws + (size_t)fd.part0 * kSplitBlock;
     f32x4 v0[16], v1[16];
-    load_partial(blk, v0);
+    load_partial(blk, t, v0);
     int s = 0;
     for (; s + 2 <= fd.nsplit; s += 2) {
-        load_partial(blk + (size_t)(s + 1) * kSplitBlock, v1);
+        load_partial(blk + (size_t)(s + 1) * kSplitBlock, t, v1);
         add_partial(v0, acc);
-        if (s + 2 < fd.nsplit) load_partial(blk + (size_t)(s + 2) * kSplitBlock, v0);
+        if (s + 2 < fd.nsplit) load_partial(blk + (size_t)(s + 2) * kSplitBlock, t, v0);
         add_partial(v1, acc);
     }
     if (s < fd.nsplit) add_partial(v0, acc);
-    gemm_epilogue(p, fd.tm, fd.tn, fd.slot, beta1, acc, red);
+    gemm_epilogue(p, fd.tm, fd.tn, fd.slot, beta1, acc, lane, wave);
 }
 
 }  // namespace jorge

@@ -10,13 +10,6 @@ namespace jorge {
 
 constexpr int kEwThreads = 256;
 
-// Sum of one double per lane over a 64-lane wave, in a fixed order.
-__device__ __forceinline__ double wave_sum(double v) {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
-    return v;
-}
-
 // Fixed-order sum of n doubles by one wave (every lane gets the total).
 __device__ __forceinline__ double wave_sum_array(const double* __restrict__ x, int n) {
     double v = 0.0;
@@ -131,7 +124,7 @@ __device__ __forceinline__ FactorScalars factor_scalars(double nu, double beta2,
 __global__ void factor_finalize_kernel(const FactorDev* __restrict__ f, const int* __restrict__ list,
                                        double beta2, int mode) {
     const FactorDev F = f[list[blockIdx.x]];
-    const double nu = sqrt(fmax(0.0, wave_sum_array(F.partials, F.nparts)));
+    const double nu = sqrt(fmax(0.0, wave_sum_array(F.partials, F.nparts * kWaveSlots)));
     if (threadIdx.x == 0) *F.sc = factor_scalars(nu, beta2, mode);
 }
 
@@ -382,7 +375,7 @@ __global__ __launch_bounds__(kGemmThreads) void lds_chain_kernel(const FactorDev
 __global__ void layer_finalize_kernel(const LayerDev* __restrict__ layers, double lr, double wd,
                                       int graft) {
     const LayerDev L = layers[blockIdx.x];
-    const double nm = sqrt(wave_sum_array(L.part_m, L.n_part_m));
+    const double nm = sqrt(wave_sum_array(L.part_m, L.n_part_m * kWaveSlots));
     const double ns = sqrt(wave_sum_array(L.part_sgd, L.n_part_sgd));
     if (threadIdx.x != 0) return;
     double g = lr;

@@ -69,7 +69,7 @@ struct GemmProblem {
     const float* X;            // EF_READX / EF_DOT operand
     const FactorScalars* sc;   // coefficients (any Coef but CO_ONE)
     float* mom;                // EF_MOMENTUM: dense valid_m x valid_n momentum
-    double* partials;          // EF_NORM, EF_DOT, EF_MOMENTUM: one double per tile slot
+    double* partials;          // EF_NORM, EF_DOT, EF_MOMENTUM: kWaveSlots doubles per tile slot
     int M, N, K, K1;
     int lda, ldb, lda2, ldb2;
     int ldc, ldc2, ldx, ldmom;
@@ -110,12 +110,16 @@ struct FixupDesc {
 
 // Floats per split-workspace block: one 128 x 128 tile.
 constexpr int kSplitBlock = 128 * 128;
+// Partial sums of a GEMM tile's epilogue (norms, dot products): one double
+// per 64 x 64 quadrant, each written by the wave that owns it; consumers sum
+// all kWaveSlots * (tile slots) of them in index order.
+constexpr int kWaveSlots = 4;
 
 // Device view of a factor (L_hat or R_hat of one layer).
 struct FactorDev {
     float* A;              // state, dp x dp, ld = dp, zero outside the d x d block
     FactorScalars* sc;
-    double* partials;      // per-tile partial sums of ||X||_F^2
+    double* partials;      // partial sums of ||X||_F^2: kWaveSlots per tile slot
     float* Z;              // explicit form: the unsymmetrized product s A P (dp x dp)
     const float* H;        // the statistic's factor, row-major d x k (ld kp, zero padded)
     int d, dp;
@@ -131,7 +135,7 @@ struct LayerDev {
     float* T;              // L_hat G, mp x np
     float* mom;            // m_t, dense m x n
     float* msgd;           // m_SGD, dense m x n
-    double* part_m;        // per-tile sums of m_ij^2
+    double* part_m;        // sums of m_ij^2: kWaveSlots per tile slot
     double* part_sgd;      // per-block sums of m_SGD,ij^2
     LayerScalars* ls;
     int m, n, mp, np;
