@@ -83,18 +83,24 @@ constexpr int kLevels[] = {ST_GRAM, ST_POW4, ST_XFORM, ST_CHAIN4, ST_CHAIN5, ST_
 constexpr size_t kAlign = 256;
 constexpr int kFlatChunkElems = 16384;
 constexpr int kGroupRows = 8;  // tile rows per group in the tile ordering
+constexpr int kXcds = 8;  // workgroup b of a launch runs on XCD b % 8, in increasing b
+constexpr int kSlots = 512;   // resident GEMM workgroups: 256 CUs x 2
+constexpr int kMinSplitK = 64;  // shortest K piece of a split tile
 
 inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 inline int64_t tiles_of(int64_t x) { return (x + kTile - 1) / kTile; }
 
 struct GemmStage {
+    bool kmajor_b = false;          // the NT launch (K-contiguous B): small mode is available
     std::vector<GemmProblem> probs;
     std::vector<TileDesc> tiles;    // work units, in dispatch order once uploaded
+    std::vector<SmallUnit> small;   // small-mode blocks (grouped by four into units of tiles)
     std::vector<FixupDesc> fix;     // split tiles
     int nparts = 0;                 // split-workspace blocks the stage uses
     double flops = 0.0;             // algorithmic flops of all its products
     GemmProblem* dprobs = nullptr;
     TileDesc* dtiles = nullptr;
+    SmallUnit* dsmall = nullptr;
     FixupDesc* dfix = nullptr;
     int ntiles() const { return (int)tiles.size(); }
 };
@@ -232,6 +238,15 @@ GemmProblem product(const float* A, int lda, const float* B, int ldb, int M, int
 // walked column by column, so concurrently running workgroups share panels.
 // flops: the product's algorithmic flops. Returns the number of partial-sum
 // slots (one per tile).
+// Whether a product may run in small mode (64 x 64 blocks, one wave each):
+// a product of the NT launch with at most 64 rows or columns and a short K,
+// other than the preconditioning products that update the momentum (their
+// 128 x 128 tiles measured faster).
+bool small_eligible(const GemmStage& st, const GemmProblem& p) {
+    return st.kmajor_b && p.K <= kSmallMaxK && (p.M <= kSmallDim || p.N <= kSmallDim) &&
+           !(p.flags & EF_MOMENTUM);
+}
+
 int add_problem(GemmStage& st, const GemmProblem& p, double flops) {
     const int idx = (int)st.probs.size();
     st.probs.push_back(p);
@@ -247,11 +262,56 @@ int add_problem(GemmStage& st, const GemmProblem& p, double flops) {
     return slot;
 }
 
+// Small mode pays where a launch has enough units to keep every CU busy:
+// then the padding of 128 x 128 tiles costs throughput, while a level with
+// few units is bound by its longest unit, which the single-buffered blocks
+// would lengthen. In a stage with at least kSlots tiles, every eligible
+// product's tiles are replaced by its 64 x 64 blocks: those quadrants of its
+// tiles that lie inside the product (and on or above the diagonal of a
+// symmetric result), each with its tile's partial-sum slot; the tile's first
+// block zeroes the partial sums of the others. The blocks are then grouped,
+// longest K first, four to a unit of the tile list.
+void make_small(GemmStage& st) {
+    if (st.tiles.size() < (size_t)kSlots) return;
+    std::vector<char> small(st.probs.size(), 0);
+    bool any = false;
+    for (size_t i = 0; i < st.probs.size(); ++i) any |= (small[i] = small_eligible(st, st.probs[i]));
+    if (!any) return;
+    std::vector<TileDesc> keep;
+    keep.reserve(st.tiles.size());
+    for (const TileDesc& t : st.tiles) {
+        if (!small[t.prob]) {
+            keep.push_back(t);
+            continue;
+        }
+        const GemmProblem& p = st.probs[t.prob];
+        const int bm_n = (p.M + kSmallDim - 1) / kSmallDim, bn_n = (p.N + kSmallDim - 1) / kSmallDim;
+        int zero = 0, first = -1;
+        for (int q = 0; q < kWaveSlots; ++q) {
+            const int bm = 2 * t.tm + (q >> 1), bn = 2 * t.tn + (q & 1);
+            if (bm >= bm_n || bn >= bn_n || (p.upper && bm > bn)) {
+                zero |= 1 << q;
+                continue;
+            }
+            if (first < 0) first = (int)st.small.size();
+            st.small.push_back({t.prob, bm, bn, t.slot, 0, 0, 0, 0});
+        }
+        if (p.flags & (EF_NORM | EF_DOT | EF_MOMENTUM)) st.small[first].zero_mask = zero;
+    }
+    st.tiles.swap(keep);
+    std::stable_sort(st.small.begin(), st.small.end(), [&](const SmallUnit& a, const SmallUnit& b) {
+        return st.probs[a.prob].K > st.probs[b.prob].K;
+    });
+    for (size_t i = 0; i < st.small.size(); i += kWaveSlots) {
+        const int n = (int)std::min<size_t>(kWaveSlots, st.small.size() - i);
+        int K = 0;
+        for (int j = 0; j < n; ++j) K = std::max(K, st.probs[st.small[i + j].prob].K);
+        st.tiles.push_back({st.small[i].prob, (int)i, n, -1, 0, K, kSmallGroup, 0});
+    }
+}
+
 int tile_count(int M, int N) { return (int)(tiles_of(M) * tiles_of(N)); }
 
-constexpr int kXcds = 8;  // workgroup b of a launch runs on XCD b % 8, in increasing b
-constexpr int kSlots = 512;   // resident GEMM workgroups: 256 CUs x 2
-constexpr int kMinSplitK = 64;  // shortest K piece of a split tile
 
 // Puts work units in dispatch order. The units are sorted by K, longest
 // first; each problem's tiles stay in bands of kGroupRows tile rows walked
@@ -461,7 +521,7 @@ void split_stage(GemmStage& st) {
     // Candidates give piece lengths in longest-first order; the model takes them in tile order.
     std::vector<int64_t> in_order(n, 0);
     auto cost_of = [&](const std::vector<int64_t>& plen) {
-        for (size_t i = 0; i < n; ++i) in_order[idx[i]] = plen[i];
+        for (size_t i = 0; i < n; ++i) in_order[idx[i]] = st.tiles[idx[i]].part == kSmallGroup ? 0 : plen[i];
         return modelled_cost(st.tiles, in_order);
     };
     const std::vector<int64_t> none(n, 0);
@@ -503,7 +563,7 @@ void split_stage(GemmStage& st) {
         }
     if (!(best_cost < kSplitGain * base)) return;
     std::vector<int64_t> plen_of(n, 0);
-    for (size_t i = 0; i < n; ++i) plen_of[idx[i]] = best[i];
+    for (size_t i = 0; i < n; ++i) plen_of[idx[i]] = st.tiles[idx[i]].part == kSmallGroup ? 0 : best[i];
     // The same units as the model's, with their workspace blocks and fixups.
     int64_t parts = 0;
     std::vector<TileDesc> out = cut_units(st.tiles, plen_of, &parts);
@@ -526,7 +586,7 @@ jorge_status launch_gemm(jorge_ctx* c, const GemmStage& st, int stage, float bet
     if (st.ntiles() == 0) return JORGE_OK;
     TimedLaunch tl(c, stage);
     hipLaunchKernelGGL((gemm_grouped<AK, BK>), dim3(st.ntiles()), dim3(kGemmThreads), 0, c->stream,
-                       st.dprobs, st.dtiles, beta1, c->splitws);
+                       st.dprobs, st.dtiles, st.dsmall, beta1, c->splitws);
     tl.finish();
     JORGE_HIP(c, hipGetLastError());
     if (!st.fix.empty()) {
@@ -1008,8 +1068,71 @@ std::string check_stage(const jorge_ctx* c, const GemmStage& st, bool bk, const 
             return std::string(name) + ": partial slot";
         return "";
     };
+    // The products in small mode: those with blocks.
+    std::vector<char> is_small(st.probs.size(), 0);
+    for (const SmallUnit& u : st.small)
+        if (u.prob >= 0 && u.prob < (int)st.probs.size()) is_small[u.prob] = 1;
+    // Small-mode units: groups of 1 to 4 blocks, each block in exactly one group,
+    // the group's K range that of its longest block.
+    std::vector<int> small_seen(st.small.size(), 0);
+    for (const TileDesc& t : st.tiles) {
+        if (t.part != kSmallGroup) continue;
+        if (!bk || t.tn < 1 || t.tn > kWaveSlots || t.tm < 0 || (size_t)t.tm + t.tn > st.small.size() || t.k0 != 0)
+            return std::string(name) + ": small-mode group";
+        int K = 0;
+        for (int j = 0; j < t.tn; ++j) {
+            if (small_seen[t.tm + j]++) return std::string(name) + ": small-mode block in two groups";
+            const int pi = st.small[t.tm + j].prob;
+            if (pi < 0 || pi >= (int)st.probs.size()) return std::string(name) + ": small-mode problem";
+            K = std::max(K, st.probs[pi].K);
+        }
+        if (t.k1 != K) return std::string(name) + ": small-mode group K";
+    }
+    // Every block of every small-mode problem is computed once; with partial sums,
+    // each tile's quadrants are computed or zeroed, never both.
+    std::vector<std::vector<int>> blocks(st.probs.size()), quads(st.probs.size());
+    for (size_t i = 0; i < st.small.size(); ++i) {
+        if (!small_seen[i]) return std::string(name) + ": small-mode block in no group";
+        const SmallUnit& u = st.small[i];
+        const GemmProblem& p = st.probs[u.prob];
+        const int bm_n = (p.M + kSmallDim - 1) / kSmallDim, bn_n = (p.N + kSmallDim - 1) / kSmallDim;
+        const std::string e = check_tile(u.prob, u.bm / 2, u.bn / 2, u.slot);
+        if (!e.empty()) return e;
+        if (!small_eligible(st, p) || u.bm < 0 || u.bn < 0 || u.bm >= bm_n || u.bn >= bn_n || (p.upper && u.bm > u.bn) ||
+            u.zero_mask < 0 || u.zero_mask >= (1 << kWaveSlots))
+            return std::string(name) + ": small-mode block";
+        auto& b = blocks[u.prob];
+        if (b.empty()) b.assign((size_t)bm_n * bn_n, 0);
+        if (b[(size_t)u.bm * bn_n + u.bn]++) return std::string(name) + ": small-mode block twice";
+        if (p.flags & (EF_NORM | EF_DOT | EF_MOMENTUM)) {
+            auto& q = quads[u.prob];
+            const int tn_n = (int)tiles_of(p.N);
+            if (q.empty()) q.assign((size_t)tiles_of(p.M) * tn_n, 0);
+            int& m = q[(size_t)(u.bm / 2) * tn_n + u.bn / 2];
+            const int mine = (1 << (((u.bm & 1) << 1) | (u.bn & 1))) | u.zero_mask;
+            if (m & mine) return std::string(name) + ": small-mode partial sum written twice";
+            m |= mine;
+        }
+    }
+    for (size_t i = 0; i < st.probs.size(); ++i) {
+        const GemmProblem& p = st.probs[i];
+        if (!is_small[i]) continue;
+        const int bm_n = (p.M + kSmallDim - 1) / kSmallDim, bn_n = (p.N + kSmallDim - 1) / kSmallDim;
+        for (int bm = 0; bm < bm_n; ++bm)
+            for (int bn = 0; bn < bn_n; ++bn)
+                if ((!p.upper || bm <= bn) && (blocks[i].empty() || blocks[i][(size_t)bm * bn_n + bn] != 1))
+                    return std::string(name) + ": small-mode coverage";
+        if (p.flags & (EF_NORM | EF_DOT | EF_MOMENTUM)) {
+            const int tm_n = (int)tiles_of(p.M), tn_n = (int)tiles_of(p.N);
+            for (int tm = 0; tm < tm_n; ++tm)
+                for (int tn = p.upper ? tm : 0; tn < tn_n; ++tn)
+                    if (quads[i][(size_t)tm * tn_n + tn] != (1 << kWaveSlots) - 1)
+                        return std::string(name) + ": small-mode partial sums";
+        }
+    }
     int64_t whole = 0, pieces = 0;
     for (const TileDesc& t : st.tiles) {
+        if (t.part == kSmallGroup) continue;
         const std::string e = check_tile(t.prob, t.tm, t.tn, t.slot);
         if (!e.empty()) return e;
         const GemmProblem& p = st.probs[t.prob];
@@ -1039,7 +1162,9 @@ std::string check_stage(const jorge_ctx* c, const GemmStage& st, bool bk, const 
         pieces -= f.nsplit;
     }
     int64_t tiles_total = 0;
-    for (const GemmProblem& p : st.probs) {
+    for (size_t i = 0; i < st.probs.size(); ++i) {
+        const GemmProblem& p = st.probs[i];
+        if (is_small[i]) continue;
         const int64_t a = tiles_of(p.M), b = tiles_of(p.N);
         tiles_total += p.upper ? a * (a + 1) / 2 : a * b;
     }
@@ -1096,9 +1221,11 @@ jorge_status layout_context(jorge_ctx* c, const jorge_shape* shapes, int32_t num
 // Launch tables for the arena at c->arena, checked on the host.
 jorge_status tables_context(jorge_ctx* c, std::vector<LayerDev>& ld, std::vector<FactorDev>& fd) {
     try {
+        for (int i = 0; i < ST_COUNT; ++i) c->nt[i].kmajor_b = true;
         build_tables(c, ld, fd);
         for (int i = 0; i < ST_COUNT; ++i)
             for (GemmStage* st : {&c->nt[i], &c->nn[i]}) {
+                make_small(*st);
                 if (c->hp.split_k) split_stage(*st);
                 order_for_xcds(st->tiles);
                 c->splitws_blocks = std::max<int64_t>(c->splitws_blocks, st->nparts);
@@ -1138,6 +1265,7 @@ jorge_status upload_stage(jorge_ctx* c, GemmStage& st) {
     jorge_status s = upload(c, st.probs, &st.dprobs);
     if (s != JORGE_OK) return s;
     if ((s = upload(c, st.fix, &st.dfix)) != JORGE_OK) return s;
+    if ((s = upload(c, st.small, &st.dsmall)) != JORGE_OK) return s;
     return upload(c, st.tiles, &st.dtiles);
 }
 
@@ -1147,6 +1275,7 @@ void free_ctx(jorge_ctx* c) {
         for (GemmStage* st : {&c->nt[i], &c->nn[i]}) {
             if (st->dprobs) (void)hipFree(st->dprobs);
             if (st->dtiles) (void)hipFree(st->dtiles);
+            if (st->dsmall) (void)hipFree(st->dsmall);
             if (st->dfix) (void)hipFree(st->dfix);
         }
     if (c->splitws) (void)hipFree(c->splitws);

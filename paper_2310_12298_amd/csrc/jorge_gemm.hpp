@@ -604,18 +604,78 @@ __device__ __forceinline__ void gemm_epilogue(const GemmProblem& p, int tm, int 
     }
 }
 
+// Global -> LDS directly, one wave: a 64 x 32 K-contiguous operand slab into
+// blocks 0 .. 7 at s (same layout as load_slab_lds; rows past lim clamped).
+__device__ __forceinline__ void load_slab_lds_wave(const float* __restrict__ base, int ld, int mn0, int lim,
+                                                   int k0, float* s) {
+    const int lane = threadIdx.x & 63;
+    const int chunk = (lane & 7) ^ (lane >> 3);
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+        const int row = min(mn0 + b * 8 + (lane >> 3), lim - 1);
+        const float* g = base + (size_t)row * ld + k0 + chunk * 4;
+        __builtin_amdgcn_global_load_lds((global_void*)g, (lds_void*)(s + b * kLdsBlock), 16, 0, 0);
+    }
+}
+
+// One small-mode block, computed by the calling wave alone in its own LDS
+// blocks sa, sb (8 blocks each): slabs are loaded, awaited and multiplied in
+// turn, with no workgroup barrier; the other waves of the CU hide the loads.
+// Then the epilogue of the block's quadrant, and the zeroing of the partial
+// sums of its tile's quadrants that no block computes.
+__device__ __forceinline__ void small_unit(const GemmProblem& p, const SmallUnit& su, float* sa, float* sb,
+                                           float beta1, int lane) {
+    f32x16 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+    const int row0 = su.bm * kSmallDim, col0 = su.bn * kSmallDim;
+    for (int k0 = 0; k0 < p.K; k0 += kSlab) {
+        const SlabSrc s = slab_src(p, k0);
+        load_slab_lds_wave(s.a, s.lda, row0, p.M, s.k, sa);
+        load_slab_lds_wave(s.b, s.ldb, col0, p.N, s.k, sb);
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's slab has landed
+        mma_slab<true, true>(sa, sb, 0, 0, lane, acc);
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // and has been read before it is refilled
+    }
+    const int quadrant = ((su.bm & 1) << 1) | (su.bn & 1);
+    gemm_epilogue(p, su.bm >> 1, su.bn >> 1, su.slot, beta1, acc, lane, quadrant);
+    if (su.zero_mask && lane == 0) {
+#pragma unroll
+        for (int q = 0; q < kWaveSlots; ++q)
+            if ((su.zero_mask >> q) & 1) p.partials[(size_t)su.slot * kWaveSlots + q] = 0.0;
+    }
+}
+
 // Grouped launch: one workgroup per work unit of the list. The list is in
 // dispatch order: consecutive workgroups go round-robin to the 8 XCDs, and
 // the host arranged it so each XCD's share is balanced and reuses operand
 // panels in its own L2. Units of split tiles leave their partial product in
-// ws for gemm_fixup.
+// ws for gemm_fixup. A small-mode unit is a group of up to four 64 x 64
+// blocks (small), one per wave, each in its own quarter of the LDS.
 template <bool AK, bool BK>
 __global__ __launch_bounds__(kGemmThreads, 2) void gemm_grouped(const GemmProblem* __restrict__ probs,
                                                                 const TileDesc* __restrict__ tiles,
+                                                                const SmallUnit* __restrict__ small,
                                                                 float beta1, float* __restrict__ ws) {
     __shared__ __attribute__((aligned(16))) GemmStageLds s0;
     __shared__ __attribute__((aligned(16))) GemmStageLds s1;
     const TileDesc td = tiles[blockIdx.x];
+    if (td.part == kSmallGroup) {
+        if constexpr (BK) {
+            const int w = threadIdx.x >> 6;
+            if (w < td.tn) {
+                const SmallUnit su = small[td.tm + w];
+                GemmStageLds& st = (w >> 1) ? s1 : s0;
+                const int half = (w & 1) * 8 * kLdsBlock;
+                small_unit(probs[su.prob], su, st.a + half, st.b + half, beta1, threadIdx.x & 63);
+            }
+        }
+        return;
+    }
     const GemmProblem p = probs[td.prob];
     f32x16 acc[2][2];
     gemm_mainloop<AK, BK>(p, td.tm, td.tn, td.k0, td.k1, s0, s1, acc);

@@ -92,9 +92,29 @@ struct TileDesc {
     int slot;  // partial-sum slot within the problem
     int k0;    // K range (multiples of 32)
     int k1;
-    int part;  // split workspace block, or -1 for a whole tile
+    int part;  // split workspace block, -1 for a whole tile, kSmallGroup for small-mode blocks
     int pad0;
 };
+
+// Small mode: a product with at most 64 rows or columns and a short K is
+// computed in 64 x 64 blocks, one wave per block, up to four blocks per
+// workgroup. Block (bm, bn) is quadrant ((bm & 1), (bn & 1)) of 128 x 128 tile
+// (bm / 2, bn / 2), with that tile's partial-sum slot; zero_mask lists the
+// quadrants of the tile that no block computes (outside the product, or below
+// the diagonal of a symmetric result), whose partial sums this block sets to 0.
+struct SmallUnit {
+    int prob;
+    int bm;
+    int bn;
+    int slot;
+    int zero_mask;
+    int pad0, pad1, pad2;
+};
+constexpr int kSmallDim = 64;     // rows or columns at most
+constexpr int kSmallMaxK = 256;   // K at most
+// TileDesc.part of a small-mode workgroup: tm = its first SmallUnit, tn = their
+// number (1 to 4), [k0, k1) = [0, the longest K among them).
+constexpr int kSmallGroup = -2;
 
 // A split tile of a grouped launch: its nsplit partial products sit in
 // workspace blocks part0 .. part0 + nsplit - 1, in K order.
