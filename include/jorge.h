@@ -158,13 +158,16 @@ jorge_status jorge_plan(const jorge_shape* shapes, int32_t num_layers, const jor
 
 /* The grouped GEMM launches of each stage as jorge_plan builds them, without a
  * GPU: for min(n, jorge_num_stages()) stages (numbered as for jorge_stage_name),
- * units[i] receives the work units of the stage's grouped launches (whole
- * 128 x 128 tiles plus the pieces of tiles split along K) and split_tiles[i]
- * the number of tiles split along K (0 when split_k = 0). units and
- * split_tiles are host arrays of n entries; either may be NULL, not both when
- * n > 0. Same argument rules and errors as jorge_plan. */
+ * units[i] receives the work units (workgroups) of the stage's grouped
+ * launches, split_tiles[i] the number of 128 x 128 tiles split along K (0 when
+ * split_k = 0) and small_blocks[i] the number of 64 x 64 blocks computed in
+ * small mode (products with at most 64 rows or columns, one wave per block,
+ * up to four per unit). A unit is a whole tile, a piece of a split tile or a
+ * group of small-mode blocks. units, split_tiles and small_blocks are host
+ * arrays of n entries; any may be NULL, not all when n > 0. Same argument
+ * rules and errors as jorge_plan. */
 jorge_status jorge_plan_stages(const jorge_shape* shapes, int32_t num_layers, const jorge_hparams* hp,
-                               int64_t* units, int64_t* split_tiles, int32_t n);
+                               int64_t* units, int64_t* split_tiles, int64_t* small_blocks, int32_t n);
 
 /* One Jorge step for every layer (Algorithm 2 with Algorithm 3 and decoupled
  * weight decay). With t the new step number (1 for the first call):

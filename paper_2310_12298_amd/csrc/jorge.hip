@@ -1455,14 +1455,15 @@ jorge_status jorge_plan(const jorge_shape* shapes, int32_t num_layers, const jor
 }
 
 jorge_status jorge_plan_stages(const jorge_shape* shapes, int32_t num_layers, const jorge_hparams* hp,
-                               int64_t* units, int64_t* split_tiles, int32_t n) {
-    if (n < 0 || (n > 0 && !units && !split_tiles)) return JORGE_ERR_INVALID_ARGUMENT;
+                               int64_t* units, int64_t* split_tiles, int64_t* small_blocks, int32_t n) {
+    if (n < 0 || (n > 0 && !units && !split_tiles && !small_blocks)) return JORGE_ERR_INVALID_ARGUMENT;
     jorge_ctx* c = nullptr;
     const jorge_status st = plan_only(shapes, num_layers, hp, &c);
     if (st != JORGE_OK) return st;
     for (int i = 0; i < std::min<int>(n, ST_COUNT); ++i) {
         if (units) units[i] = (int64_t)c->nt[i].tiles.size() + (int64_t)c->nn[i].tiles.size();
         if (split_tiles) split_tiles[i] = (int64_t)c->nt[i].fix.size() + (int64_t)c->nn[i].fix.size();
+        if (small_blocks) small_blocks[i] = (int64_t)c->nt[i].small.size() + (int64_t)c->nn[i].small.size();
     }
     delete c;
     return JORGE_OK;

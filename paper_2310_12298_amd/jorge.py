@@ -50,7 +50,7 @@ _SIGNATURES = {
                                     ctypes.POINTER(ctypes.c_int64)]),
     "jorge_plan_stages": (ctypes.c_int32, [ctypes.POINTER(Shape), ctypes.c_int32, ctypes.POINTER(HParams),
                                            ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_int64),
-                                           ctypes.c_int32]),
+                                           ctypes.POINTER(ctypes.c_int64), ctypes.c_int32]),
     "jorge_step": (ctypes.c_int32, [_P, ctypes.POINTER(_P), ctypes.POINTER(_P), ctypes.c_double,
                                     ctypes.c_double, ctypes.c_double, ctypes.c_double]),
     "jorge_get_state": (ctypes.c_int32, [_P, ctypes.c_int32, ctypes.c_int32, _P, ctypes.c_int64]),
@@ -160,15 +160,16 @@ class Jorge:
 
     @staticmethod
     def plan_stages(shapes, **hp):
-        """Per stage name: (work units, tiles split along K) of its grouped GEMM launches (no GPU)."""
+        """Per stage name: (work units, tiles split along K, small-mode blocks) of its grouped
+        GEMM launches (no GPU)."""
         lib = load_library()
         shapes = [(int(m), int(n)) for m, n in shapes]
         arr = (Shape * max(1, len(shapes)))(*[Shape(m, n) for m, n in shapes])
         h = Jorge.hparams(**hp)
         n = lib.jorge_num_stages()
-        units, split = (ctypes.c_int64 * n)(), (ctypes.c_int64 * n)()
-        _check(lib, lib.jorge_plan_stages(arr, len(shapes), ctypes.byref(h), units, split, n))
-        return {lib.jorge_stage_name(i).decode(): (units[i], split[i]) for i in range(n)}
+        units, split, small = (ctypes.c_int64 * n)(), (ctypes.c_int64 * n)(), (ctypes.c_int64 * n)()
+        _check(lib, lib.jorge_plan_stages(arr, len(shapes), ctypes.byref(h), units, split, small, n))
+        return {lib.jorge_stage_name(i).decode(): (units[i], split[i], small[i]) for i in range(n)}
 
     # -------------------------------------------------------------- stepping
     def _ptrs(self, tensors, what):

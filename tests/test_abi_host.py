@@ -167,7 +167,7 @@ def test_plan_stages_split_choices(lib):
     plain = J.Jorge.plan_stages(one, split_k=False)
     split = J.Jorge.plan_stages(one)
     assert set(plain) == set(split) and all(v[1] == 0 for v in plain.values())
-    for name, (units, nsplit) in split.items():
+    for name, (units, nsplit, _) in split.items():
         # A split tile becomes at least two units; an unsplit level keeps its tiles.
         assert units >= plain[name][0] + nsplit, name
         assert (units == plain[name][0]) == (nsplit == 0), name
@@ -184,15 +184,31 @@ def test_plan_stages_split_choices(lib):
     assert all(v[1] == 0 for v in r50.values()), r50
 
 
+def test_plan_stages_small_mode(lib):
+    # Full levels of many small layers run their at-most-64-wide products as 64 x 64
+    # blocks; a level of a few tiles (one 64 x 576 layer) keeps 128 x 128 tiles.
+    many = J.Jorge.plan_stages(CONFIGS["many_small"][0])
+    assert many["gram"][2] > 0 and many["pow4"][2] > 0
+    for name, (units, nsplit, small) in many.items():
+        assert units >= (small + 3) // 4, name   # at most four blocks per unit
+    one = J.Jorge.plan_stages([(64, 576)])
+    assert all(v[2] == 0 for v in one.values()), one
+    # The second preconditioning product updates the momentum: it stays in tiles.
+    assert many["precond_R"][2] == 0 and many["uprecond_R"][2] == 0
+    # The literal mode's NN launches have no small mode; its NT products still do.
+    lit = J.Jorge.plan_stages(CONFIGS["many_small"][0], symmetrize=False)
+    assert lit["gram"][2] > 0
+
+
 def test_plan_stages_rejects_bad_arguments(lib):
     arr = (J.Shape * 1)(J.Shape(4, 4))
     units = (ctypes.c_int64 * 4)()
-    assert lib.jorge_plan_stages(arr, 1, None, None, None, 4) == ERR_INVALID
-    assert lib.jorge_plan_stages(arr, 1, None, units, None, -1) == ERR_INVALID
-    assert lib.jorge_plan_stages(arr, 1, None, None, None, 0) == 0
-    assert lib.jorge_plan_stages(arr, 0, None, units, None, 4) == ERR_INVALID
+    assert lib.jorge_plan_stages(arr, 1, None, None, None, None, 4) == ERR_INVALID
+    assert lib.jorge_plan_stages(arr, 1, None, units, None, None, -1) == ERR_INVALID
+    assert lib.jorge_plan_stages(arr, 1, None, None, None, None, 0) == 0
+    assert lib.jorge_plan_stages(arr, 0, None, units, None, None, 4) == ERR_INVALID
     bad = (J.Shape * 1)(J.Shape(4, 0))
-    assert lib.jorge_plan_stages(bad, 1, None, units, None, 4) == ERR_INVALID
+    assert lib.jorge_plan_stages(bad, 1, None, units, None, None, 4) == ERR_INVALID
 
 
 @pytest.mark.parametrize("form", FORMS)
