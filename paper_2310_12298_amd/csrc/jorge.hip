@@ -239,12 +239,9 @@ GemmProblem product(const float* A, int lda, const float* B, int ldb, int M, int
 // flops: the product's algorithmic flops. Returns the number of partial-sum
 // slots (one per tile).
 // Whether a product may run in small mode (64 x 64 blocks, one wave each):
-// a product of the NT launch with at most 64 rows or columns and a short K,
-// other than the preconditioning products that update the momentum (their
-// 128 x 128 tiles measured faster).
+// a product of the NT launch with at most 64 rows or columns and a short K.
 bool small_eligible(const GemmStage& st, const GemmProblem& p) {
-    return st.kmajor_b && p.K <= kSmallMaxK && (p.M <= kSmallDim || p.N <= kSmallDim) &&
-           !(p.flags & EF_MOMENTUM);
+    return st.kmajor_b && p.K <= kSmallMaxK && (p.M <= kSmallDim || p.N <= kSmallDim);
 }
 
 int add_problem(GemmStage& st, const GemmProblem& p, double flops) {
@@ -264,8 +261,7 @@ int add_problem(GemmStage& st, const GemmProblem& p, double flops) {
 
 // Small mode pays where a launch has enough units to keep every CU busy:
 // then the padding of 128 x 128 tiles costs throughput, while a level with
-// few units is bound by its longest unit, which the single-buffered blocks
-// would lengthen. In a stage with at least kSlots tiles, every eligible
+// few units is bound by its longest unit, which a one-wave block lengthens. In a stage with at least kSlots tiles, every eligible
 // product's tiles are replaced by its 64 x 64 blocks: those quadrants of its
 // tiles that lie inside the product (and on or above the diagonal of a
 // symmetric result), each with its tile's partial-sum slot; the tile's first

@@ -44,6 +44,7 @@ constexpr int kLdsBlock = 8 * 32 + 32;        // floats per 8-row block, with it
 constexpr int kLdsMN = kTile + 8;             // row stride of an M/N-contiguous operand in LDS
 constexpr int kLdsOperand = 16 * kLdsBlock;   // floats per operand per stage (>= kSlab * kLdsMN)
 static_assert(kLdsOperand >= kSlab * kLdsMN, "LDS operand buffer too small");
+static_assert(kLdsOperand / 2 >= 2 * 64 * 16, "a small-mode stage (two 64 x 16 slabs) must fit in half an operand buffer");
 
 // Pointers into global memory (address space 1): loads through them compile
 // to global_load rather than flat_load, which would also count against the
@@ -604,26 +605,71 @@ __device__ __forceinline__ void gemm_epilogue(const GemmProblem& p, int tm, int 
     }
 }
 
-// Global -> LDS directly, one wave: a 64 x 32 K-contiguous operand slab into
-// blocks 0 .. 7 at s (same layout as load_slab_lds; rows past lim clamped).
-__device__ __forceinline__ void load_slab_lds_wave(const float* __restrict__ base, int ld, int mn0, int lim,
-                                                   int k0, float* s) {
+// Small-mode operand slab: 64 rows x 16 k in LDS as 4 groups of 16 rows of
+// 64 bytes, each group the 1 KB that one wave-wide 16-byte load to LDS
+// writes. Lane L of a load fills row L / 4 of its group; it reads logical
+// chunk (L % 4) ^ ((row / 4) % 4) of that row (chunk c holds k = 4c .. 4c+3),
+// so chunk c of row r sits at physical chunk c ^ ((r / 4) % 4): sixteen lanes
+// reading one chunk of sixteen consecutive rows hit sixteen distinct 16-byte
+// bank groups.
+constexpr int kSmallSlab = 16;                    // K per slab of a small-mode block
+constexpr int kSmallOperand = 64 * kSmallSlab;    // floats per operand slab
+
+// One wave loads a 64 x 16 K-contiguous slab (rows past lim clamped).
+__device__ __forceinline__ void small_load(const float* __restrict__ base, int ld, int mn0, int lim, int k0,
+                                           float* s) {
     const int lane = threadIdx.x & 63;
-    const int chunk = (lane & 7) ^ (lane >> 3);
 #pragma unroll
-    for (int b = 0; b < 8; ++b) {
-        const int row = min(mn0 + b * 8 + (lane >> 3), lim - 1);
+    for (int j = 0; j < 4; ++j) {
+        const int r = j * 16 + (lane >> 2);
+        const int row = min(mn0 + r, lim - 1);
+        const int chunk = (lane & 3) ^ ((r >> 2) & 3);
         const float* g = base + (size_t)row * ld + k0 + chunk * 4;
-        __builtin_amdgcn_global_load_lds((global_void*)g, (lds_void*)(s + b * kLdsBlock), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds((global_void*)g, (lds_void*)(s + j * 256), 16, 0, 0);
     }
 }
 
+// Values for k = k .. k+3 (k a multiple of 4 below 16) at row mn of a small-mode slab.
+__device__ __forceinline__ void small_fragment(const float* s, int mn, int k, float (&f)[4]) {
+    const f32x4 v = *reinterpret_cast<const f32x4*>(s + mn * kSmallSlab + (((k >> 2) ^ ((mn >> 2) & 3)) << 2));
+    f[0] = v[0]; f[1] = v[1]; f[2] = v[2]; f[3] = v[3];
+}
+
+// The MFMAs of one small-mode slab: lane l contributes k = 8 g + 4 (l / 32) + s
+// to step s of group g, for A and B alike (as in mma_slab).
+__device__ __forceinline__ void small_mma(const float* sa, const float* sb, int lane, f32x16 (&acc)[2][2]) {
+    const int r = lane & 31, h = lane >> 5;
+#pragma unroll
+    for (int g = 0; g < kSmallSlab / 8; ++g) {
+        float a[2][4], b[2][4];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            small_fragment(sa, i * 32 + r, g * 8 + h * 4, a[i]);
+            small_fragment(sb, i * 32 + r, g * 8 + h * 4, b[i]);
+        }
+#pragma unroll
+        for (int st = 0; st < 4; ++st)
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][st], b[j][st], acc[i][j], 0, 0, 0);
+    }
+}
+
+// Starts the loads of slab k0 of a small-mode block into stage s (A then B).
+__device__ __forceinline__ void small_issue(const GemmProblem& p, int row0, int col0, int k0, float* s) {
+    const SlabSrc src = slab_src(p, k0);
+    small_load(src.a, src.lda, row0, p.M, src.k, s);
+    small_load(src.b, src.ldb, col0, p.N, src.k, s + kSmallOperand);
+}
+
 // One small-mode block, computed by the calling wave alone in its own LDS
-// blocks sa, sb (8 blocks each): slabs are loaded, awaited and multiplied in
-// turn, with no workgroup barrier; the other waves of the CU hide the loads.
-// Then the epilogue of the block's quadrant, and the zeroing of the partial
-// sums of its tile's quadrants that no block computes.
-__device__ __forceinline__ void small_unit(const GemmProblem& p, const SmallUnit& su, float* sa, float* sb,
+// stages s0, s1 (2 x 64 x 16 floats each), with no workgroup barrier: slab
+// k + 1 loads while slab k is multiplied. Then the epilogue of the block's
+// quadrant, and the zeroing of the partial sums of its tile's quadrants that
+// no block computes.
+__device__ __forceinline__ void small_unit(const GemmProblem& p, const SmallUnit& su, float* s0, float* s1,
                                            float beta1, int lane) {
     f32x16 acc[2][2];
 #pragma unroll
@@ -633,13 +679,20 @@ __device__ __forceinline__ void small_unit(const GemmProblem& p, const SmallUnit
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
     const int row0 = su.bm * kSmallDim, col0 = su.bn * kSmallDim;
-    for (int k0 = 0; k0 < p.K; k0 += kSlab) {
-        const SlabSrc s = slab_src(p, k0);
-        load_slab_lds_wave(s.a, s.lda, row0, p.M, s.k, sa);
-        load_slab_lds_wave(s.b, s.ldb, col0, p.N, s.k, sb);
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's slab has landed
-        mma_slab<true, true>(sa, sb, 0, 0, lane, acc);
-        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // and has been read before it is refilled
+    const int nk = p.K / kSmallSlab;
+    small_issue(p, row0, col0, 0, s0);
+    for (int kt = 0; kt < nk; ++kt) {
+        float* cur = (kt & 1) ? s1 : s0;
+        float* nxt = (kt & 1) ? s0 : s1;
+        // The other stage's slab was read by the previous step's MFMAs; refill it.
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        if (kt + 1 < nk) {
+            small_issue(p, row0, col0, (kt + 1) * kSmallSlab, nxt);
+            asm volatile("s_waitcnt vmcnt(8)" ::: "memory");  // all but the 8 loads just issued: slab kt
+        } else {
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        }
+        small_mma(cur, cur + kSmallOperand, lane, acc);
     }
     const int quadrant = ((su.bm & 1) << 1) | (su.bn & 1);
     gemm_epilogue(p, su.bm >> 1, su.bn >> 1, su.slot, beta1, acc, lane, quadrant);
@@ -666,11 +719,12 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_grouped(const GemmProble
     const TileDesc td = tiles[blockIdx.x];
     if (td.part == kSmallGroup) {
         if constexpr (BK) {
-            const int w = threadIdx.x >> 6;
+            const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: its block is read with scalar loads
             if (w < td.tn) {
                 const SmallUnit su = small[td.tm + w];
+                // Wave w's two stages: half w % 2 of the A and B buffers of s0 or s1.
                 GemmStageLds& st = (w >> 1) ? s1 : s0;
-                const int half = (w & 1) * 8 * kLdsBlock;
+                const int half = (w & 1) * (kLdsOperand / 2);
                 small_unit(probs[su.prob], su, st.a + half, st.b + half, beta1, threadIdx.x & 63);
             }
         }
