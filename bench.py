@@ -127,7 +127,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="resnet50", choices=sorted(WORKLOAD_NAMES))
     ap.add_argument("--interval", type=int, default=1, help="preconditioner update interval k")
-    ap.add_argument("--form", default="auto", choices=("auto", "explicit", "factored"),
+    ap.add_argument("--form", default="auto", choices=("auto", "explicit", "factored", "squared"),
                     help="evaluation order of the factor updates")
     ap.add_argument("--split-k", type=int, default=1, choices=(0, 1),
                     help="split the K range of long tiles in levels with too few tiles")
@@ -225,7 +225,7 @@ def main():
         k_ms = timing[k][0] / max(1, timing[k][1])
         gbs = nbytes / (k_ms * 1e-3) / 1e9 if k_ms else 0.0
         hbm[k] = {"achieved": gbs, "frac": gbs / PEAK_HBM_GBS, "bytes_per_launch": nbytes}
-    forms = {"explicit": 0, "factored": 0}
+    forms = {"explicit": 0, "factored": 0, "squared": 0}
     for l in range(len(shapes)):
         for side in (0, 1):
             forms[opt.factor_form(l, side)] += 1

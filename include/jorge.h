@@ -57,10 +57,16 @@ typedef int32_t jorge_status;
  * FACTORED: through H: U = A^4 H, X = U H^T, X X = U (H^T U) H^T,
  *           A P = A - A^5 H (a I - b H^T U) H^T, ||X||_F^2 = <U^T U, H^T H>;
  *           about 12 d^2 k + 5 d k^2 flops, far less when k << d.
- * AUTO:     per factor, whichever order has less tile work. */
+ * SQUARED:  the factored order with A^2 formed once: A^2 H and A^4 H as
+ *           H^T A^2 and (H^T A^2) A^2, A^5 H from A^4 H; about
+ *           d^3 + 8 d^2 k + 5 d k^2 flops, less than either order above for k
+ *           between about d/4 and 2d/3. Needs symmetric factors (symmetrize = 1).
+ * AUTO:     per factor, whichever order has the least tile work (SQUARED only
+ *           with symmetrize = 1). */
 #define JORGE_FORM_AUTO     0
 #define JORGE_FORM_EXPLICIT 1
 #define JORGE_FORM_FACTORED 2
+#define JORGE_FORM_SQUARED  3
 
 /* State tensors of one layer (Algorithm 2 and Algorithm 3). */
 #define JORGE_STATE_L       0 /* L_hat, rows x rows, fp32 (symmetric unless symmetrize = 0) */
@@ -95,7 +101,8 @@ typedef struct jorge_hparams {
     int32_t graft;            /* 1: SGD grafting (Algorithm 3); 0: theta -= lr * m_t. Default 1. */
     int32_t symmetrize;       /* 1: each updated factor is replaced by (Z + Z^T)/2, Z being
                                  Algorithm 2's product; 0: Z itself. Default 1. */
-    int32_t factor_form;      /* JORGE_FORM_*: evaluation order of each factor update.
+    int32_t factor_form;      /* JORGE_FORM_*: evaluation order of each factor update
+                                 (JORGE_FORM_SQUARED needs symmetrize = 1).
                                  Default JORGE_FORM_AUTO. */
     int32_t split_k;          /* 1: a GEMM level splits some of its tiles along K where the
                                  library's cost model of the launch says it then finishes
@@ -237,7 +244,7 @@ jorge_status jorge_stage_flops(const jorge_ctx* ctx, double* flops, int32_t n);
 const char*  jorge_stage_name(int32_t stage);  /* NULL if out of range */
 
 /* The evaluation order chosen for one factor: side 0 = L_hat, 1 = R_hat;
- * *form receives JORGE_FORM_EXPLICIT or JORGE_FORM_FACTORED. */
+ * *form receives JORGE_FORM_EXPLICIT, JORGE_FORM_FACTORED or JORGE_FORM_SQUARED. */
 jorge_status jorge_factor_form(const jorge_ctx* ctx, int32_t layer, int32_t side, int32_t* form);
 
 /* Frees the context and all device memory it holds; NULL is ignored.

@@ -19,16 +19,23 @@
 //     P = I - U (aI - bS) H^T and A P = A - W H^T with W = A^5 H (aI - bS);
 //     nu^2 = ||U H^T||_F^2 = <U^T U, H^T H>; the symmetrized factor is
 //     s A - (s/2)(W H^T + H W^T). It costs about 12 d^2 k + 5 d k^2 flops
-//     against 8 d^3 + d^2 k, and is chosen per factor by the tile work of
-//     both orders (hp.factor_form can force either).
+//     against 8 d^3 + d^2 k.
+//   squared (symmetric factors): the factored order with A^2 formed once, so
+//     that A^2 H and A^4 H take one product each: about d^3 + 8 d^2 k + 5 d k^2
+//     flops, the cheapest of the three for k between about d/4 and 2d/3.
+// Each factor takes the order with the least tile work (hp.factor_form can
+// force one).
 //
 // Update step, as dependency levels (every GEMM of a level is one grouped
 // launch; "Yt_j" is (A^j H)^T, k x d):
 //   stage-in  Gp <- G, Gpt <- G^T, m_SGD <- beta1 m_SGD + G, partial sums of m_SGD^2
 //   gram      explicit: M = H H^T, A^2      factored: Q = H^T H, Yt_1 = H^T A^T
-//   pow4      explicit: A^4                 factored: Yt_2
+//                                           squared: Q, A^2 (and A H)
+//   pow4      explicit: A^4                 factored: Yt_2          squared: Yt_2 = H^T A^2
 //   xform     explicit: X, X^T, ||X||^2     factored: Yt_3, S = Yt_2 Yt_2^T
+//                                           squared: Yt_4 = Yt_2 A^2, S
 //   chain4                                  factored: Yt_4
+//                                           squared: A^5 H, <U^T U, Q>
 //   chain5                                  factored: A^5 H (stored d x k), <U^T U, Q>
 //   ffinal    nu = ||X||_F, beta, c, s per factor
 //   poly      explicit: P^T                 factored: W = a A^5 H - b A^5 H S
@@ -119,6 +126,7 @@ struct LayerHost {
 struct FactorHost {
     int layer, side, d, dp, k, kp;
     bool expl = true;
+    bool squared = false;  // (not explicit) the squared order: A^2 formed, the chain in steps of A^2
     bool chain = false;  // small: the whole update in one workgroup (lds_chain_kernel), explicit order
     // Low-rank preconditioning on update steps (factored, symmetric, d > 3k): the
     // layer's A_new H comes from the chain's A H, W, Q and H^T W (see add_factored).
@@ -127,6 +135,7 @@ struct FactorHost {
     size_t off_A, off_part, off_sc;
     size_t off_w[4];
     size_t off_s2 = 0;
+    size_t off_a2 = 0;     // the squared order's A^2 (dp x dp)
     int nparts = 0;
 };
 
@@ -604,8 +613,9 @@ jorge_status validate_hparams(const jorge_hparams* hp) {
         return JORGE_ERR_INVALID_ARGUMENT;
     if ((hp->graft != 0 && hp->graft != 1) || (hp->symmetrize != 0 && hp->symmetrize != 1))
         return JORGE_ERR_INVALID_ARGUMENT;
-    if (hp->factor_form < JORGE_FORM_AUTO || hp->factor_form > JORGE_FORM_FACTORED)
+    if (hp->factor_form < JORGE_FORM_AUTO || hp->factor_form > JORGE_FORM_SQUARED)
         return JORGE_ERR_INVALID_ARGUMENT;
+    if (hp->factor_form == JORGE_FORM_SQUARED && hp->symmetrize != 1) return JORGE_ERR_INVALID_ARGUMENT;
     if (hp->split_k != 0 && hp->split_k != 1) return JORGE_ERR_INVALID_ARGUMENT;
     if (hp->lds_chain_max < 0 || hp->lds_chain_max > kChainMax) return JORGE_ERR_INVALID_ARGUMENT;
     if (hp->precond_lowrank != 0 && hp->precond_lowrank != 1) return JORGE_ERR_INVALID_ARGUMENT;
@@ -619,18 +629,26 @@ int64_t tile_work(int64_t M, int64_t N, int64_t K, bool upper) {
     return (upper ? tm * (tm + 1) / 2 : tm * tn) * K;
 }
 
-// Whether a factor of padded size dp with statistic rank kp is cheaper in the
-// explicit order than in the factored one (same product list as build_tables).
-bool explicit_is_cheaper(int64_t dp, int64_t kp, bool sym, int order) {
+// The order with the least tile work for a factor of padded size dp with
+// statistic rank kp (same product lists as build_tables); ties go to the
+// explicit, then the factored order. lrp: the factor would precondition in
+// low rank if not explicit (the squared order then also forms A H).
+int choose_form(int64_t dp, int64_t kp, bool sym, int order, bool lrp) {
     int64_t e = tile_work(dp, dp, kp, true) + 2 * tile_work(dp, dp, dp, sym) + 3 * tile_work(dp, dp, dp, false);
     int64_t f = tile_work(kp, kp, dp, true) + 5 * tile_work(kp, dp, dp, false) + tile_work(kp, kp, dp, sym) +
                 tile_work(kp, kp, dp, true) + tile_work(dp, kp, kp, false) +
                 (sym ? tile_work(dp, dp, 2 * kp, true) : tile_work(dp, dp, kp, false));
+    // A^2, Q, three chain products, S, nu, W and the SYR2K (and A H)
+    int64_t q = tile_work(dp, dp, dp, true) + tile_work(kp, kp, dp, true) + 3 * tile_work(kp, dp, dp, false) +
+                2 * tile_work(kp, kp, dp, true) + tile_work(dp, kp, kp, false) + tile_work(dp, dp, 2 * kp, true) +
+                (lrp ? tile_work(kp, dp, dp, false) : 0);
     if (order == 3) {  // X V, and S S
         e += tile_work(dp, dp, dp, false);
         f += tile_work(kp, kp, kp, sym);
+        q += tile_work(kp, kp, kp, true);
     }
-    return e <= f;
+    if (sym && q < std::min(e, f)) return JORGE_FORM_SQUARED;
+    return e <= f ? JORGE_FORM_EXPLICIT : JORGE_FORM_FACTORED;
 }
 
 // Builds every offset; returns the arena size in bytes.
@@ -659,9 +677,15 @@ size_t plan(jorge_ctx* c) {
             F.k = side == 0 ? L.n : L.m;
             F.kp = side == 0 ? L.np : L.mp;
             F.chain = use_chain;
-            if (F.chain || c->hp.factor_form == JORGE_FORM_EXPLICIT) F.expl = true;
-            else if (c->hp.factor_form == JORGE_FORM_FACTORED) F.expl = false;
-            else F.expl = explicit_is_cheaper(F.dp, F.kp, sym, c->hp.series_order);
+            // A_new H (d x k) replaces a d x d product in the preconditioning when
+            // 6 k^2 d < 2 d^2 k, i.e. d > 3 k (both orders then cost 2 k^2 d more).
+            const bool lrp_ok = sym && c->hp.precond_lowrank && (int64_t)F.d > 3 * (int64_t)F.k;
+            const int form = F.chain ? JORGE_FORM_EXPLICIT
+                             : c->hp.factor_form != JORGE_FORM_AUTO
+                                 ? c->hp.factor_form
+                                 : choose_form(F.dp, F.kp, sym, c->hp.series_order, lrp_ok);
+            F.expl = form == JORGE_FORM_EXPLICIT;
+            F.squared = form == JORGE_FORM_SQUARED;
             const size_t dd = (size_t)F.dp * F.dp * sizeof(float);
             F.off_A = take(dd);
             if (F.chain) {
@@ -676,11 +700,10 @@ size_t plan(jorge_ctx* c) {
                 F.off_w[2] = take(kk);
                 F.off_w[3] = take(kk);
                 if (c->hp.series_order == 3) F.off_s2 = take(kk);
+                if (F.squared) F.off_a2 = take(dd);
                 F.nparts = tile_count(F.kp, F.kp);
             }
-            // A_new H (d x k) replaces a d x d product in the preconditioning when
-            // 6 k^2 d < 2 d^2 k, i.e. d > 3 k (both orders then cost 2 k^2 d more).
-            F.lrp = !F.expl && sym && c->hp.precond_lowrank && (int64_t)F.d > 3 * (int64_t)F.k;
+            F.lrp = !F.expl && lrp_ok;
             if (F.lrp) {
                 const size_t kd = (size_t)F.kp * F.dp * sizeof(float), kk = (size_t)F.kp * F.kp * sizeof(float);
                 F.off_y1 = take(kd);   // A H, d x k
@@ -788,39 +811,65 @@ int add_factored(jorge_ctx* c, const FactorHost& F, const FactorDev& fd, const f
         q.C = Q; q.ldc = kp; q.flags = EF_STORE; q.upper = 1;
         add_problem(c->nt[ST_GRAM], q, k * k * d);
     }
-    // Yt_{j+1} = Yt_j A^T, starting from Yt_0 = H^T: P0, P1, P0, P1.
-    const float* src = Ht;
-    float* dst[4] = {P0, P1, P0, P1};
-    const int lvl[4] = {ST_GRAM, ST_POW4, ST_XFORM, ST_CHAIN4};
-    for (int j = 0; j < 4; ++j) {
-        GemmProblem y = product(src, dp, A, dp, kp, dp, dp);
-        y.C = dst[j]; y.ldc = dp; y.flags = EF_STORE;
-        if (j == 0 && F.lrp) {  // keep A H (= Yt_1^T) for the preconditioning
-            y.C2 = at<float>(c, F.off_y1); y.ldc2 = kp; y.flags |= EF_STORE_T;
+    // Yt_4 = (A^4 H)^T is built in Yt4; A^5 H goes to Y5 (d x k) and W to Wb.
+    float* Yt4;
+    float* Y5;
+    float* Wb;
+    int last;  // level of A^5 H and nu
+    if (!F.squared) {
+        // Yt_{j+1} = Yt_j A^T, starting from Yt_0 = H^T: P0, P1, P0, P1.
+        const float* src = Ht;
+        float* dst[4] = {P0, P1, P0, P1};
+        const int lvl[4] = {ST_GRAM, ST_POW4, ST_XFORM, ST_CHAIN4};
+        for (int j = 0; j < 4; ++j) {
+            GemmProblem y = product(src, dp, A, dp, kp, dp, dp);
+            y.C = dst[j]; y.ldc = dp; y.flags = EF_STORE;
+            if (j == 0 && F.lrp) {  // keep A H (= Yt_1^T) for the preconditioning
+                y.C2 = at<float>(c, F.off_y1); y.ldc2 = kp; y.flags |= EF_STORE_T;
+            }
+            add_problem(c->nt[lvl[j]], y, 2 * k * d * d);
+            src = dst[j];
         }
-        add_problem(c->nt[lvl[j]], y, 2 * k * d * d);
-        src = dst[j];
+        Yt4 = P1; Y5 = P0; Wb = P1; last = ST_CHAIN5;
+    } else {
+        // Squared order: A^2 (symmetric), Yt_2 = H^T A^2 into P1, Yt_4 = Yt_2 A^2 into P0.
+        float* A2 = at<float>(c, F.off_a2);
+        GemmProblem a2 = product(A, dp, A, dp, dp, dp, dp);
+        a2.C = A2; a2.ldc = dp; a2.flags = EF_STORE; a2.upper = 1;
+        add_problem(c->nt[ST_GRAM], a2, d * d * d);
+        if (F.lrp) {  // A H for the preconditioning, stored d x k
+            GemmProblem y1 = product(Ht, dp, A, dp, kp, dp, dp);
+            y1.C2 = at<float>(c, F.off_y1); y1.ldc2 = kp; y1.flags = EF_STORE_T;
+            add_problem(c->nt[ST_GRAM], y1, 2 * k * d * d);
+        }
+        GemmProblem y2 = product(Ht, dp, A2, dp, kp, dp, dp);
+        y2.C = P1; y2.ldc = dp; y2.flags = EF_STORE;
+        add_problem(c->nt[ST_POW4], y2, 2 * k * d * d);
+        GemmProblem y4 = product(P1, dp, A2, dp, kp, dp, dp);
+        y4.C = P0; y4.ldc = dp; y4.flags = EF_STORE;
+        add_problem(c->nt[ST_XFORM], y4, 2 * k * d * d);
+        Yt4 = P0; Y5 = P1; Wb = P0; last = ST_CHAIN4;
     }
-    // S = H^T A^4 H: Yt_2 Yt_2^T for symmetric factors (read from P1 while Yt_3 goes to P0).
+    // S = H^T A^4 H: Yt_2 Yt_2^T for symmetric factors (Yt_2 is in P1 at the xform level).
     if (sym) {
         GemmProblem s = product(P1, dp, P1, dp, kp, kp, dp);
         s.C = S; s.ldc = kp; s.flags = EF_STORE; s.upper = 1;
         add_problem(c->nt[ST_XFORM], s, k * k * d);
     }
-    // A^5 H = (Yt_4 A^T)^T, stored d x k in P0; ||X||^2 = <Yt_4 Yt_4^T, Q>.
-    GemmProblem y5 = product(P1, dp, A, dp, kp, dp, dp);
-    y5.C2 = P0; y5.ldc2 = kp; y5.flags = EF_STORE_T;
-    add_problem(c->nt[ST_CHAIN5], y5, 2 * k * d * d);
-    GemmProblem nu = product(P1, dp, P1, dp, kp, kp, dp);
+    // A^5 H = (Yt_4 A^T)^T, stored d x k; ||X||^2 = <Yt_4 Yt_4^T, Q>.
+    GemmProblem y5 = product(Yt4, dp, A, dp, kp, dp, dp);
+    y5.C2 = Y5; y5.ldc2 = kp; y5.flags = EF_STORE_T;
+    add_problem(c->nt[last], y5, 2 * k * d * d);
+    GemmProblem nu = product(Yt4, dp, Yt4, dp, kp, kp, dp);
     nu.X = Q; nu.ldx = kp; nu.flags = EF_DOT; nu.upper = 1; nu.partials = fd.partials;
-    const int slots = add_problem(c->nt[ST_CHAIN5], nu, k * k * d);
-    // Literal mode: S^T = U^T H = Yt_4 H (general).
+    const int slots = add_problem(c->nt[last], nu, k * k * d);
+    // Literal mode (factored order only): S^T = U^T H = Yt_4 H (general).
     if (!sym) {
-        GemmProblem s = product(P1, dp, Ht, dp, kp, kp, dp);
+        GemmProblem s = product(Yt4, dp, Ht, dp, kp, kp, dp);
         s.C = S; s.ldc = kp; s.flags = EF_STORE;
         add_problem(c->nt[ST_CHAIN5], s, 2 * k * k * d);
     }
-    // W = a A^5 H - b A^5 H S (B = S^T row-major), into P1. With the cubic
+    // W = a A^5 H - b A^5 H S (B = S^T row-major), into Wb. With the cubic
     // term, W = a A^5 H - A^5 H V with V = b S - e S S (X^r = U S^(r-1) H^T),
     // one level later: V^T = b S^T - e S^T S^T (S^T symmetric, or the literal
     // mode's S^T as an MN-major B), then W.
@@ -834,8 +883,8 @@ int add_factored(jorge_ctx* c, const FactorHost& F, const FactorDev& fd, const f
         add_problem(sym ? c->nt[ST_POLY] : c->nn[ST_POLY], v, (sym ? 1 : 2) * k * k * k);
         wb = V;
     }
-    GemmProblem w = product(P0, kp, wb, kp, dp, kp, kp);
-    w.C = P1; w.ldc = kp; w.X = P0; w.ldx = kp; w.sc = fd.sc;
+    GemmProblem w = product(Y5, kp, wb, kp, dp, kp, kp);
+    w.C = Wb; w.ldc = kp; w.X = Y5; w.ldx = kp; w.sc = fd.sc;
     w.flags = EF_STORE | EF_READX; w.coef = cubic ? CO_WMIX3 : CO_WMIX;
     if (F.lrp) {  // and W^T for H^T W
         w.C2 = at<float>(c, F.off_wt); w.ldc2 = dp; w.flags |= EF_STORE_T;
@@ -848,7 +897,7 @@ int add_factored(jorge_ctx* c, const FactorHost& F, const FactorDev& fd, const f
         add_problem(c->nt[ST_UPDATE], v, 2 * k * k * d);
         // A_new H = s A H - (s/2)(W H^T H + H W^T H), in the first preconditioning level:
         // K segments [W | H] x [Q | (H^T W)^T]^T (Q is symmetric), coefficients of the SYR2K.
-        GemmProblem x = product(P1, kp, Q, kp, dp, kp, kp);
+        GemmProblem x = product(Wb, kp, Q, kp, dp, kp, kp);
         x.A2 = Hr; x.lda2 = kp; x.B2 = at<float>(c, F.off_v2t); x.ldb2 = kp; x.K = 2 * kp;
         x.C = at<float>(c, F.off_xa); x.ldc = kp;
         x.X = at<float>(c, F.off_y1); x.ldx = kp; x.sc = fd.sc;
@@ -856,10 +905,10 @@ int add_factored(jorge_ctx* c, const FactorHost& F, const FactorDev& fd, const f
         add_problem(c->nt[ST_UPRECOND_L], x, 2 * d * k * 2 * k);
     }
     // A <- s A - (s/2)(W H^T + H W^T) (symmetric, in place) or s A - s W H^T.
-    GemmProblem u = product(P1, kp, Hr, kp, dp, dp, kp);
+    GemmProblem u = product(Wb, kp, Hr, kp, dp, dp, kp);
     u.C = A; u.ldc = dp; u.X = A; u.ldx = dp; u.sc = fd.sc; u.flags = EF_STORE | EF_READX;
     if (sym) {
-        u.A2 = Hr; u.lda2 = kp; u.B2 = P1; u.ldb2 = kp;
+        u.A2 = Hr; u.lda2 = kp; u.B2 = Wb; u.ldb2 = kp;
         u.K = 2 * kp;
         u.coef = CO_SYR2K;
         u.upper = 1;
@@ -1641,7 +1690,8 @@ jorge_status jorge_factor_form(const jorge_ctx* c, int32_t layer, int32_t side, 
     if (!c || !form || layer < 0 || layer >= (int32_t)c->layers.size() || (side != 0 && side != 1))
         return JORGE_ERR_INVALID_ARGUMENT;
     const auto& L = c->layers[layer];
-    *form = c->factors[side == 0 ? L.fL : L.fR].expl ? JORGE_FORM_EXPLICIT : JORGE_FORM_FACTORED;
+    const FactorHost& F = c->factors[side == 0 ? L.fL : L.fR];
+    *form = F.expl ? JORGE_FORM_EXPLICIT : F.squared ? JORGE_FORM_SQUARED : JORGE_FORM_FACTORED;
     return JORGE_OK;
 }
 

@@ -16,7 +16,7 @@ LIB_PATH = os.path.join(PKG, "libjorge.so")
 JORGE_OK = 0
 BETA_MODES = {"fixed": 0, "dynamic": 1, "clamped": 2}
 STATE_KINDS = {"L": 0, "R": 1, "mom": 2, "mom_sgd": 3}
-FACTOR_FORMS = {"auto": 0, "explicit": 1, "factored": 2}
+FACTOR_FORMS = {"auto": 0, "explicit": 1, "factored": 2, "squared": 3}
 DIAG_NAMES = ("nu_L", "nu_R", "beta_L", "beta_R", "norm_m", "norm_sgd", "g")
 
 
@@ -256,10 +256,10 @@ class Jorge:
         return v.value
 
     def factor_form(self, layer, side):
-        """'explicit' or 'factored': the evaluation order of L_hat (side 0) or R_hat (side 1)."""
+        """'explicit', 'factored' or 'squared': the evaluation order of L_hat (side 0) or R_hat (side 1)."""
         v = ctypes.c_int32()
         _check(self.lib, self.lib.jorge_factor_form(self.ctx, int(layer), int(side), ctypes.byref(v)), self.ctx)
-        return {1: "explicit", 2: "factored"}[v.value]
+        return {1: "explicit", 2: "factored", 3: "squared"}[v.value]
 
     # -------------------------------------------------------------- timing
     def set_timing(self, enable: bool):

@@ -21,12 +21,15 @@ pytestmark = pytest.mark.gpu
 STEP_TOL = 1e-5
 TRAJ_TOL = 1e-3
 # Evaluation orders of the factor update: the paper's explicit powers, the
-# factored order through the statistic's factor H (both through the grouped
-# levels only), and the default per-factor choice, where a context whose
-# factors all have padded size <= 64 runs them in the one-workgroup LDS chain.
-FORMS = ("explicit", "factored", "auto")
+# factored order through the statistic's factor H, the squared order (A^2
+# formed, the chain through H in steps of A^2; symmetric factors only), all
+# through the grouped levels, and the default per-factor choice, where a
+# context whose factors all have padded size <= 64 runs them in the
+# one-workgroup LDS chain.
+FORMS = ("explicit", "factored", "squared", "auto")
 FORM_KW = {"explicit": dict(factor_form="explicit", lds_chain_max=0),
            "factored": dict(factor_form="factored", lds_chain_max=0),
+           "squared": dict(factor_form="squared", lds_chain_max=0),
            "auto": dict(factor_form="auto")}
 HP = dict(lr=0.1, beta2=0.9, beta1=0.9, weight_decay=5e-5)
 KINDS = ("L", "R", "mom", "mom_sgd")
@@ -154,6 +157,10 @@ def test_beta_modes(mode, sigma, beta2, form):
 @pytest.mark.parametrize("form", FORMS)
 def test_literal_mode_without_symmetrization(form):
     say("literal mode", form)
+    if form == "squared":  # needs symmetric factors: rejected before any GPU work
+        with pytest.raises(JorgeError):
+            Jorge([(48, 96)], symmetrize=False, factor_form="squared")
+        return
     run_pair([(48, 96), (160, 40), (300, 130)], 6, 1e-2, check_every=3,
              gpu_kw=dict(FORM_KW[form], symmetrize=False), orc_kw=dict(symmetrize=False))
 
@@ -277,11 +284,16 @@ def test_full_size_512x4608_first_step():
 
 
 def test_auto_form_choice():
-    """The cheaper order by tile work: factored when the statistic's rank k is well below d."""
-    opt = Jorge([(64, 576), (512, 512), (256, 2304), (2048, 512), (64, 64)])
-    forms = [(opt.factor_form(l, 0), opt.factor_form(l, 1)) for l in range(5)]
+    """The cheapest order by tile work: factored when the statistic's rank k is well below d,
+    squared for k about d/2, explicit from about 2d/3 up."""
+    opt = Jorge([(64, 576), (512, 512), (256, 2304), (2048, 512), (64, 64), (1024, 512), (2048, 1024)])
+    forms = [(opt.factor_form(l, 0), opt.factor_form(l, 1)) for l in range(7)]
     assert forms == [("explicit", "factored"), ("explicit", "explicit"), ("explicit", "factored"),
-                     ("factored", "explicit"), ("explicit", "explicit")], forms
+                     ("factored", "explicit"), ("explicit", "explicit"), ("squared", "explicit"),
+                     ("squared", "explicit")], forms
+    # The literal mode has no squared order.
+    lit = Jorge([(1024, 512)], symmetrize=False)
+    assert lit.factor_form(0, 0) == "factored"
 
 
 def test_diagnostics_match_oracle():
@@ -313,26 +325,26 @@ def test_invalid_step_arguments():
 
 
 def test_stage_timing_reports_every_update_stage():
-    opt = Jorge([(256, 512)])
-    p = [torch.zeros((256, 512), device="cuda")]
-    g = [to_dev(gradient(0, 0, 1, (256, 512), 1e-2))]
+    opt = Jorge([(256, 1024)])
+    p = [torch.zeros((256, 1024), device="cuda")]
+    g = [to_dev(gradient(0, 0, 1, (256, 1024), 1e-2))]
     opt.set_timing(True)
     opt.step(p, g, 0.1)
     tm = opt.read_timing()
-    # L_hat (256) is explicit and R_hat (512, rank 256) factored, so every update stage runs once.
+    # L_hat (256) is explicit and R_hat (1024, rank 256) factored, so every update stage runs once.
     assert (opt.factor_form(0, 0), opt.factor_form(0, 1)) == ("explicit", "factored")
     for name in ("stage_in", "gram", "pow4", "xform", "chain4", "chain5", "factor_finalize", "poly",
                  "update", "symmetrize", "uprecond_L", "uprecond_R", "layer_finalize", "weight"):
         assert tm[name][1] == 1 and tm[name][0] > 0, name
     assert tm["precond_L"][1] == 0      # the non-update steps' preconditioning
     fl = opt.stage_flops()
-    m, n = 256, 512
+    m, n = 256, 1024
     assert fl["precond_L"] == 2 * m * m * n and fl["precond_R"] == 2 * m * n * n
     assert fl["stage_in"] == 0 and fl["weight"] == 0
     # The literal mode launches the powers of non-symmetric factors apart (MN-major B).
     lit = Jorge([(256, 512)], symmetrize=False)
     lit.set_timing(True)
-    lit.step([torch.zeros((256, 512), device="cuda")], g, 0.1)
+    lit.step([torch.zeros((256, 512), device="cuda")], [to_dev(gradient(0, 0, 1, (256, 512), 1e-2))], 0.1)
     assert lit.read_timing()["gram"][1] == 2 and lit.read_timing()["pow4"][1] == 2
     opt.reset_timing()
     assert all(v == (0.0, 0) for v in opt.read_timing().values())
@@ -474,6 +486,8 @@ CUBIC_SHAPES = [(64, 576), (48, 96), (300, 130), (256, 1152), (512, 128), (128, 
 @pytest.mark.parametrize("form", FORMS)
 def test_cubic_series_term(form, symmetrize):
     say("cubic series term", form, "symmetrize", symmetrize)
+    if form == "squared" and not symmetrize:
+        pytest.skip("the squared order needs symmetric factors (rejection: test_literal_mode_without_symmetrization)")
     kw = dict(series_order=3, symmetrize=symmetrize)
     opt, orc, pg, po, worst = run_pair(CUBIC_SHAPES, 6, 1e-2, check_every=2,
                                        gpu_kw=dict(FORM_KW[form], **kw), orc_kw=kw)
@@ -507,7 +521,7 @@ def test_cubic_series_first_step(shapes, form):
 
 
 def test_cubic_series_launches_and_flops():
-    shapes = [(256, 512)]     # L_hat explicit, R_hat factored
+    shapes = [(256, 512)]     # L_hat explicit; R_hat (rank 256) squared, with the factored order's poly products
     g = [to_dev(gradient(0, 0, 1, shapes[0], 1e-2))]
     runs = {}
     for order in (2, 3):
@@ -517,7 +531,7 @@ def test_cubic_series_launches_and_flops():
         runs[order] = (opt.read_timing(), opt.stage_flops())
     assert runs[2][0]["poly2"][1] == 0 and runs[3][0]["poly2"][1] == 1
     m, n = shapes[0]
-    # Explicit L_hat: X V (2 m^3) one level after V; factored R_hat (k = m): S S (m^3, symmetric).
+    # Explicit L_hat: X V (2 m^3) one level after V; R_hat (k = m): S S (m^3, symmetric).
     f2, f3 = runs[2][1], runs[3][1]
     assert f3["poly2"] == 2 * m ** 3 + 2 * n * m * m
     assert f3["poly"] == 2 * m ** 3 + m ** 3
