@@ -47,7 +47,12 @@ def stage_bytes(shapes):
             "stage_in": 20 * mn}     # read G, write Gp and its transpose, read and write m_SGD
 
 
-PROFILE = os.path.join(ROOT, "profiles", "gemm_grouped_resnet50.md")
+# Committed rocprofv3 summaries that carry HBM counter figures for a workload.
+PROFILES = {"resnet50": os.path.join(ROOT, "profiles", "gemm_grouped_resnet50.md")}
+
+
+def profile_path(config):
+    return PROFILES.get(config, os.path.join(ROOT, "profiles", f"jorge_step_{config}.md"))
 
 
 def kernel_sources_sha256():
@@ -62,15 +67,16 @@ def kernel_sources_sha256():
 
 
 def measured_traffic(config):
-    """HBM bytes per gemm_grouped launch from the committed counter summary, or None.
+    """HBM bytes per gemm_grouped launch from the workload's committed counter summary, or None.
 
     The figure applies only to the workload it was taken on, and only while the
     kernel sources are the ones it was taken with.
     """
-    if config != "resnet50" or not os.path.exists(PROFILE):
+    path = profile_path(config)
+    if not os.path.exists(path):
         return None
     vals = {}
-    with open(PROFILE) as fh:
+    with open(path) as fh:
         for line in fh:
             if ":" in line and line.split(":")[0] in ("traffic_bytes_per_launch", "kernel_sources_sha256"):
                 k, v = line.split(":", 1)
@@ -219,6 +225,9 @@ def main():
     g_ms = sum(timing[k][0] for k in GEMM_STAGES) + timing[FIXUP_STAGE][0]
     g_launches = sum(timing[k][1] for k in GEMM_STAGES)
     achieved = g_flops / (g_ms * 1e-3) / 1e12
+    traffic = measured_traffic(args.config)
+    ms_launch = g_ms / max(1, g_launches)
+    traffic_gbs = traffic / (ms_launch * 1e-3) / 1e9 if traffic and ms_launch else None
     f_paper = sum(falg_paper(m, n) for m, n in shapes) * updates_clean / steps
     hbm = {}  # the bandwidth-bound kernels: algorithmic bytes / average launch time
     for k, nbytes in stage_bytes(shapes).items():
@@ -249,8 +258,11 @@ def main():
                    "series_order": args.series_order, "seed": args.seed},
         "roofline": {"bound": "mfma", "kernel": "gemm_grouped<true, true> (every GEMM stage of the step)",
                      "achieved": achieved, "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / PEAK_FP32_MFMA_TFLOPS, "traffic": measured_traffic(args.config), "traffic_unit": "HBM bytes per launch",
-                     "launches": g_launches, "ms_per_launch": g_ms / max(1, g_launches),
+                     "frac": achieved / PEAK_FP32_MFMA_TFLOPS, "traffic": traffic, "traffic_unit": "HBM bytes per launch",
+                     # the measured traffic over the launch time: how far the kernel is from the HBM roof
+                     "traffic_gbs": traffic_gbs,
+                     "traffic_hbm_frac": traffic_gbs / PEAK_HBM_GBS if traffic_gbs else None,
+                     "launches": g_launches, "ms_per_launch": ms_launch,
                      "gflop_per_launch": g_flops / max(1, g_launches) / 1e9},
         # executed algorithmic flops of the whole step / (step time x fp32 MFMA peak)
         "mfma_util_pct": 100.0 * g_flops / steps / (inst_ms / steps * 1e-3) / (PEAK_FP32_MFMA_TFLOPS * 1e12),
