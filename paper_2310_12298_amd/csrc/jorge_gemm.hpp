@@ -59,22 +59,40 @@ __device__ __forceinline__ f32x4 gload4(const float* p) {
 typedef __attribute__((address_space(1))) void global_void;
 typedef __attribute__((address_space(3))) void lds_void;
 
-// Global -> LDS directly: one 128 x 32 K-contiguous operand slab. Wave w
-// fills blocks 4w .. 4w+3 with one 16-byte load per lane each. Rows past
-// the extent `lim` are clamped to the last valid one: they only feed outputs
-// that the epilogue discards. The loads complete asynchronously (vmcnt).
-__device__ __forceinline__ void load_slab_lds(const float* __restrict__ base, int ld, int mn0, int lim,
-                                              int k0, float* s) {
+// Byte offsets, from the operand's base at k = 0, of the four 16-byte chunks
+// this lane loads for each 128 x 32 K-contiguous operand slab of a tile. Wave
+// w fills LDS blocks 4w .. 4w+3 with one 16-byte load per lane each. Rows
+// past the extent `lim` are clamped to the last valid one: they only feed
+// outputs that the epilogue discards. The offsets do not change along K, so
+// they are computed once per tile.
+struct SlabLanes {
+    unsigned o[4];
+};
+
+__device__ __forceinline__ void slab_lanes(int ld, int mn0, int lim, SlabLanes& L) {
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int chunk = (lane & 7) ^ (lane >> 3);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-        const int b = wave * 4 + j;
-        const int row = min(mn0 + b * 8 + (lane >> 3), lim - 1);
-        const float* g = base + (size_t)row * ld + k0 + chunk * 4;
-        __builtin_amdgcn_global_load_lds((global_void*)g, (lds_void*)(s + b * kLdsBlock), 16, 0, 0);
+        const int row = min(mn0 + (wave * 4 + j) * 8 + (lane >> 3), lim - 1);
+        L.o[j] = (unsigned)row * (unsigned)ld * 4u + (unsigned)chunk * 16u;
     }
+}
+
+typedef __attribute__((address_space(1))) const char gcchar;
+
+// Global -> LDS directly: the slab at k0 of an operand whose lane offsets
+// are L. The uniform part of the address (base + k0) stays in scalar
+// registers, so each load is one instruction with no address arithmetic.
+// The loads complete asynchronously (vmcnt).
+__device__ __forceinline__ void load_slab_lds(const float* __restrict__ base, const SlabLanes& L, int k0, float* s) {
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const gcchar* g = (const gcchar*)(base + k0);
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+        __builtin_amdgcn_global_load_lds((global_void*)(g + L.o[j]), (lds_void*)(s + (wave * 4 + j) * kLdsBlock), 16,
+                                         0, 0);
 }
 
 // Global -> registers: one 32 x 128 MN-contiguous operand slab, four 16-byte
@@ -119,9 +137,9 @@ __device__ __forceinline__ void fragment(const float* s, int mn, int k, float (&
 // from LDS while the MFMAs of the current group run: the scheduling groups
 // at the end place each of those four reads after one of the group's first
 // MFMAs, so their latency hides behind the remaining twelve.
-template <bool AK, bool BK>
+template <bool AK, bool BK, class Issue>
 __device__ __forceinline__ void mma_slab(const float* sa, const float* sb, int wy, int wx, int lane,
-                                         f32x16 (&acc)[2][2]) {
+                                         f32x16 (&acc)[2][2], Issue&& issue) {
     const int r = lane & 31, h = lane >> 5;
     float a[2][2][4], b[2][2][4];
 #pragma unroll
@@ -129,6 +147,9 @@ __device__ __forceinline__ void mma_slab(const float* sa, const float* sb, int w
         fragment<AK>(sa, wy * 64 + i * 32 + r, h * 4, a[0][i]);
         fragment<BK>(sb, wx * 64 + i * 32 + r, h * 4, b[0][i]);
     }
+    // The loads of a later slab into the other stage start while the first
+    // fragments of this one are read.
+    issue();
 #pragma unroll
     for (int k8 = 0; k8 < kSlab / 8; ++k8) {
         const int cur = k8 & 1;
@@ -149,8 +170,9 @@ __device__ __forceinline__ void mma_slab(const float* sa, const float* sb, int w
                                                                      0, 0, 0);
     }
     if constexpr (AK && BK) {
-        constexpr int kMfma = 0x008, kDsRead = 0x100;
+        constexpr int kMfma = 0x008, kDsRead = 0x100, kVmemRead = 0x020;
         __builtin_amdgcn_sched_group_barrier(kDsRead, 4, 0);      // group 0's fragments
+        __builtin_amdgcn_sched_group_barrier(kVmemRead, 8, 0);    // the other stage's slab
 #pragma unroll
         for (int k8 = 0; k8 + 1 < kSlab / 8; ++k8) {
 #pragma unroll
@@ -202,16 +224,30 @@ struct GemmStageLds {
     float b[kLdsOperand];
 };
 
+// Lane offsets of a tile's operand slabs for both K segments.
+struct TileLanes {
+    SlabLanes a, b, a2, b2;
+};
+
 // Starts the copy of slab k0 (absolute K) of tile (row0, col0) into stage st.
 // K-contiguous operands load to LDS directly; the MN-contiguous B is held in rb
 // until store_b (after the MFMAs of the other stage).
 template <bool BK>
-__device__ __forceinline__ void issue_slab(const GemmProblem& p, int row0, int col0, int k0, GemmStageLds& st,
-                                           f32x4 (&rb)[4]) {
-    const SlabSrc s = slab_src(p, k0);
-    load_slab_lds(s.a, s.lda, row0, p.M, s.k, st.a);
-    if constexpr (BK) load_slab_lds(s.b, s.ldb, col0, p.N, s.k, st.b);
-    else load_slab_mn(s.b, s.ldb, col0, p.N, s.k, rb);
+__device__ __forceinline__ void issue_slab(const GemmProblem& p, const TileLanes& tl, int col0, int k0,
+                                           GemmStageLds& st, f32x4 (&rb)[4]) {
+    // Segment selection by selects, not branches, so the loads stay in the
+    // scheduling region of the MFMAs they are interleaved with.
+    const bool two = k0 >= p.K1;
+    const int k = two ? k0 - p.K1 : k0;
+    SlabLanes la, lb;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        la.o[j] = two ? tl.a2.o[j] : tl.a.o[j];
+        if constexpr (BK) lb.o[j] = two ? tl.b2.o[j] : tl.b.o[j];
+    }
+    load_slab_lds(two ? p.A2 : p.A, la, k, st.a);
+    if constexpr (BK) load_slab_lds(two ? p.B2 : p.B, lb, k, st.b);
+    else load_slab_mn(two ? p.B2 : p.B, two ? p.ldb2 : p.ldb, col0, p.N, k, rb);
 }
 
 template <bool BK>
@@ -241,30 +277,40 @@ __device__ __forceinline__ void gemm_mainloop(const GemmProblem& p, int tm, int 
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
 
+    TileLanes tl;
+    slab_lanes(p.lda, row0, p.M, tl.a);
+    slab_lanes(p.lda2, row0, p.M, tl.a2);
+    if constexpr (BK) {
+        slab_lanes(p.ldb, col0, p.N, tl.b);
+        slab_lanes(p.ldb2, col0, p.N, tl.b2);
+    }
     f32x4 rb[4];
     const int nk = (k1 - k0) / kSlab;
-    issue_slab<BK>(p, row0, col0, k0, s0, rb);
+    issue_slab<BK>(p, tl, col0, k0, s0, rb);
     finish_slab<BK>(s0, rb);
     // Pairs of slabs: slab kt is in s0, kt+1 goes to s1 and kt+2 back to s0.
     // The loop has no other exit, so the accumulators stay in place.
     int kt = 0;
     for (; kt + 2 <= nk; kt += 2) {
-        issue_slab<BK>(p, row0, col0, k0 + (kt + 1) * kSlab, s1, rb);
         // Raised issue priority while this wave runs its MFMAs: the two waves
         // sharing a SIMD then alternate between MFMA and memory phases.
         __builtin_amdgcn_s_setprio(1);
-        mma_slab<AK, BK>(s0.a, s0.b, wy, wx, lane, acc);
+        mma_slab<AK, BK>(s0.a, s0.b, wy, wx, lane, acc,
+                         [&] { issue_slab<BK>(p, tl, col0, k0 + (kt + 1) * kSlab, s1, rb); });
         __builtin_amdgcn_s_setprio(0);
         finish_slab<BK>(s1, rb);
-        if (kt + 2 < nk) issue_slab<BK>(p, row0, col0, k0 + (kt + 2) * kSlab, s0, rb);
+        // Past the last slab the load repeats slab nk - 1 into the idle stage
+        // (never read), which keeps the loop free of branches.
+        const int kn = min(kt + 2, nk - 1);
         __builtin_amdgcn_s_setprio(1);
-        mma_slab<AK, BK>(s1.a, s1.b, wy, wx, lane, acc);
+        mma_slab<AK, BK>(s1.a, s1.b, wy, wx, lane, acc,
+                         [&] { issue_slab<BK>(p, tl, col0, k0 + kn * kSlab, s0, rb); });
         __builtin_amdgcn_s_setprio(0);
         finish_slab<BK>(s0, rb);
     }
     if (kt < nk) {  // odd slab count: the last slab is in s0
         __builtin_amdgcn_s_setprio(1);
-        mma_slab<AK, BK>(s0.a, s0.b, wy, wx, lane, acc);
+        mma_slab<AK, BK>(s0.a, s0.b, wy, wx, lane, acc, [] {});
         __builtin_amdgcn_s_setprio(0);
     }
     __syncthreads();  // every wave is done with both stages
