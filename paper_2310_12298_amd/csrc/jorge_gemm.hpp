@@ -5,19 +5,21 @@
 // carries its own epilogue (flags and coefficient set, decided at run time
 // per problem), so products with different epilogues share a launch. A
 // workgroup of 256 threads computes one 128 x 128 tile of C = A * B; its
-// four waves each own a 64 x 64 sub-tile held
-// as 2 x 2 blocks of v_mfma_f32_32x32x2_f32 accumulators. K is consumed in
+// four waves each own a 64 x 64 sub-tile held as 4 x 4 blocks of
+// v_mfma_f32_16x16x4_f32 accumulators (this form moves half as many
+// accumulator registers per flop as the 32 x 32 one, which keeps the clock
+// higher under the chip's power limit). K is consumed in
 // slabs of 32 staged through double-buffered LDS (one barrier per slab): while
 // the waves run the MFMAs of slab k, slab k+1 streams into the other buffer.
 // K-contiguous operands go straight from global memory to LDS
 // (global_load_lds_dwordx4, no register staging); an MN-contiguous operand
 // (the NN kernel's B) is held in registers and written to LDS after the MFMAs.
 //
-// Within a slab, lane l of a wave contributes k = 8*k8 + 4*(l/32) + s to the
-// MFMA of step s (s = 0..3): the half-waves take disjoint halves of each
-// 8-wide k group, so a K-contiguous operand is read from LDS as one 16-byte
-// load per lane per 8 k values. The same k map is used for A and B, so every
-// product A[i][k] * B[k][j] is formed exactly once.
+// Within a slab, lane l of a wave contributes k = 16*kg + 4*(l/16) + s to the
+// MFMA of step s (s = 0..3) of 16-wide k group kg: the four lane groups take
+// disjoint quarters of each group, so a K-contiguous operand is read from LDS
+// as one 16-byte load per lane per 16 k values. The same k map is used for A
+// and B, so every product A[i][k] * B[k][j] is formed exactly once.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -28,6 +30,15 @@ namespace jorge {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+// Accumulator layout. A wave's 64 x 64 quadrant (wy, wx) of its tile is a
+// 4 x 4 grid of 16 x 16 blocks; block b = 4 i + j (rows 16 i, columns 16 j of
+// the quadrant) is one v_mfma_f32_16x16x4_f32 accumulator, in which lane l
+// holds column l % 16, rows 4 (l / 16) .. 4 (l / 16) + 3. Each lane thus
+// holds, for each of its 16 blocks, four consecutive rows of one column.
+// Row and column of the first of those four values, relative to the tile:
+__device__ __forceinline__ int acc_row(int b, int lane, int wy) { return wy * 64 + (b >> 2) * 16 + (lane >> 4) * 4; }
+__device__ __forceinline__ int acc_col(int b, int lane, int wx) { return wx * 64 + (b & 3) * 16 + (lane & 15); }
 
 constexpr int kTile = 128;                    // tile rows = tile columns
 constexpr int kSlab = 32;                     // K per LDS stage
@@ -41,7 +52,9 @@ constexpr int kGemmThreads = 256;
 // 8 distinct 16-byte bank groups, and the 128-byte pad between blocks moves
 // the next 8 rows to the other half of a 64-bank LDS.
 constexpr int kLdsBlock = 8 * 32 + 32;        // floats per 8-row block, with its pad
-constexpr int kLdsMN = kTile + 8;             // row stride of an M/N-contiguous operand in LDS
+// Row stride of an M/N-contiguous operand in LDS: 132 floats puts the four
+// k rows that one fragment read touches (4 apart) on distinct bank quarters.
+constexpr int kLdsMN = kTile + 4;
 constexpr int kLdsOperand = 16 * kLdsBlock;   // floats per operand per stage (>= kSlab * kLdsMN)
 static_assert(kLdsOperand >= kSlab * kLdsMN, "LDS operand buffer too small");
 static_assert(kLdsOperand / 2 >= 2 * 64 * 16, "a small-mode stage (two 64 x 16 slabs) must fit in half an operand buffer");
@@ -133,56 +146,56 @@ __device__ __forceinline__ void fragment(const float* s, int mn, int k, float (&
     }
 }
 
-// The MFMAs of one LDS slab. Fragments of the next 8-wide k group are read
+// The MFMAs of one LDS slab. Fragments of the next 16-wide k group are read
 // from LDS while the MFMAs of the current group run: the scheduling groups
-// at the end place each of those four reads after one of the group's first
-// MFMAs, so their latency hides behind the remaining twelve.
+// at the end place each of those eight reads after one of the group's first
+// MFMAs, so their latency hides behind the remaining 56.
 template <bool AK, bool BK, class Issue>
 __device__ __forceinline__ void mma_slab(const float* sa, const float* sb, int wy, int wx, int lane,
-                                         f32x16 (&acc)[2][2], Issue&& issue) {
-    const int r = lane & 31, h = lane >> 5;
-    float a[2][2][4], b[2][2][4];
+                                         f32x4 (&acc)[16], Issue&& issue) {
+    const int r = lane & 15, g = lane >> 4;
+    float a[2][4][4], b[2][4][4];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-        fragment<AK>(sa, wy * 64 + i * 32 + r, h * 4, a[0][i]);
-        fragment<BK>(sb, wx * 64 + i * 32 + r, h * 4, b[0][i]);
+    for (int i = 0; i < 4; ++i) {
+        fragment<AK>(sa, wy * 64 + i * 16 + r, g * 4, a[0][i]);
+        fragment<BK>(sb, wx * 64 + i * 16 + r, g * 4, b[0][i]);
     }
     // The loads of a later slab into the other stage start while the first
     // fragments of this one are read.
     issue();
 #pragma unroll
-    for (int k8 = 0; k8 < kSlab / 8; ++k8) {
-        const int cur = k8 & 1;
-        if (k8 + 1 < kSlab / 8) {
+    for (int kg = 0; kg < kSlab / 16; ++kg) {
+        const int cur = kg & 1;
+        if (kg + 1 < kSlab / 16) {
 #pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                fragment<AK>(sa, wy * 64 + i * 32 + r, (k8 + 1) * 8 + h * 4, a[cur ^ 1][i]);
-                fragment<BK>(sb, wx * 64 + i * 32 + r, (k8 + 1) * 8 + h * 4, b[cur ^ 1][i]);
+            for (int i = 0; i < 4; ++i) {
+                fragment<AK>(sa, wy * 64 + i * 16 + r, (kg + 1) * 16 + g * 4, a[cur ^ 1][i]);
+                fragment<BK>(sb, wx * 64 + i * 16 + r, (kg + 1) * 16 + g * 4, b[cur ^ 1][i]);
             }
         }
 #pragma unroll
-        for (int s = 0; s < 4; ++s)
+        for (int st = 0; st < 4; ++st)
 #pragma unroll
-            for (int i = 0; i < 2; ++i)
+            for (int i = 0; i < 4; ++i)
 #pragma unroll
-                for (int j = 0; j < 2; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[cur][i][s], b[cur][j][s], acc[i][j],
-                                                                     0, 0, 0);
+                for (int j = 0; j < 4; ++j)
+                    acc[i * 4 + j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[cur][i][st], b[cur][j][st],
+                                                                          acc[i * 4 + j], 0, 0, 0);
     }
     if constexpr (AK && BK) {
         constexpr int kMfma = 0x008, kDsRead = 0x100, kVmemRead = 0x020;
-        __builtin_amdgcn_sched_group_barrier(kDsRead, 4, 0);      // group 0's fragments
+        __builtin_amdgcn_sched_group_barrier(kDsRead, 8, 0);      // group 0's fragments
         __builtin_amdgcn_sched_group_barrier(kVmemRead, 8, 0);    // the other stage's slab
 #pragma unroll
-        for (int k8 = 0; k8 + 1 < kSlab / 8; ++k8) {
+        for (int kg = 0; kg + 1 < kSlab / 16; ++kg) {
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
+            for (int q = 0; q < 8; ++q) {
                 __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
-                __builtin_amdgcn_sched_group_barrier(kDsRead, 1, 0);  // group k8+1's fragments
+                __builtin_amdgcn_sched_group_barrier(kDsRead, 1, 0);  // group kg+1's fragments
             }
-            __builtin_amdgcn_sched_group_barrier(kMfma, 12, 0);
+            __builtin_amdgcn_sched_group_barrier(kMfma, 56, 0);
         }
-        __builtin_amdgcn_sched_group_barrier(kMfma, 16, 0);
+        __builtin_amdgcn_sched_group_barrier(kMfma, 64, 0);
     }
 }
 
@@ -264,18 +277,16 @@ __device__ __forceinline__ void finish_slab(GemmStageLds& st, const f32x4 (&rb)[
 // unrolled by two so each half reads one stage and fills the other.
 template <bool AK, bool BK>
 __device__ __forceinline__ void gemm_mainloop(const GemmProblem& p, int tm, int tn, int k0, int k1,
-                                              GemmStageLds& s0, GemmStageLds& s1, f32x16 (&acc)[2][2]) {
+                                              GemmStageLds& s0, GemmStageLds& s1, f32x4 (&acc)[16]) {
     static_assert(AK, "the A operand is always K-contiguous");
     const int row0 = tm * kTile, col0 = tn * kTile;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int wy = wave >> 1, wx = wave & 1;
 
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int b = 0; b < 16; ++b)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+        for (int e = 0; e < 4; ++e) acc[b][e] = 0.0f;
 
     TileLanes tl;
     slab_lanes(p.lda, row0, p.M, tl.a);
@@ -317,20 +328,11 @@ __device__ __forceinline__ void gemm_mainloop(const GemmProblem& p, int tm, int 
 }
 
 // Partial products of split tiles: thread t (= 64 wave + lane) keeps its 64
-// accumulators as 16 float4, float4 q of a block at q * 1024 + 4 t (coalesced
-// across threads).
-__device__ __forceinline__ void store_partial(float* __restrict__ blk, const f32x16 (&acc)[2][2]) {
+// accumulators as 16 float4 (one per block), float4 b of a partial at
+// b * 1024 + 4 t (coalesced across threads).
+__device__ __forceinline__ void store_partial(float* __restrict__ blk, const f32x4 (&acc)[16]) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                f32x4 v;
-                v[0] = acc[i][j][q * 4 + 0]; v[1] = acc[i][j][q * 4 + 1];
-                v[2] = acc[i][j][q * 4 + 2]; v[3] = acc[i][j][q * 4 + 3];
-                *reinterpret_cast<f32x4*>(blk + ((i * 2 + j) * 4 + q) * 1024 + 4 * threadIdx.x) = v;
-            }
+    for (int b = 0; b < 16; ++b) *reinterpret_cast<f32x4*>(blk + b * 1024 + 4 * threadIdx.x) = acc[b];
 }
 
 // The 64 values of one partial product that thread t of the computing workgroup kept.
@@ -339,17 +341,12 @@ __device__ __forceinline__ void load_partial(const float* __restrict__ blk, int 
     for (int b = 0; b < 16; ++b) v[b] = *(global_f32x4*)(blk + b * 1024 + 4 * t);
 }
 
-__device__ __forceinline__ void add_partial(const f32x4 (&v)[16], f32x16 (&acc)[2][2]) {
+__device__ __forceinline__ void add_partial(const f32x4 (&v)[16], f32x4 (&acc)[16]) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const f32x4 w = v[(i * 2 + j) * 4 + q];
-                acc[i][j][q * 4 + 0] += w[0]; acc[i][j][q * 4 + 1] += w[1];
-                acc[i][j][q * 4 + 2] += w[2]; acc[i][j][q * 4 + 3] += w[3];
-            }
+    for (int b = 0; b < 16; ++b) {
+        acc[b][0] += v[b][0]; acc[b][1] += v[b][1];
+        acc[b][2] += v[b][2]; acc[b][3] += v[b][3];
+    }
 }
 
 typedef __attribute__((address_space(1))) float gfloat;
@@ -375,12 +372,12 @@ __device__ __forceinline__ void st4_at(float* base, unsigned byte_off, f32x4 v) 
 // uniform base pointers; per-element masks are only evaluated on edge tiles
 // and on diagonal tiles of symmetric results.
 template <int F, bool UP, bool MASKED>
-__device__ __forceinline__ double epilogue_body(const GemmProblem& p, int tm, int tn, const f32x16 (&acc)[2][2],
+__device__ __forceinline__ double epilogue_body(const GemmProblem& p, int tm, int tn, const f32x4 (&acc)[16],
                                                 float ci, float cx, float cc, int lane, int wave) {
     constexpr bool kReadX = (F & EF_READX) != 0;
     constexpr bool kRead = (F & (EF_READX | EF_DOT)) != 0;
     const int row0 = tm * kTile, col0 = tn * kTile;
-    const int wy = wave >> 1, wx = wave & 1, h = lane >> 5;
+    const int wy = wave >> 1, wx = wave & 1;
     const bool diag = MASKED && UP && tm == tn;
     const bool ident = kReadX && ci != 0.f && tm == tn;
     constexpr double w_off = UP ? 2.0 : 1.0;   // off-diagonal tiles of a symmetric result
@@ -396,173 +393,150 @@ __device__ __forceinline__ double epilogue_body(const GemmProblem& p, int tm, in
     // Masked tiles clamp positions outside M x N to the last row and column
     // and drop those values; every position the thread uses is also one it
     // writes, and no other thread writes it.
-    f32x16 xv[2][2];
+    f32x4 xv[16];
     if constexpr (kRead) {
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int b = 0; b < 16; ++b) {
+            const int col = col0 + acc_col(b, lane, wx);
+            const int colc = MASKED ? min(col, p.N - 1) : col;
+            // rowb .. rowb+3 are all inside M when rowb is (M is a multiple of 4).
+            const int rowb = row0 + acc_row(b, lane, wy);
+            const int rowc = MASKED ? min(rowb, p.M - 4) : rowb;
+            const unsigned ox = (unsigned)rowc * sx + 4u * (unsigned)colc;
 #pragma unroll
-            for (int j = 0; j < 2; ++j) {
-                const int col = col0 + wx * 64 + j * 32 + (lane & 31);
-                const int colc = MASKED ? min(col, p.N - 1) : col;
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    // rowb .. rowb+3 are all inside M when rowb is (M is a multiple of 4).
-                    const int rowb = row0 + wy * 64 + i * 32 + q * 8 + h * 4;
-                    const int rowc = MASKED ? min(rowb, p.M - 4) : rowb;
-                    const unsigned ox = (unsigned)rowc * sx + 4u * (unsigned)colc;
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) xv[i][j][q * 4 + e] = ld_at(X, ox + e * sx);
-                }
-            }
+            for (int e = 0; e < 4; ++e) xv[b][e] = ld_at(X, ox + e * sx);
+        }
     }
 
     double part = 0.0;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int b = 0; b < 16; ++b) {
+        const int col = col0 + acc_col(b, lane, wx);
+        const int rowb = row0 + acc_row(b, lane, wy);
+        // rowb .. rowb+3 are all inside M when rowb is (M is a multiple of 4).
+        if (MASKED && (rowb >= p.M || col >= p.N)) continue;
+        // X at positions this thread writes (read and written by the same thread).
+        f32x4 x;
+        f32x4 out;
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const int col = col0 + wx * 64 + j * 32 + (lane & 31);
+        for (int e = 0; e < 4; ++e) {
+            const float v = acc[b][e];
+            float o = cc * v;
+            if constexpr (kRead) x[e] = xv[b][e];
+            if constexpr (kReadX) {
+                const float id = (ident && rowb + e == col && col < p.valid_m) ? ci : 0.0f;
+                o = (id + cx * x[e]) + o;
+            }
+            out[e] = o;
+        }
+        if (!diag) {
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int rowb = row0 + wy * 64 + i * 32 + q * 8 + h * 4;
-                // rowb .. rowb+3 are all inside M when rowb is (M is a multiple of 4).
-                if (MASKED && (rowb >= p.M || col >= p.N)) continue;
-                // X at positions this thread writes (read and written by the same thread).
-                f32x4 x;
-                f32x4 out;
+            for (int e = 0; e < 4; ++e) {
+                if constexpr ((F & EF_NORM) != 0) part += w_off * (double)out[e] * (double)out[e];
+                if constexpr ((F & EF_DOT) != 0) part += w_off * (double)acc[b][e] * (double)x[e];
+            }
+            if constexpr ((F & EF_STORE) != 0) {
+                const unsigned oc = (unsigned)rowb * sc + 4u * (unsigned)col;
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const float v = acc[i][j][q * 4 + e];
-                    float o = cc * v;
-                    if constexpr (kRead) x[e] = xv[i][j][q * 4 + e];
-                    if constexpr (kReadX) {
-                        const float id = (ident && rowb + e == col && col < p.valid_m) ? ci : 0.0f;
-                        o = (id + cx * x[e]) + o;
-                    }
-                    out[e] = o;
-                }
-                if (!diag) {
+                for (int e = 0; e < 4; ++e) st_at(C, oc + e * sc, out[e]);
+                if constexpr (UP) st4_at(C, (unsigned)col * sc + 4u * (unsigned)rowb, out);
+            }
+            if constexpr ((F & EF_STORE_T) != 0) st4_at(C2, (unsigned)col * sc2 + 4u * (unsigned)rowb, out);
+        } else {
+            // Diagonal tile of a symmetric result: element (row, col) with
+            // row <= col is written at both positions.
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        if constexpr ((F & EF_NORM) != 0) part += w_off * (double)out[e] * (double)out[e];
-                        if constexpr ((F & EF_DOT) != 0) part += w_off * (double)acc[i][j][q * 4 + e] * (double)x[e];
-                    }
-                    if constexpr ((F & EF_STORE) != 0) {
-                        const unsigned oc = (unsigned)rowb * sc + 4u * (unsigned)col;
-#pragma unroll
-                        for (int e = 0; e < 4; ++e) st_at(C, oc + e * sc, out[e]);
-                        if constexpr (UP) st4_at(C, (unsigned)col * sc + 4u * (unsigned)rowb, out);
-                    }
-                    if constexpr ((F & EF_STORE_T) != 0) st4_at(C2, (unsigned)col * sc2 + 4u * (unsigned)rowb, out);
-                } else {
-                    // Diagonal tile of a symmetric result: element (row, col) with
-                    // row <= col is written at both positions.
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const int row = rowb + e;
-                        if (row > col) continue;
-                        const double w = row != col ? 2.0 : 1.0;
-                        if constexpr ((F & EF_NORM) != 0) part += w * (double)out[e] * (double)out[e];
-                        if constexpr ((F & EF_DOT) != 0) part += w * (double)acc[i][j][q * 4 + e] * (double)x[e];
-                        if constexpr ((F & EF_STORE) != 0) {
-                            st_at(C, (unsigned)row * sc + 4u * (unsigned)col, out[e]);
-                            if (row != col) st_at(C, (unsigned)col * sc + 4u * (unsigned)row, out[e]);
-                        }
-                    }
+            for (int e = 0; e < 4; ++e) {
+                const int row = rowb + e;
+                if (row > col) continue;
+                const double w = row != col ? 2.0 : 1.0;
+                if constexpr ((F & EF_NORM) != 0) part += w * (double)out[e] * (double)out[e];
+                if constexpr ((F & EF_DOT) != 0) part += w * (double)acc[b][e] * (double)x[e];
+                if constexpr ((F & EF_STORE) != 0) {
+                    st_at(C, (unsigned)row * sc + 4u * (unsigned)col, out[e]);
+                    if (row != col) st_at(C, (unsigned)col * sc + 4u * (unsigned)row, out[e]);
                 }
             }
         }
+    }
     return part;
 }
 
 // The epilogue for a flag combination without a compiled body (not used by
 // the launch tables the library builds; kept so every combination works).
-__device__ __forceinline__ double epilogue_generic(const GemmProblem& p, int tm, int tn, const f32x16 (&acc)[2][2],
+__device__ __forceinline__ double epilogue_generic(const GemmProblem& p, int tm, int tn, const f32x4 (&acc)[16],
                                                 float ci, float cx, float cc, int lane, int wave) {
     double part = 0.0;
     const int F = p.flags;
     const bool up = p.upper != 0;
     const int row0 = tm * kTile, col0 = tn * kTile;
-    const int wy = wave >> 1, wx = wave & 1, h = lane >> 5;
+    const int wy = wave >> 1, wx = wave & 1;
     float* C = p.C;
     float* C2 = p.C2;
     const float* X = p.X;
     const unsigned sc = 4u * p.ldc, sc2 = 4u * p.ldc2, sx = 4u * p.ldx;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int b = 0; b < 16; ++b) {
+        const int col = col0 + acc_col(b, lane, wx);
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const int col = col0 + wx * 64 + j * 32 + (lane & 31);
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int row = row0 + wy * 64 + i * 32 + q * 8 + h * 4 + e;
-                    if (row >= p.M || col >= p.N || (up && row > col)) continue;
-                    const float v = acc[i][j][q * 4 + e];
-                    const float xe = (F & (EF_READX | EF_DOT)) ? ld_at(X, (unsigned)row * sx + 4u * (unsigned)col) : 0.f;
-                    float o = cc * v;
-                    if (F & EF_READX) o = (((row == col && row < p.valid_m) ? ci : 0.0f) + cx * xe) + o;
-                    const double w = (up && row != col) ? 2.0 : 1.0;
-                    if (F & EF_NORM) part += w * (double)o * (double)o;
-                    if (F & EF_DOT) part += w * (double)v * (double)xe;
-                    if (F & EF_STORE) {
-                        st_at(C, (unsigned)row * sc + 4u * (unsigned)col, o);
-                        if (up && row != col) st_at(C, (unsigned)col * sc + 4u * (unsigned)row, o);
-                    }
-                    if (F & EF_STORE_T) st_at(C2, (unsigned)col * sc2 + 4u * (unsigned)row, o);
-                }
+        for (int e = 0; e < 4; ++e) {
+            const int row = row0 + acc_row(b, lane, wy) + e;
+            if (row >= p.M || col >= p.N || (up && row > col)) continue;
+            const float v = acc[b][e];
+            const float xe = (F & (EF_READX | EF_DOT)) ? ld_at(X, (unsigned)row * sx + 4u * (unsigned)col) : 0.f;
+            float o = cc * v;
+            if (F & EF_READX) o = (((row == col && row < p.valid_m) ? ci : 0.0f) + cx * xe) + o;
+            const double w = (up && row != col) ? 2.0 : 1.0;
+            if (F & EF_NORM) part += w * (double)o * (double)o;
+            if (F & EF_DOT) part += w * (double)v * (double)xe;
+            if (F & EF_STORE) {
+                st_at(C, (unsigned)row * sc + 4u * (unsigned)col, o);
+                if (up && row != col) st_at(C, (unsigned)col * sc + 4u * (unsigned)row, o);
+            }
+            if (F & EF_STORE_T) st_at(C2, (unsigned)col * sc2 + 4u * (unsigned)row, o);
         }
+    }
     return part;
 }
 
 // m = beta1 m + (1 - beta1) acc on the dense valid_m x valid_n momentum.
 template <bool MASKED>
 __device__ __forceinline__ double epilogue_momentum(const GemmProblem& p, int tm, int tn,
-                                                    const f32x16 (&acc)[2][2], float beta1, int lane, int wave) {
+                                                    const f32x4 (&acc)[16], float beta1, int lane, int wave) {
     const int row0 = tm * kTile, col0 = tn * kTile;
-    const int wy = wave >> 1, wx = wave & 1, h = lane >> 5;
+    const int wy = wave >> 1, wx = wave & 1;
     float* mom = p.mom;
     const unsigned sm = 4u * p.ldmom;
     // All of this thread's momentum values are loaded before any is stored
     // (one memory round trip per tile); masked tiles clamp positions outside
     // the dense valid_m x valid_n momentum to its last row and column and
     // drop those values.
-    f32x16 mv[2][2];
+    f32x4 mv[16];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int b = 0; b < 16; ++b) {
+        const int col = col0 + acc_col(b, lane, wx);
+        const int colc = MASKED ? min(col, p.valid_n - 1) : col;
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const int col = col0 + wx * 64 + j * 32 + (lane & 31);
-            const int colc = MASKED ? min(col, p.valid_n - 1) : col;
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int row = row0 + wy * 64 + i * 32 + q * 8 + h * 4 + e;
-                    const int rowc = MASKED ? min(row, p.valid_m - 1) : row;
-                    mv[i][j][q * 4 + e] = ld_at(mom, (unsigned)rowc * sm + 4u * (unsigned)colc);
-                }
+        for (int e = 0; e < 4; ++e) {
+            const int row = row0 + acc_row(b, lane, wy) + e;
+            const int rowc = MASKED ? min(row, p.valid_m - 1) : row;
+            mv[b][e] = ld_at(mom, (unsigned)rowc * sm + 4u * (unsigned)colc);
         }
+    }
     double part = 0.0;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int b = 0; b < 16; ++b) {
+        const int col = col0 + acc_col(b, lane, wx);
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const int col = col0 + wx * 64 + j * 32 + (lane & 31);
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int row = row0 + wy * 64 + i * 32 + q * 8 + h * 4 + e;
-                    if (MASKED && !(row < p.valid_m && col < p.valid_n)) continue;
-                    const unsigned o = (unsigned)row * sm + 4u * (unsigned)col;
-                    const float old = mv[i][j][q * 4 + e];
-                    const float mn = beta1 * old + (1.0f - beta1) * acc[i][j][q * 4 + e];
-                    st_at(mom, o, mn);
-                    part += (double)mn * (double)mn;
-                }
+        for (int e = 0; e < 4; ++e) {
+            const int row = row0 + acc_row(b, lane, wy) + e;
+            if (MASKED && !(row < p.valid_m && col < p.valid_n)) continue;
+            const unsigned o = (unsigned)row * sm + 4u * (unsigned)col;
+            const float mn = beta1 * mv[b][e] + (1.0f - beta1) * acc[b][e];
+            st_at(mom, o, mn);
+            part += (double)mn * (double)mn;
         }
+    }
     return part;
 }
 
@@ -579,7 +553,7 @@ __device__ __forceinline__ double epilogue_momentum(const GemmProblem& p, int tm
 // The epilogue reads X only at the positions it is about to write, by the
 // same thread, so X may alias C (an in-place update).
 __device__ __forceinline__ void gemm_epilogue(const GemmProblem& p, int tm, int tn, int slot, float beta1,
-                                              const f32x16 (&acc)[2][2], int lane, int wave) {
+                                              const f32x4 (&acc)[16], int lane, int wave) {
     const int flags = p.flags;
     double part = 0.0;
     if (flags & EF_MOMENTUM) {
@@ -681,26 +655,23 @@ __device__ __forceinline__ void small_fragment(const float* s, int mn, int k, fl
     f[0] = v[0]; f[1] = v[1]; f[2] = v[2]; f[3] = v[3];
 }
 
-// The MFMAs of one small-mode slab: lane l contributes k = 8 g + 4 (l / 32) + s
-// to step s of group g, for A and B alike (as in mma_slab).
-__device__ __forceinline__ void small_mma(const float* sa, const float* sb, int lane, f32x16 (&acc)[2][2]) {
-    const int r = lane & 31, h = lane >> 5;
+// The MFMAs of one small-mode slab: lane l contributes k = 4 (l / 16) + s
+// to step s, for A and B alike (as in mma_slab).
+__device__ __forceinline__ void small_mma(const float* sa, const float* sb, int lane, f32x4 (&acc)[16]) {
+    const int r = lane & 15, g = lane >> 4;
+    float a[4][4], b[4][4];
 #pragma unroll
-    for (int g = 0; g < kSmallSlab / 8; ++g) {
-        float a[2][4], b[2][4];
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            small_fragment(sa, i * 32 + r, g * 8 + h * 4, a[i]);
-            small_fragment(sb, i * 32 + r, g * 8 + h * 4, b[i]);
-        }
-#pragma unroll
-        for (int st = 0; st < 4; ++st)
-#pragma unroll
-            for (int i = 0; i < 2; ++i)
-#pragma unroll
-                for (int j = 0; j < 2; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][st], b[j][st], acc[i][j], 0, 0, 0);
+    for (int i = 0; i < 4; ++i) {
+        small_fragment(sa, i * 16 + r, g * 4, a[i]);
+        small_fragment(sb, i * 16 + r, g * 4, b[i]);
     }
+#pragma unroll
+    for (int st = 0; st < 4; ++st)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                acc[i * 4 + j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i][st], b[j][st], acc[i * 4 + j], 0, 0, 0);
 }
 
 // Starts the loads of slab k0 of a small-mode block into stage s (A then B).
@@ -717,13 +688,11 @@ __device__ __forceinline__ void small_issue(const GemmProblem& p, int row0, int 
 // no block computes.
 __device__ __forceinline__ void small_unit(const GemmProblem& p, const SmallUnit& su, float* s0, float* s1,
                                            float beta1, int lane) {
-    f32x16 acc[2][2];
+    f32x4 acc[16];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int b = 0; b < 16; ++b)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+        for (int e = 0; e < 4; ++e) acc[b][e] = 0.0f;
     const int row0 = su.bm * kSmallDim, col0 = su.bn * kSmallDim;
     const int nk = p.K / kSmallSlab;
     small_issue(p, row0, col0, 0, s0);
@@ -777,7 +746,7 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_grouped(const GemmProble
         return;
     }
     const GemmProblem p = probs[td.prob];
-    f32x16 acc[2][2];
+    f32x4 acc[16];
     gemm_mainloop<AK, BK>(p, td.tm, td.tn, td.k0, td.k1, s0, s1, acc);
     if (td.part >= 0)
         store_partial(ws + (size_t)td.part * kSplitBlock, acc);
@@ -799,13 +768,11 @@ __global__ __launch_bounds__(kFixupThreads) void gemm_fixup(const GemmProblem* _
     const int wave = blockIdx.x % kWaveSlots, lane = threadIdx.x;
     const int t = wave * 64 + lane;  // thread of the computing workgroup
     const GemmProblem p = probs[fd.prob];
-    f32x16 acc[2][2];
+    f32x4 acc[16];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int b = 0; b < 16; ++b)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+        for (int e = 0; e < 4; ++e) acc[b][e] = 0.0f;
     // Partials are added in K order; the loads of the next one are in flight
     // while the current one is added (nsplit >= 2).
     const float* blk = ws + (size_t)fd.part0 * kSplitBlock;
