@@ -146,13 +146,24 @@ __device__ __forceinline__ void fragment(const float* s, int mn, int k, float (&
     }
 }
 
+// Which of a wave's 16 blocks it multiplies: every block; on a diagonal
+// tile of a symmetric result, only blocks on or above the diagonal (i <= j)
+// of a diagonal quadrant; or none, for the quadrant below the diagonal. The
+// epilogue of a symmetric result never reads the blocks left out.
+enum BlockSet : int { BS_ALL = 0, BS_UPPER = 1, BS_NONE = 2 };
+
 // The MFMAs of one LDS slab. Fragments of the next 16-wide k group are read
 // from LDS while the MFMAs of the current group run: the scheduling groups
 // at the end place each of those eight reads after one of the group's first
-// MFMAs, so their latency hides behind the remaining 56.
-template <bool AK, bool BK, class Issue>
+// MFMAs, so their latency hides behind the rest.
+template <bool AK, bool BK, int BS, class Issue>
 __device__ __forceinline__ void mma_slab(const float* sa, const float* sb, int wy, int wx, int lane,
                                          f32x4 (&acc)[16], Issue&& issue) {
+    if constexpr (BS == BS_NONE) {
+        issue();
+        return;
+    }
+    constexpr int kBlocks = BS == BS_UPPER ? 10 : 16;   // MFMAs per step
     const int r = lane & 15, g = lane >> 4;
     float a[2][4][4], b[2][4][4];
 #pragma unroll
@@ -179,8 +190,9 @@ __device__ __forceinline__ void mma_slab(const float* sa, const float* sb, int w
             for (int i = 0; i < 4; ++i)
 #pragma unroll
                 for (int j = 0; j < 4; ++j)
-                    acc[i * 4 + j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[cur][i][st], b[cur][j][st],
-                                                                          acc[i * 4 + j], 0, 0, 0);
+                    if (BS == BS_ALL || i <= j)
+                        acc[i * 4 + j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[cur][i][st], b[cur][j][st],
+                                                                              acc[i * 4 + j], 0, 0, 0);
     }
     if constexpr (AK && BK) {
         constexpr int kMfma = 0x008, kDsRead = 0x100, kVmemRead = 0x020;
@@ -193,10 +205,19 @@ __device__ __forceinline__ void mma_slab(const float* sa, const float* sb, int w
                 __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
                 __builtin_amdgcn_sched_group_barrier(kDsRead, 1, 0);  // group kg+1's fragments
             }
-            __builtin_amdgcn_sched_group_barrier(kMfma, 56, 0);
+            __builtin_amdgcn_sched_group_barrier(kMfma, 4 * kBlocks - 8, 0);
         }
-        __builtin_amdgcn_sched_group_barrier(kMfma, 64, 0);
+        __builtin_amdgcn_sched_group_barrier(kMfma, 4 * kBlocks, 0);
     }
+}
+
+// mma_slab for the block set `bs` of the calling wave (uniform across it).
+template <bool AK, bool BK, class Issue>
+__device__ __forceinline__ void mma_slab_for(int bs, const float* sa, const float* sb, int wy, int wx, int lane,
+                                             f32x4 (&acc)[16], Issue&& issue) {
+    if (bs == BS_ALL) mma_slab<AK, BK, BS_ALL>(sa, sb, wy, wx, lane, acc, issue);
+    else if (bs == BS_UPPER) mma_slab<AK, BK, BS_UPPER>(sa, sb, wy, wx, lane, acc, issue);
+    else mma_slab<AK, BK, BS_NONE>(sa, sb, wy, wx, lane, acc, issue);
 }
 
 // Sum of one double per lane over a 64-lane wave, in a fixed order.
@@ -280,8 +301,11 @@ __device__ __forceinline__ void gemm_mainloop(const GemmProblem& p, int tm, int 
                                               GemmStageLds& s0, GemmStageLds& s1, f32x4 (&acc)[16]) {
     static_assert(AK, "the A operand is always K-contiguous");
     const int row0 = tm * kTile, col0 = tn * kTile;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int wy = wave >> 1, wx = wave & 1;
+    // On a diagonal tile of a symmetric result the quadrant below the
+    // diagonal is not needed and the diagonal quadrants only on and above it.
+    const int bs = (p.upper && tm == tn) ? (wy > wx ? BS_NONE : wy == wx ? BS_UPPER : BS_ALL) : BS_ALL;
 
 #pragma unroll
     for (int b = 0; b < 16; ++b)
@@ -306,22 +330,22 @@ __device__ __forceinline__ void gemm_mainloop(const GemmProblem& p, int tm, int 
         // Raised issue priority while this wave runs its MFMAs: the two waves
         // sharing a SIMD then alternate between MFMA and memory phases.
         __builtin_amdgcn_s_setprio(1);
-        mma_slab<AK, BK>(s0.a, s0.b, wy, wx, lane, acc,
-                         [&] { issue_slab<BK>(p, tl, col0, k0 + (kt + 1) * kSlab, s1, rb); });
+        mma_slab_for<AK, BK>(bs, s0.a, s0.b, wy, wx, lane, acc,
+                             [&] { issue_slab<BK>(p, tl, col0, k0 + (kt + 1) * kSlab, s1, rb); });
         __builtin_amdgcn_s_setprio(0);
         finish_slab<BK>(s1, rb);
         // Past the last slab the load repeats slab nk - 1 into the idle stage
         // (never read), which keeps the loop free of branches.
         const int kn = min(kt + 2, nk - 1);
         __builtin_amdgcn_s_setprio(1);
-        mma_slab<AK, BK>(s1.a, s1.b, wy, wx, lane, acc,
-                         [&] { issue_slab<BK>(p, tl, col0, k0 + kn * kSlab, s0, rb); });
+        mma_slab_for<AK, BK>(bs, s1.a, s1.b, wy, wx, lane, acc,
+                             [&] { issue_slab<BK>(p, tl, col0, k0 + kn * kSlab, s0, rb); });
         __builtin_amdgcn_s_setprio(0);
         finish_slab<BK>(s0, rb);
     }
     if (kt < nk) {  // odd slab count: the last slab is in s0
         __builtin_amdgcn_s_setprio(1);
-        mma_slab<AK, BK>(s0.a, s0.b, wy, wx, lane, acc, [] {});
+        mma_slab_for<AK, BK>(bs, s0.a, s0.b, wy, wx, lane, acc, [] {});
         __builtin_amdgcn_s_setprio(0);
     }
     __syncthreads();  // every wave is done with both stages
