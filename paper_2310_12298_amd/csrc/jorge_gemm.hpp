@@ -680,7 +680,10 @@ __device__ __forceinline__ void small_fragment(const float* s, int mn, int k, fl
 }
 
 // The MFMAs of one small-mode slab: lane l contributes k = 4 (l / 16) + s
-// to step s, for A and B alike (as in mma_slab).
+// to step s, for A and B alike (as in mma_slab). UPPER: a block on the
+// diagonal of a symmetric result, whose 16 x 16 blocks below the diagonal are
+// left out.
+template <bool UPPER>
 __device__ __forceinline__ void small_mma(const float* sa, const float* sb, int lane, f32x4 (&acc)[16]) {
     const int r = lane & 15, g = lane >> 4;
     float a[4][4], b[4][4];
@@ -695,7 +698,8 @@ __device__ __forceinline__ void small_mma(const float* sa, const float* sb, int 
         for (int i = 0; i < 4; ++i)
 #pragma unroll
             for (int j = 0; j < 4; ++j)
-                acc[i * 4 + j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i][st], b[j][st], acc[i * 4 + j], 0, 0, 0);
+                if (!UPPER || i <= j)
+                    acc[i * 4 + j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i][st], b[j][st], acc[i * 4 + j], 0, 0, 0);
 }
 
 // Starts the loads of slab k0 of a small-mode block into stage s (A then B).
@@ -719,6 +723,7 @@ __device__ __forceinline__ void small_unit(const GemmProblem& p, const SmallUnit
         for (int e = 0; e < 4; ++e) acc[b][e] = 0.0f;
     const int row0 = su.bm * kSmallDim, col0 = su.bn * kSmallDim;
     const int nk = p.K / kSmallSlab;
+    const bool diag = p.upper && su.bm == su.bn;   // uniform: the block is read with scalar loads
     small_issue(p, row0, col0, 0, s0);
     for (int kt = 0; kt < nk; ++kt) {
         float* cur = (kt & 1) ? s1 : s0;
@@ -731,7 +736,8 @@ __device__ __forceinline__ void small_unit(const GemmProblem& p, const SmallUnit
         } else {
             asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         }
-        small_mma(cur, cur + kSmallOperand, lane, acc);
+        if (diag) small_mma<true>(cur, cur + kSmallOperand, lane, acc);
+        else small_mma<false>(cur, cur + kSmallOperand, lane, acc);
     }
     const int quadrant = ((su.bm & 1) << 1) | (su.bn & 1);
     gemm_epilogue(p, su.bm >> 1, su.bn >> 1, su.slot, beta1, acc, lane, quadrant);
