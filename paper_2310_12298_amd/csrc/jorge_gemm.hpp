@@ -15,11 +15,12 @@
 // (global_load_lds_dwordx4, no register staging); an MN-contiguous operand
 // (the NN kernel's B) is held in registers and written to LDS after the MFMAs.
 //
-// Within a slab, lane l of a wave contributes k = 16*kg + 4*(l/16) + s to the
-// MFMA of step s (s = 0..3) of 16-wide k group kg: the four lane groups take
-// disjoint quarters of each group, so a K-contiguous operand is read from LDS
-// as one 16-byte load per lane per 16 k values. The same k map is used for A
-// and B, so every product A[i][k] * B[k][j] is formed exactly once.
+// Within a slab, lane l of a wave contributes k = 16*kg + 4*q + s to the MFMA
+// of step s (s = 0..3) of 16-wide k group kg, with q = quarter(l / 16): the
+// four lane groups take disjoint quarters of each group, so a K-contiguous
+// operand is read from LDS as one 16-byte load per lane per 16 k values. The
+// same k map is used for A and B, so every product A[i][k] * B[k][j] is
+// formed exactly once.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -36,6 +37,12 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 // the quadrant) is one v_mfma_f32_16x16x4_f32 accumulator, in which lane l
 // holds column l % 16, rows 4 (l / 16) .. 4 (l / 16) + 3. Each lane thus
 // holds, for each of its 16 blocks, four consecutive rows of one column.
+// The k quarter that lane group g (lanes 16 g .. 16 g + 15) reads: groups 1
+// and 2 swapped. A 16-byte LDS read is served in passes that pair lanes
+// 0-7 with 32-39 (8-15 with 40-47, ...); with the swap, the two halves of a
+// pass read chunks an odd distance apart, which the XOR layout below puts in
+// opposite halves of the banks (with the identity map they collide 2-way).
+__device__ __forceinline__ int quarter(int g) { return ((g & 1) << 1) | (g >> 1); }
 // Row and column of the first of those four values, relative to the tile:
 __device__ __forceinline__ int acc_row(int b, int lane, int wy) { return wy * 64 + (b >> 2) * 16 + (lane >> 4) * 4; }
 __device__ __forceinline__ int acc_col(int b, int lane, int wx) { return wx * 64 + (b & 3) * 16 + (lane & 15); }
@@ -164,12 +171,12 @@ __device__ __forceinline__ void mma_slab(const float* sa, const float* sb, int w
         issue();
         return;
     }
-    const int r = lane & 15, g = lane >> 4;
+    const int r = lane & 15, q = quarter(lane >> 4);
     float a[2][4][4], b[2][4][4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        fragment<AK>(sa, wy * 64 + i * 16 + r, g * 4, a[0][i]);
-        fragment<BK>(sb, wx * 64 + i * 16 + r, g * 4, b[0][i]);
+        fragment<AK>(sa, wy * 64 + i * 16 + r, q * 4, a[0][i]);
+        fragment<BK>(sb, wx * 64 + i * 16 + r, q * 4, b[0][i]);
     }
     // The loads of a later slab into the other stage (the compiler places
     // them among this slab's MFMAs).
@@ -180,8 +187,8 @@ __device__ __forceinline__ void mma_slab(const float* sa, const float* sb, int w
         if (kg + 1 < kSlab / 16) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                fragment<AK>(sa, wy * 64 + i * 16 + r, (kg + 1) * 16 + g * 4, a[cur ^ 1][i]);
-                fragment<BK>(sb, wx * 64 + i * 16 + r, (kg + 1) * 16 + g * 4, b[cur ^ 1][i]);
+                fragment<AK>(sa, wy * 64 + i * 16 + r, (kg + 1) * 16 + q * 4, a[cur ^ 1][i]);
+                fragment<BK>(sb, wx * 64 + i * 16 + r, (kg + 1) * 16 + q * 4, b[cur ^ 1][i]);
             }
         }
 #pragma unroll
