@@ -6,9 +6,8 @@
 // per problem), so products with different epilogues share a launch. A
 // workgroup of 256 threads computes one 128 x 128 tile of C = A * B; its
 // four waves each own a 64 x 64 sub-tile held as 4 x 4 blocks of
-// v_mfma_f32_16x16x4_f32 accumulators (this form moves half as many
-// accumulator registers per flop as the 32 x 32 one, which keeps the clock
-// higher under the chip's power limit). K is consumed in
+// v_mfma_f32_16x16x4_f32 accumulators (this form reads and writes half as
+// many accumulator registers per flop as the 32 x 32 one). K is consumed in
 // slabs of 32 staged through double-buffered LDS (one barrier per slab): while
 // the waves run the MFMAs of slab k, slab k+1 streams into the other buffer.
 // K-contiguous operands go straight from global memory to LDS
@@ -37,15 +36,16 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 // the quadrant) is one v_mfma_f32_16x16x4_f32 accumulator, in which lane l
 // holds column l % 16, rows 4 (l / 16) .. 4 (l / 16) + 3. Each lane thus
 // holds, for each of its 16 blocks, four consecutive rows of one column.
+// Row and column of the first of those four values, relative to the tile:
+__device__ __forceinline__ int acc_row(int b, int lane, int wy) { return wy * 64 + (b >> 2) * 16 + (lane >> 4) * 4; }
+__device__ __forceinline__ int acc_col(int b, int lane, int wx) { return wx * 64 + (b & 3) * 16 + (lane & 15); }
+
 // The k quarter that lane group g (lanes 16 g .. 16 g + 15) reads: groups 1
 // and 2 swapped. A 16-byte LDS read is served in passes that pair lanes
 // 0-7 with 32-39 (8-15 with 40-47, ...); with the swap, the two halves of a
 // pass read chunks an odd distance apart, which the XOR layout below puts in
 // opposite halves of the banks (with the identity map they collide 2-way).
 __device__ __forceinline__ int quarter(int g) { return ((g & 1) << 1) | (g >> 1); }
-// Row and column of the first of those four values, relative to the tile:
-__device__ __forceinline__ int acc_row(int b, int lane, int wy) { return wy * 64 + (b >> 2) * 16 + (lane >> 4) * 4; }
-__device__ __forceinline__ int acc_col(int b, int lane, int wx) { return wx * 64 + (b & 3) * 16 + (lane & 15); }
 
 constexpr int kTile = 128;                    // tile rows = tile columns
 constexpr int kSlab = 32;                     // K per LDS stage
@@ -59,8 +59,9 @@ constexpr int kGemmThreads = 256;
 // 8 distinct 16-byte bank groups, and the 128-byte pad between blocks moves
 // the next 8 rows to the other half of a 64-bank LDS.
 constexpr int kLdsBlock = 8 * 32 + 32;        // floats per 8-row block, with its pad
-// Row stride of an M/N-contiguous operand in LDS: 132 floats puts the four
-// k rows that one fragment read touches (4 apart) on distinct bank quarters.
+// Row stride of an M/N-contiguous operand in LDS: 132 floats puts the rows
+// that the four lane groups read in one step (4 apart) on distinct quarters
+// of the banks.
 constexpr int kLdsMN = kTile + 4;
 constexpr int kLdsOperand = 16 * kLdsBlock;   // floats per operand per stage (>= kSlab * kLdsMN)
 static_assert(kLdsOperand >= kSlab * kLdsMN, "LDS operand buffer too small");
