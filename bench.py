@@ -55,11 +55,15 @@ def profile_path(config):
     return PROFILES.get(config, os.path.join(ROOT, "profiles", f"jorge_step_{config}.md"))
 
 
+# The sources that decide what the grouped GEMM runs: the kernel itself and the
+# host code that builds its launch tables (not the bandwidth-bound kernels).
+GEMM_SOURCES = ("jorge.hip", "jorge_gemm.hpp", "jorge_types.hpp")
+
+
 def kernel_sources_sha256():
-    import glob
     import hashlib
     h = hashlib.sha256()
-    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2310_12298_amd", "csrc", "*"))):
+    for f in sorted(os.path.join(ROOT, "paper_2310_12298_amd", "csrc", n) for n in GEMM_SOURCES):
         h.update(os.path.basename(f).encode())
         with open(f, "rb") as fh:
             h.update(fh.read())

@@ -42,22 +42,49 @@ __global__ __launch_bounds__(kEwThreads) void stagein_kernel(const LayerDev* __r
     const int m = L.m, n = L.n;
     const bool vec = (n & 3) == 0 && (reinterpret_cast<uintptr_t>(G) & 15) == 0;
     double part = 0.0;
-    // Row r, columns c .. c+3 of the block.
-    for (int q = threadIdx.x; q < 64 * 16; q += kEwThreads) {
-        const int r = q >> 4, c = (q & 15) * 4, gr = st.r0 + r, gc = st.c0 + c;
-        if (gr >= m || gc >= n) continue;
-        const size_t gi = (size_t)gr * n + gc;
-        f32x4 g, v;
-        if (vec) {  // gc + 3 < n: n and gc are multiples of 4
-            g = *reinterpret_cast<const f32x4*>(G + gi);
-            const f32x4 ms = *reinterpret_cast<const f32x4*>(L.msgd + gi);
+    // Row r, columns c .. c+3 of the block, for q = 16 r + c / 4.
+    if (vec) {
+        // Every load of the thread is issued before its first store, so
+        // eight 16-byte loads are in flight at once (no store overwrites what
+        // a later load of the thread reads, which the compiler cannot prove
+        // by itself). The loads are unconditional: a position outside the
+        // layer reads the nearest one inside it (n >= 4) and its values are
+        // dropped.
+        constexpr int kIt = 64 * 16 / kEwThreads;
+        float* __restrict__ msgd = L.msgd;
+        float* __restrict__ Gp = L.Gp;
+        const size_t np = (size_t)L.np;
+        f32x4 g[kIt], ms[kIt];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) v[j] = beta1 * ms[j] + g[j];
-            *reinterpret_cast<f32x4*>(L.Gp + (size_t)gr * L.np + gc) = g;
-            *reinterpret_cast<f32x4*>(L.msgd + gi) = v;
+        for (int i = 0; i < kIt; ++i) {
+            const int q = threadIdx.x + i * kEwThreads;
+            const int gr = min(st.r0 + (q >> 4), m - 1), gc = min(st.c0 + (q & 15) * 4, n - 4);
+            const size_t gi = (size_t)gr * n + gc;
+            g[i] = gload4(G + gi);
+            ms[i] = gload4(msgd + gi);
+        }
+#pragma unroll
+        for (int i = 0; i < kIt; ++i) {
+            const int q = threadIdx.x + i * kEwThreads, r = q >> 4, c = (q & 15) * 4;
+            const int gr = st.r0 + r, gc = st.c0 + c;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) blk[r][c + j] = g[i][j];
+            if (gr >= m || gc >= n) continue;  // gc + 3 < n: n and gc are multiples of 4
+            const size_t gi = (size_t)gr * n + gc;
+            f32x4 v;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) v[j] = beta1 * ms[i][j] + g[i][j];
+            *(gfloat4*)(Gp + (size_t)gr * np + gc) = g[i];
+            *(gfloat4*)(msgd + gi) = v;
 #pragma unroll
             for (int j = 0; j < 4; ++j) part += (double)v[j] * (double)v[j];
-        } else {
+        }
+    } else {
+        for (int q = threadIdx.x; q < 64 * 16; q += kEwThreads) {
+            const int r = q >> 4, c = (q & 15) * 4, gr = st.r0 + r, gc = st.c0 + c;
+            if (gr >= m || gc >= n) continue;
+            const size_t gi = (size_t)gr * n + gc;
+            f32x4 g;
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 g[j] = 0.0f;
@@ -69,9 +96,9 @@ __global__ __launch_bounds__(kEwThreads) void stagein_kernel(const LayerDev* __r
                     part += (double)w * (double)w;
                 }
             }
-        }
 #pragma unroll
-        for (int j = 0; j < 4; ++j) blk[r][c + j] = g[j];
+            for (int j = 0; j < 4; ++j) blk[r][c + j] = g[j];
+        }
     }
     __syncthreads();
     // Column c, rows r .. r+3 of the block: Gpt[c][r..r+3] (mp is a multiple of 32).
@@ -400,9 +427,27 @@ __global__ __launch_bounds__(kEwThreads) void weight_kernel(const LayerDev* __re
     const float* __restrict__ m = L.mom;
     if ((ck.count & 3) == 0 && (reinterpret_cast<uintptr_t>(th) & 15) == 0) {
         const int n4 = ck.count >> 2;
-        f32x4* t4 = reinterpret_cast<f32x4*>(th + ck.start);
-        const f32x4* m4 = reinterpret_cast<const f32x4*>(m + ck.start);
-        for (int e = threadIdx.x; e < n4; e += kEwThreads) {
+        // Global (not generic) accesses, four per array per thread in flight:
+        // each group of four iterations issues its loads before its stores,
+        // then the remainder goes one by one.
+        gfloat4* t4 = (gfloat4*)(th + ck.start);
+        const global_f32x4* m4 = (const global_f32x4*)(m + ck.start);
+        int e = threadIdx.x;
+        for (; e + 3 * kEwThreads < n4; e += 4 * kEwThreads) {
+            f32x4 t[4], mv[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                t[i] = t4[e + i * kEwThreads];
+                mv[i] = m4[e + i * kEwThreads];
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+#pragma unroll
+                for (int q = 0; q < 4; ++q) t[i][q] = t[i][q] * decay - g * mv[i][q];
+                t4[e + i * kEwThreads] = t[i];
+            }
+        }
+        for (; e < n4; e += kEwThreads) {
             f32x4 t = t4[e];
             const f32x4 mv = m4[e];
 #pragma unroll
