@@ -98,6 +98,30 @@ NON_UPDATE_STAGES = ("precond_L", "precond_R")
 FIXUP_STAGE = "split_fixup"
 
 
+def copy_reference_gbs(mib=1024, reps=10):
+    """Device-to-device copy rate of a buffer far larger than the caches (GB/s).
+
+    The streaming rate this GPU sustains in practice, beside which the
+    bandwidth-bound kernels' rates are read (bytes read plus bytes written).
+    """
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    stop.record()
+    torch.cuda.synchronize()
+    gbs = 2 * n * 4 * reps / (start.elapsed_time(stop) * 1e-3) / 1e9
+    del src, dst
+    torch.cuda.empty_cache()
+    return gbs
+
+
 def cpu_baseline(shapes, sigma, seed, budget_s, series_order=2):
     """The fp64 oracle timed on the host over a bounded, deterministic sample.
 
@@ -238,6 +262,9 @@ def main():
         k_ms = timing[k][0] / max(1, timing[k][1])
         gbs = nbytes / (k_ms * 1e-3) / 1e9 if k_ms else 0.0
         hbm[k] = {"achieved": gbs, "frac": gbs / PEAK_HBM_GBS, "bytes_per_launch": nbytes}
+    copy_gbs = copy_reference_gbs()
+    hbm["copy_reference"] = {"achieved": copy_gbs, "frac": copy_gbs / PEAK_HBM_GBS,
+                             "bytes_per_launch": 2 * (1 << 30)}
     forms = {"explicit": 0, "factored": 0, "squared": 0}
     for l in range(len(shapes)):
         for side in (0, 1):

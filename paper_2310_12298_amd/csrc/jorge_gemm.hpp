@@ -160,48 +160,64 @@ __device__ __forceinline__ void fragment(const float* s, int mn, int k, float (&
 // epilogue of a symmetric result never reads the blocks left out.
 enum BlockSet : int { BS_ALL = 0, BS_UPPER = 1, BS_NONE = 2 };
 
-// The MFMAs of one LDS slab. Fragments of the next 16-wide k group are read
-// from LDS while the MFMAs of the current group run. The compiler's own
-// schedule spreads those reads and the other stage's loads among the MFMAs;
-// it measured 2-4% faster than a fixed interleave (which issued all loads
-// right after the first fragment reads).
-template <bool AK, bool BK, int BS, class Issue>
-__device__ __forceinline__ void mma_slab(const float* sa, const float* sb, int wy, int wx, int lane,
-                                         f32x4 (&acc)[16], Issue&& issue) {
-    if constexpr (BS == BS_NONE) {
-        issue();
-        return;
-    }
+// Fragments of one 16-wide k group of a slab for the calling wave: A rows
+// wy*64 + 16 i + (lane % 16) and B columns wx*64 + 16 i + (lane % 16), at k
+// = kg*16 + 4 quarter(lane / 16) .. + 3.
+template <bool AK, bool BK>
+__device__ __forceinline__ void group_fragments(const float* sa, const float* sb, int wy, int wx, int lane, int kg,
+                                                float (&a)[4][4], float (&b)[4][4]) {
     const int r = lane & 15, q = quarter(lane >> 4);
-    float a[2][4][4], b[2][4][4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        fragment<AK>(sa, wy * 64 + i * 16 + r, q * 4, a[0][i]);
-        fragment<BK>(sb, wx * 64 + i * 16 + r, q * 4, b[0][i]);
+        fragment<AK>(sa, wy * 64 + i * 16 + r, kg * 16 + q * 4, a[i]);
+        fragment<BK>(sb, wx * 64 + i * 16 + r, kg * 16 + q * 4, b[i]);
     }
-    // The loads of a later slab into the other stage (the compiler places
-    // them among this slab's MFMAs).
+}
+
+// The 64 MFMAs of one 16-wide k group (the blocks of block set BS).
+template <int BS>
+__device__ __forceinline__ void group_mma(const float (&a)[4][4], const float (&b)[4][4], f32x4 (&acc)[16]) {
+#pragma unroll
+    for (int st = 0; st < 4; ++st)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (BS == BS_ALL || i <= j)
+                    acc[i * 4 + j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i][st], b[j][st], acc[i * 4 + j], 0, 0, 0);
+}
+
+// The MFMAs of one LDS slab (sa, sb) of two 16-wide k groups, whose first
+// group's fragments the caller has already read into (fa, fb). The second
+// group's fragments are read while the first group's MFMAs run. Between the
+// two groups, `sync` makes the next slab (nsa, nsb) visible to every wave
+// (and ends every wave's reads of this slab); the next slab's first-group
+// fragments are then read into (fa, fb) while the second group's MFMAs run,
+// so neither the barrier nor that LDS latency leaves the matrix pipe idle.
+// `issue` starts the loads of a later slab into the stage that is free; the
+// compiler's own schedule spreads those loads and the LDS reads among the
+// MFMAs (it measured 2-4% faster than a fixed interleave).
+template <bool AK, bool BK, int BS, class Issue, class Sync>
+__device__ __forceinline__ void mma_slab(const float* sa, const float* sb, const float* nsa, const float* nsb, int wy,
+                                         int wx, int lane, float (&fa)[4][4], float (&fb)[4][4], f32x4 (&acc)[16],
+                                         Issue&& issue, Sync&& sync) {
+    static_assert(kSlab == 32, "a slab is two 16-wide k groups");
+    if constexpr (BS == BS_NONE) {
+        issue();
+        sync();
+        return;
+    }
+    float a[4][4], b[4][4];
+    group_fragments<AK, BK>(sa, sb, wy, wx, lane, 1, a, b);
+    // These reads too go first: the barrier in `sync` waits for them.
+    __builtin_amdgcn_sched_barrier(0);
     issue();
-#pragma unroll
-    for (int kg = 0; kg < kSlab / 16; ++kg) {
-        const int cur = kg & 1;
-        if (kg + 1 < kSlab / 16) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                fragment<AK>(sa, wy * 64 + i * 16 + r, (kg + 1) * 16 + q * 4, a[cur ^ 1][i]);
-                fragment<BK>(sb, wx * 64 + i * 16 + r, (kg + 1) * 16 + q * 4, b[cur ^ 1][i]);
-            }
-        }
-#pragma unroll
-        for (int st = 0; st < 4; ++st)
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    if (BS == BS_ALL || i <= j)
-                        acc[i * 4 + j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[cur][i][st], b[cur][j][st],
-                                                                              acc[i * 4 + j], 0, 0, 0);
-    }
+    group_mma<BS>(fa, fb, acc);
+    sync();
+    group_fragments<AK, BK>(nsa, nsb, wy, wx, lane, 0, fa, fb);
+    // Keep those reads ahead of the MFMAs (the scheduler would sink them).
+    __builtin_amdgcn_sched_barrier(0);
+    group_mma<BS>(a, b, acc);
 }
 
 // Sum of one double per lane over a 64-lane wave, in a fixed order.
@@ -271,42 +287,46 @@ __device__ __forceinline__ void issue_slab(const GemmProblem& p, const TileLanes
 template <bool BK>
 __device__ __forceinline__ void finish_slab(GemmStageLds& st, const f32x4 (&rb)[4]) {
     if constexpr (!BK) store_slab_mn(st.b, rb);
-    // This wave's loads to LDS have landed; the barrier makes every wave's visible.
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    // This wave's loads to LDS have landed and its reads of the other stage
+    // are complete; the barrier makes every wave's loads visible and lets the
+    // other stage be refilled.
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
     __syncthreads();
 }
 
 // The slab loop of gemm_mainloop for the calling wave's block set BS (one
-// copy per set, so the loop itself has no branches on it).
+// copy per set, so the loop itself has no branches on it). Slab 0 is in s0
+// and its first-group fragments in (fa, fb).
 template <bool AK, bool BK, int BS>
 __device__ __forceinline__ void slab_loop(const GemmProblem& p, const TileLanes& tl, int col0, int k0, int nk,
                                           GemmStageLds& s0, GemmStageLds& s1, f32x4 (&rb)[4], int wy, int wx,
-                                          int lane, f32x4 (&acc)[16]) {
+                                          int lane, float (&fa)[4][4], float (&fb)[4][4], f32x4 (&acc)[16]) {
+    // Raised issue priority while this wave runs its MFMAs (lowered around
+    // each barrier): the two waves sharing a SIMD then alternate between
+    // MFMA and memory phases.
+    auto sync_to = [&](GemmStageLds& st) {
+        __builtin_amdgcn_s_setprio(0);
+        finish_slab<BK>(st, rb);
+        __builtin_amdgcn_s_setprio(1);
+    };
     // Pairs of slabs: slab kt is in s0, kt+1 goes to s1 and kt+2 back to s0.
     // The loop has no other exit, so the accumulators stay in place.
     int kt = 0;
+    __builtin_amdgcn_s_setprio(1);
     for (; kt + 2 <= nk; kt += 2) {
-        // Raised issue priority while this wave runs its MFMAs: the two waves
-        // sharing a SIMD then alternate between MFMA and memory phases.
-        __builtin_amdgcn_s_setprio(1);
-        mma_slab<AK, BK, BS>(s0.a, s0.b, wy, wx, lane, acc,
-                             [&] { issue_slab<BK>(p, tl, col0, k0 + (kt + 1) * kSlab, s1, rb); });
-        __builtin_amdgcn_s_setprio(0);
-        finish_slab<BK>(s1, rb);
+        mma_slab<AK, BK, BS>(s0.a, s0.b, s1.a, s1.b, wy, wx, lane, fa, fb, acc,
+                             [&] { issue_slab<BK>(p, tl, col0, k0 + (kt + 1) * kSlab, s1, rb); },
+                             [&] { sync_to(s1); });
         // Past the last slab the load repeats slab nk - 1 into the idle stage
-        // (never read), which keeps the loop free of branches.
+        // (never multiplied), which keeps the loop free of branches.
         const int kn = min(kt + 2, nk - 1);
-        __builtin_amdgcn_s_setprio(1);
-        mma_slab<AK, BK, BS>(s1.a, s1.b, wy, wx, lane, acc,
-                             [&] { issue_slab<BK>(p, tl, col0, k0 + kn * kSlab, s0, rb); });
-        __builtin_amdgcn_s_setprio(0);
-        finish_slab<BK>(s0, rb);
+        mma_slab<AK, BK, BS>(s1.a, s1.b, s0.a, s0.b, wy, wx, lane, fa, fb, acc,
+                             [&] { issue_slab<BK>(p, tl, col0, k0 + kn * kSlab, s0, rb); },
+                             [&] { sync_to(s0); });
     }
-    if (kt < nk) {  // odd slab count: the last slab is in s0
-        __builtin_amdgcn_s_setprio(1);
-        mma_slab<AK, BK, BS>(s0.a, s0.b, wy, wx, lane, acc, [] {});
-        __builtin_amdgcn_s_setprio(0);
-    }
+    if (kt < nk)  // odd slab count: the last slab is in s0; nothing follows it
+        mma_slab<AK, BK, BS>(s0.a, s0.b, s1.a, s1.b, wy, wx, lane, fa, fb, acc, [] {}, [] {});
+    __builtin_amdgcn_s_setprio(0);
 }
 
 // The product of one 128 x 128 tile (tm, tn) of problem p over K range
@@ -337,14 +357,16 @@ __device__ __forceinline__ void gemm_mainloop(const GemmProblem& p, int tm, int 
     const int nk = (k1 - k0) / kSlab;
     issue_slab<BK>(p, tl, col0, k0, s0, rb);
     finish_slab<BK>(s0, rb);
+    float fa[4][4], fb[4][4];
+    group_fragments<AK, BK>(s0.a, s0.b, wy, wx, lane, 0, fa, fb);
     // On a diagonal tile of a symmetric result the quadrant below the
     // diagonal is not needed and the diagonal quadrants only on and above it.
     if (p.upper && tm == tn) {
-        if (wy > wx) slab_loop<AK, BK, BS_NONE>(p, tl, col0, k0, nk, s0, s1, rb, wy, wx, lane, acc);
-        else if (wy == wx) slab_loop<AK, BK, BS_UPPER>(p, tl, col0, k0, nk, s0, s1, rb, wy, wx, lane, acc);
-        else slab_loop<AK, BK, BS_ALL>(p, tl, col0, k0, nk, s0, s1, rb, wy, wx, lane, acc);
+        if (wy > wx) slab_loop<AK, BK, BS_NONE>(p, tl, col0, k0, nk, s0, s1, rb, wy, wx, lane, fa, fb, acc);
+        else if (wy == wx) slab_loop<AK, BK, BS_UPPER>(p, tl, col0, k0, nk, s0, s1, rb, wy, wx, lane, fa, fb, acc);
+        else slab_loop<AK, BK, BS_ALL>(p, tl, col0, k0, nk, s0, s1, rb, wy, wx, lane, fa, fb, acc);
     } else {
-        slab_loop<AK, BK, BS_ALL>(p, tl, col0, k0, nk, s0, s1, rb, wy, wx, lane, acc);
+        slab_loop<AK, BK, BS_ALL>(p, tl, col0, k0, nk, s0, s1, rb, wy, wx, lane, fa, fb, acc);
     }
     __syncthreads();  // every wave is done with both stages
 }
