@@ -170,7 +170,8 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time (0 = skip)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
-                    help="before timing, copy a buffer of this many MiB once (calibrates HBM byte counters)")
+                    help="before timing, copy a buffer of this many MiB once (calibrates HBM byte counters; "
+                         "skips the copy-rate reference)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -262,9 +263,10 @@ def main():
         k_ms = timing[k][0] / max(1, timing[k][1])
         gbs = nbytes / (k_ms * 1e-3) / 1e9 if k_ms else 0.0
         hbm[k] = {"achieved": gbs, "frac": gbs / PEAK_HBM_GBS, "bytes_per_launch": nbytes}
-    copy_gbs = copy_reference_gbs()
-    hbm["copy_reference"] = {"achieved": copy_gbs, "frac": copy_gbs / PEAK_HBM_GBS,
-                             "bytes_per_launch": 2 * (1 << 30)}
+    if args.copy_probe_mib == 0:  # counter runs identify their probe as the one large copy
+        copy_gbs = copy_reference_gbs()
+        hbm["copy_reference"] = {"achieved": copy_gbs, "frac": copy_gbs / PEAK_HBM_GBS,
+                                 "bytes_per_launch": 2 * (1 << 30)}
     forms = {"explicit": 0, "factored": 0, "squared": 0}
     for l in range(len(shapes)):
         for side in (0, 1):
