@@ -47,6 +47,12 @@ def stage_bytes(shapes):
             "stage_in": 20 * mn}     # read G, write Gp and its transpose, read and write m_SGD
 
 
+def step_bytes(shapes, update):
+    """Algorithmic HBM bytes of one step: read G, theta, m, m_SGD and the factors,
+    write theta, m, m_SGD and (on factor-updating steps) the factors."""
+    return sum(4 * (7 * m * n + (2 if update else 1) * (m * m + n * n)) for m, n in shapes)
+
+
 # Committed rocprofv3 summaries that carry HBM counter figures for a workload.
 PROFILES = {"resnet50": os.path.join(ROOT, "profiles", "gemm_grouped_resnet50.md")}
 
@@ -267,6 +273,12 @@ def main():
         copy_gbs = copy_reference_gbs()
         hbm["copy_reference"] = {"achieved": copy_gbs, "frac": copy_gbs / PEAK_HBM_GBS,
                                  "bytes_per_launch": 2 * (1 << 30)}
+    step_f = g_flops / steps
+    step_b = (step_bytes(shapes, True) * updates + step_bytes(shapes, False) * (steps - updates)) / steps
+    t_mfma, t_hbm = step_f / (PEAK_FP32_MFMA_TFLOPS * 1e12), step_b / (PEAK_HBM_GBS * 1e9)
+    step_roof = {"flops": step_f, "bytes": step_b, "t_mfma_ms": t_mfma * 1e3, "t_hbm_ms": t_hbm * 1e3,
+                 "bound": "mfma" if t_mfma >= t_hbm else "hbm",
+                 "frac": max(t_mfma, t_hbm) / (total_ms / steps * 1e-3)}
     forms = {"explicit": 0, "factored": 0, "squared": 0}
     for l in range(len(shapes)):
         for side in (0, 1):
@@ -297,6 +309,10 @@ def main():
                      "traffic_hbm_frac": traffic_gbs / PEAK_HBM_GBS if traffic_gbs else None,
                      "launches": g_launches, "ms_per_launch": ms_launch,
                      "gflop_per_launch": g_flops / max(1, g_launches) / 1e9},
+        # The whole step against its own roofline: the executed algorithmic flops at the
+        # fp32 MFMA peak and the algorithmic bytes at the HBM peak, the larger of the two
+        # over the measured step time.
+        "step_roofline": step_roof,
         # executed algorithmic flops of the whole step / (step time x fp32 MFMA peak)
         "mfma_util_pct": 100.0 * g_flops / steps / (inst_ms / steps * 1e-3) / (PEAK_FP32_MFMA_TFLOPS * 1e12),
         # the same step's flops counted in the paper's explicit order, per second of step time
