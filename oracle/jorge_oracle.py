@@ -114,7 +114,7 @@ def beta_select(nu: float, beta2: float, mode: int) -> tuple[float, float, float
 
 def update_factor(A_hat: np.ndarray, M: np.ndarray, beta2: float,
                   mode: int = BETA_CLAMPED, symmetrize: bool = True, series_order: int = 2):
-    """One preconditioner update of Algorithm 2 (lines 5-6 for L, 7-8 for R).
+    """One preconditioner update of Algorithm 2 (the same form for L_hat and R_hat).
 
     A_hat is the previous factor (L_hat or R_hat), M the matching statistic
     (G G^T or G^T G). series_order is the last power of X kept from the
@@ -128,10 +128,10 @@ def update_factor(A_hat: np.ndarray, M: np.ndarray, beta2: float,
     d = A_hat.shape[0]
     A2 = A_hat @ A_hat
     A4 = A2 @ A2
-    X = A4 @ M                                   # X = A_hat^4 G G^T (line 5)
+    X = A4 @ M                                   # X = A_hat^4 G G^T (Algorithm 2)
     nu = float(np.sqrt(np.sum(X * X)))           # Frobenius norm (Appendix A.1)
     c, s, beta_eff = beta_select(nu, beta2, mode)
-    # Truncated series of (I + c X)^(-1/4) (Eq. 6-7, line 6)
+    # Truncated series of (I + c X)^(-1/4) (Eq. 6-7, Algorithm 2's factor update)
     X2 = X @ X
     P = np.eye(d) + SERIES_C1 * c * X + SERIES_C2 * (c * c) * X2
     if series_order == 3:                        # the next term of Eq. 5
@@ -143,17 +143,17 @@ def update_factor(A_hat: np.ndarray, M: np.ndarray, beta2: float,
 
 
 def precondition(L_hat: np.ndarray, G: np.ndarray, R_hat: np.ndarray) -> np.ndarray:
-    """G_tilde = L_hat G R_hat (Algorithm 2, line 11), evaluated as (L_hat G) R_hat."""
+    """G_tilde = L_hat G R_hat (Algorithm 2's preconditioned gradient), evaluated as (L_hat G) R_hat."""
     return (L_hat @ np.asarray(G, dtype=np.float64)) @ R_hat
 
 
 def update_weights(theta, m, m_sgd, G_tilde, G, lr, beta1, weight_decay, graft=True):
     """Momentum, SGD grafting and decoupled weight decay.
 
-    m = beta1 m + (1-beta1) G_tilde (Algorithm 2 line 14, Algorithm 3 line 2);
-    m_SGD = beta1 m_SGD + G (Algorithm 3 line 3);
+    m = beta1 m + (1-beta1) G_tilde (the momentum of Algorithms 2 and 3);
+    m_SGD = beta1 m_SGD + G (Algorithm 3's SGD momentum);
     theta = theta (1 - lr wd) - g m with g = lr ||m_SGD|| / ||m|| when grafting
-    (Algorithm 3 line 5, Section 4's decoupled weight decay), g = lr otherwise.
+    (Algorithm 3's grafted step, Section 4's decoupled weight decay), g = lr otherwise.
     """
     G = np.asarray(G, dtype=np.float64)
     m = beta1 * m + (1.0 - beta1) * G_tilde
