@@ -319,9 +319,11 @@ int tile_count(int M, int N) { return (int)(tiles_of(M) * tiles_of(N)); }
 
 
 // Puts work units in dispatch order. The units are sorted by K, longest
-// first; each problem's tiles stay in bands of kGroupRows tile rows walked
-// column by column. Runs of consecutive units of one problem, one column and
-// one K range (they share the B panel and neighbouring A panels) are dealt,
+// first, and then by problem and by the start of their K range (the pieces of
+// split tiles that cover one K range stay together); each problem's tiles
+// stay in bands of kGroupRows tile rows walked column by column. Runs of
+// consecutive units of one problem, one column and one K range (they share
+// the B panel and neighbouring A panels) are dealt,
 // in that order, to the XCD with the least accumulated work (K of the unit),
 // so every XCD gets a balanced, largest-first share whose units reuse panels
 // in its own L2. The shares are then interleaved so that XCD x's i-th unit
@@ -330,9 +332,21 @@ int tile_count(int M, int N) { return (int)(tiles_of(M) * tiles_of(N)); }
 void order_for_xcds(std::vector<TileDesc>& tiles) {
     const size_t n = tiles.size();
     if (n == 0) return;
-    // Longest K range first (stable: each problem's tiles stay together and in order).
+    // Longest K range first; within one length, by problem (in list order)
+    // and then by the start of the K range, so the pieces of split tiles that
+    // share a K range stay together (stable: tile order is kept otherwise).
+    std::vector<int> first_of;
+    {
+        int mx = 0;
+        for (const TileDesc& t : tiles) mx = std::max(mx, t.prob);
+        first_of.assign(mx + 1, INT32_MAX);
+        for (size_t i = 0; i < n; ++i) first_of[tiles[i].prob] = std::min(first_of[tiles[i].prob], (int)i);
+    }
     std::stable_sort(tiles.begin(), tiles.end(), [&](const TileDesc& a, const TileDesc& b) {
-        return a.k1 - a.k0 > b.k1 - b.k0;
+        const int la = a.k1 - a.k0, lb = b.k1 - b.k0;
+        if (la != lb) return la > lb;
+        if (first_of[a.prob] != first_of[b.prob]) return first_of[a.prob] < first_of[b.prob];
+        return a.k0 < b.k0;
     });
     std::vector<std::vector<TileDesc>> share(kXcds);
     std::vector<int64_t> work(kXcds, 0);
