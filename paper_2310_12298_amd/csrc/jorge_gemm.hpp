@@ -331,8 +331,10 @@ __device__ __forceinline__ void slab_loop(const GemmProblem& p, const TileLanes&
 
 // The product of one 128 x 128 tile (tm, tn) of problem p over K range
 // [k0, k1), accumulated by the whole workgroup into acc. Every thread of the
-// workgroup must call it; it leaves LDS free for reuse. The slab loop is
-// unrolled by two so each half reads one stage and fills the other.
+// workgroup must call it. Waves return without waiting for each other, so
+// LDS may be written after it only behind a barrier (the grouped kernel
+// writes none). The slab loop is unrolled by two so each half reads one stage
+// and fills the other.
 template <bool AK, bool BK>
 __device__ __forceinline__ void gemm_mainloop(const GemmProblem& p, int tm, int tn, int k0, int k1,
                                               GemmStageLds& s0, GemmStageLds& s1, f32x4 (&acc)[16]) {
@@ -368,7 +370,9 @@ __device__ __forceinline__ void gemm_mainloop(const GemmProblem& p, int tm, int 
     } else {
         slab_loop<AK, BK, BS_ALL>(p, tl, col0, k0, nk, s0, s1, rb, wy, wx, lane, fa, fb, acc);
     }
-    __syncthreads();  // every wave is done with both stages
+    // No closing barrier: every load into LDS has landed (the last slab's
+    // wait), and nothing after the main loop writes LDS, so each wave goes on
+    // to its epilogue as soon as its own MFMAs are issued.
 }
 
 // Partial products of split tiles: thread t (= 64 wave + lane) keeps its 64
