@@ -7,7 +7,9 @@ updated every step (interval 1). Inputs are synthetic, seeded and resident in
 HBM before the timed region. The K timed steps run twice: once with only
 the two bracketing events (steps/s), once with HIP events around every launch
 on the library's streams (per-stage times and the roofline of the grouped
-GEMM). Prints one JSON line.
+GEMM). Prints one JSON line; with --others 1 (the default) it also times the
+other four workloads, each for its stated number of steps, and reports them
+in the line's "other_workloads" record.
 """
 import argparse
 import json
@@ -160,59 +162,57 @@ def cpu_baseline(shapes, sigma, seed, budget_s, series_order=2):
                       f"scaled by flop share"}
 
 
-def main():
-    ap = argparse.ArgumentParser(description=__doc__)
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=None, help="timed steps (default: the workload's run)")
-    ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", default="resnet50", choices=sorted(WORKLOAD_NAMES))
-    ap.add_argument("--interval", type=int, default=1, help="preconditioner update interval k")
-    ap.add_argument("--form", default="auto", choices=("auto", "explicit", "factored", "squared"),
-                    help="evaluation order of the factor updates")
-    ap.add_argument("--split-k", type=int, default=1, choices=(0, 1),
-                    help="split the K range of long tiles in levels with too few tiles")
-    ap.add_argument("--series-order", type=int, default=2, choices=(2, 3),
-                    help="last power of X kept from the binomial series (Section 3 keeps 2)")
-    ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time (0 = skip)")
-    ap.add_argument("--copy-probe-mib", type=int, default=0,
-                    help="before timing, copy a buffer of this many MiB once (calibrates HBM byte counters; "
-                         "skips the copy-rate reference)")
-    args = ap.parse_args()
-    world = int(os.environ.get("WORLD_SIZE", "1"))
-    if args.gpus != 1 or world != 1:
-        print(f"bench.py runs on exactly one GPU (asked for {max(args.gpus, world)}): the Jorge step is "
-              f"replicated per data-parallel rank and this build measures one GPU's step.", file=sys.stderr)
-        return 2
+FLOP_BASIS = ("executed: the algorithmic flops of the products the step runs, each factor in the evaluation "
+              "order the library chose for it (explicit, factored or squared, with low-rank preconditioning), "
+              "symmetric products counted once, over unpadded extents (jorge_stage_flops)")
+PAPER_ORDER_NOTE = ("an effective rate, not a utilisation: the step counted in the paper's explicit order "
+                    "(8m^3 + 8n^3 + 3m^2n + 3mn^2 per layer) per second of step time; it can exceed the peak "
+                    "because the factored and squared orders need fewer flops for the same factors")
 
+
+def cpu_info():
+    model = None
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"os_cpu_count": os.cpu_count(), "cpu_model": model}
+
+
+def measure(config, steps, warmup, interval=1, form="auto", split_k=1, series_order=2, seed=0,
+            copy_probe_mib=0):
+    """Times one workload: W warm-up steps, then K steps twice (clean, then with per-launch events)."""
     import torch
 
     from paper_2310_12298_amd.jorge import Jorge
     from paper_2310_12298_amd.workloads import CONFIGS, DEFAULT_HPARAMS, device_gradient, device_initial_params
 
-    torch.cuda.set_device(0)
-    shapes, sigma, run_steps = CONFIGS[args.config]
-    steps = args.steps if args.steps is not None else run_steps
+    shapes, sigma, run_steps = CONFIGS[config]
+    steps = steps if steps is not None else run_steps
     hp = DEFAULT_HPARAMS
-    opt = Jorge(shapes, eps=hp["eps"], precond_interval=args.interval, factor_form=args.form,
-                split_k=bool(args.split_k), series_order=args.series_order)
-    params = [device_initial_params(args.seed, l, s) for l, s in enumerate(shapes)]
-    grads = [[device_gradient(args.seed, l, t, s, sigma) for l, s in enumerate(shapes)]
-             for t in range(1, args.warmup + steps + 1)]
+    opt = Jorge(shapes, eps=hp["eps"], precond_interval=interval, factor_form=form,
+                split_k=bool(split_k), series_order=series_order)
+    params = [device_initial_params(seed, l, s) for l, s in enumerate(shapes)]
+    grads = [[device_gradient(seed, l, t, s, sigma) for l, s in enumerate(shapes)]
+             for t in range(1, warmup + steps + 1)]
     pp = Jorge.pointer_array(params)
     gp = [Jorge.pointer_array(g) for g in grads]
 
     def step(i):
         opt.step_ptrs(pp, gp[i], hp["lr"], hp["beta2"], hp["beta1"], hp["weight_decay"])
 
-    if args.copy_probe_mib > 0:
-        n = args.copy_probe_mib * (1 << 20) // 4
+    if copy_probe_mib > 0:
+        n = copy_probe_mib * (1 << 20) // 4
         src = torch.ones(n, dtype=torch.float32, device="cuda")
         dst = torch.empty_like(src)
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
-    for i in range(args.warmup):
+    for i in range(warmup):
         step(i)
     torch.cuda.synchronize()
 
@@ -225,14 +225,14 @@ def main():
         torch.cuda.synchronize()
         start.record()
         for i in range(steps):
-            step(args.warmup + i)
+            step(warmup + i)
         stop.record()
         torch.cuda.synchronize()
         ms = start.elapsed_time(stop)
         timing = opt.read_timing()
         opt.set_timing(False)
         # factor-updating steps among this pass's step numbers t0+1 .. t0+steps
-        upd = sum(1 for t in range(t0 + 1, t0 + steps + 1) if (t - 1) % args.interval == 0)
+        upd = sum(1 for t in range(t0 + 1, t0 + steps + 1) if (t - 1) % interval == 0)
         return ms, timing, upd
 
     # Throughput from a pass without per-launch events (they add gaps between
@@ -242,8 +242,7 @@ def main():
     inst_ms, timing, updates = timed(True)
     for t in params:
         if not torch.isfinite(t).all():
-            raise RuntimeError("non-finite parameters after the timed steps")
-
+            raise RuntimeError(f"{config}: non-finite parameters after the timed steps")
     if updates == 0:
         raise SystemExit("no factor update in the timed steps; use more steps or a smaller interval")
     # Algorithmic flops of each stage in one factor-updating step, from the library's launch tables.
@@ -259,39 +258,103 @@ def main():
     g_flops = sum(flops[k] * ran[k] for k in GEMM_STAGES)
     g_ms = sum(timing[k][0] for k in GEMM_STAGES) + timing[FIXUP_STAGE][0]
     g_launches = sum(timing[k][1] for k in GEMM_STAGES)
-    achieved = g_flops / (g_ms * 1e-3) / 1e12
-    traffic = measured_traffic(args.config)
+    achieved = g_flops / (g_ms * 1e-3) / 1e12 if g_ms > 0 else 0.0
     ms_launch = g_ms / max(1, g_launches)
-    traffic_gbs = traffic / (ms_launch * 1e-3) / 1e9 if traffic and ms_launch else None
     f_paper = sum(falg_paper(m, n) for m, n in shapes) * updates_clean / steps
     hbm = {}  # the bandwidth-bound kernels: algorithmic bytes / average launch time
     for k, nbytes in stage_bytes(shapes).items():
         k_ms = timing[k][0] / max(1, timing[k][1])
         gbs = nbytes / (k_ms * 1e-3) / 1e9 if k_ms else 0.0
         hbm[k] = {"achieved": gbs, "frac": gbs / PEAK_HBM_GBS, "bytes_per_launch": nbytes}
-    if args.copy_probe_mib == 0:  # counter runs identify their probe as the one large copy
-        copy_gbs = copy_reference_gbs()
-        hbm["copy_reference"] = {"achieved": copy_gbs, "frac": copy_gbs / PEAK_HBM_GBS,
-                                 "bytes_per_launch": 2 * (1 << 30)}
     step_f = g_flops / steps
     step_b = (step_bytes(shapes, True) * updates + step_bytes(shapes, False) * (steps - updates)) / steps
     t_mfma, t_hbm = step_f / (PEAK_FP32_MFMA_TFLOPS * 1e12), step_b / (PEAK_HBM_GBS * 1e9)
     step_roof = {"flops": step_f, "bytes": step_b, "t_mfma_ms": t_mfma * 1e3, "t_hbm_ms": t_hbm * 1e3,
                  "bound": "mfma" if t_mfma >= t_hbm else "hbm",
-                 "frac": max(t_mfma, t_hbm) / (total_ms / steps * 1e-3)}
+                 "frac": max(t_mfma, t_hbm) / (total_ms / steps * 1e-3), "flop_basis": "executed (as roofline)"}
     forms = {"explicit": 0, "factored": 0, "squared": 0}
     for l in range(len(shapes)):
         for side in (0, 1):
             forms[opt.factor_form(l, side)] += 1
+    res = {
+        "config": config, "shapes": shapes, "sigma": sigma, "steps": steps, "updates": updates,
+        "value": steps / (total_ms * 1e-3), "ms_per_step": total_ms / steps,
+        "ms_per_step_instrumented": inst_ms / steps, "forms": forms,
+        "gemm": {"achieved": achieved, "ms_per_launch": ms_launch, "launches": g_launches,
+                 "gflop_per_launch": g_flops / max(1, g_launches) / 1e9},
+        "step_roofline": step_roof,
+        "mfma_util_pct": 100.0 * step_f / (inst_ms / steps * 1e-3) / (PEAK_FP32_MFMA_TFLOPS * 1e12),
+        "paper_order": {"flops_per_step": f_paper, "effective_tflops": f_paper / (total_ms / steps * 1e-3) / 1e12,
+                        "note": PAPER_ORDER_NOTE},
+        "hbm": hbm, "stages": per_stage,
+    }
+    del opt, params, grads, pp, gp
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return res
+
+
+def summary(res):
+    """The sub-record of a workload measured beside the headline one."""
+    return {"workload": WORKLOAD_NAMES[res["config"]], "steps": res["steps"], "value": res["value"], "unit": "steps/s",
+            "ms_per_step": res["ms_per_step"], "gemm_frac": res["gemm"]["achieved"] / PEAK_FP32_MFMA_TFLOPS,
+            "gemm_tflops": res["gemm"]["achieved"], "step_roofline_frac": res["step_roofline"]["frac"],
+            "step_roofline_bound": res["step_roofline"]["bound"], "factors": res["forms"],
+            "traffic_bytes_per_launch": measured_traffic(res["config"])}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=None, help="timed steps (default: the workload's run)")
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="resnet50", choices=sorted(WORKLOAD_NAMES))
+    ap.add_argument("--interval", type=int, default=1, help="preconditioner update interval k")
+    ap.add_argument("--form", default="auto", choices=("auto", "explicit", "factored", "squared"),
+                    help="evaluation order of the factor updates")
+    ap.add_argument("--split-k", type=int, default=1, choices=(0, 1),
+                    help="split the K range of long tiles in levels with too few tiles")
+    ap.add_argument("--series-order", type=int, default=2, choices=(2, 3),
+                    help="last power of X kept from the binomial series (Section 3 keeps 2)")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time (0 = skip)")
+    ap.add_argument("--others", type=int, default=1, choices=(0, 1),
+                    help="also time the other four workloads, each for its stated number of steps, and report "
+                         "them in the same line (with the default interval, order and options)")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="before timing, copy a buffer of this many MiB once (calibrates HBM byte counters; "
+                         "skips the copy-rate reference and the other workloads)")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py runs on exactly one GPU (asked for {max(args.gpus, world)}): the Jorge step is "
+              f"replicated per data-parallel rank and this build measures one GPU's step.", file=sys.stderr)
+        return 2
+
+    import torch
+
+    torch.cuda.set_device(0)
+    res = measure(args.config, args.steps, args.warmup, args.interval, args.form, args.split_k, args.series_order,
+                  args.seed, args.copy_probe_mib)
+    shapes, steps = res["shapes"], res["steps"]
+    traffic = measured_traffic(args.config)
+    ms_launch = res["gemm"]["ms_per_launch"]
+    traffic_gbs = traffic / (ms_launch * 1e-3) / 1e9 if traffic and ms_launch else None
+    hbm = dict(res["hbm"])
+    if args.copy_probe_mib == 0:  # counter runs identify their probe as the one large copy
+        copy_gbs = copy_reference_gbs()
+        hbm["copy_reference"] = {"achieved": copy_gbs, "frac": copy_gbs / PEAK_HBM_GBS,
+                                 "bytes_per_launch": 2 * (1 << 30)}
+    achieved = res["gemm"]["achieved"]
     out = {
         "metric": METRIC,
-        "value": steps / (total_ms * 1e-3),
+        "value": res["value"],
         "unit": "steps/s",
         "n_gpus": 1,
         "steps": steps,
         "warmup": args.warmup,
-        "ms_per_step": total_ms / steps,
-        "ms_per_step_instrumented": inst_ms / steps,
+        "ms_per_step": res["ms_per_step"],
+        "ms_per_step_instrumented": res["ms_per_step_instrumented"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -299,29 +362,33 @@ def main():
         "data": "synthetic",
         "config": {"workload": WORKLOAD_NAMES[args.config], "name": args.config, "layers": len(shapes),
                    "params": sum(m * n for m, n in shapes), "precond_interval": args.interval,
-                   "factor_updates": updates, "factor_form": args.form, "factors": forms, "split_k": args.split_k,
-                   "series_order": args.series_order, "seed": args.seed},
+                   "factor_updates": res["updates"], "factor_form": args.form, "factors": res["forms"],
+                   "split_k": args.split_k, "series_order": args.series_order, "seed": args.seed},
         "roofline": {"bound": "mfma", "kernel": "gemm_grouped<true, true> (every GEMM stage of the step)",
                      "achieved": achieved, "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / PEAK_FP32_MFMA_TFLOPS, "traffic": traffic, "traffic_unit": "HBM bytes per launch",
+                     "frac": achieved / PEAK_FP32_MFMA_TFLOPS, "flop_basis": FLOP_BASIS,
+                     "traffic": traffic, "traffic_unit": "HBM bytes per launch",
                      # the measured traffic over the launch time: how far the kernel is from the HBM roof
                      "traffic_gbs": traffic_gbs,
                      "traffic_hbm_frac": traffic_gbs / PEAK_HBM_GBS if traffic_gbs else None,
-                     "launches": g_launches, "ms_per_launch": ms_launch,
-                     "gflop_per_launch": g_flops / max(1, g_launches) / 1e9},
+                     "launches": res["gemm"]["launches"], "ms_per_launch": ms_launch,
+                     "gflop_per_launch": res["gemm"]["gflop_per_launch"]},
         # The whole step against its own roofline: the executed algorithmic flops at the
         # fp32 MFMA peak and the algorithmic bytes at the HBM peak, the larger of the two
         # over the measured step time.
-        "step_roofline": step_roof,
-        # executed algorithmic flops of the whole step / (step time x fp32 MFMA peak)
-        "mfma_util_pct": 100.0 * g_flops / steps / (inst_ms / steps * 1e-3) / (PEAK_FP32_MFMA_TFLOPS * 1e12),
-        # the same step's flops counted in the paper's explicit order, per second of step time
-        "paper_order_tflops": f_paper / (total_ms / steps * 1e-3) / 1e12,
+        "step_roofline": res["step_roofline"],
+        # executed algorithmic flops of the whole step / (instrumented step time x fp32 MFMA peak)
+        "mfma_util_pct": res["mfma_util_pct"],
+        "paper_order": res["paper_order"],
         "hbm": dict(hbm, peak=PEAK_HBM_GBS, unit="GB/s"),
-        "stages": per_stage,
+        "stages": res["stages"],
     }
+    if args.others and args.copy_probe_mib == 0:
+        out["other_workloads"] = {c: summary(measure(c, None, args.warmup, seed=args.seed))
+                                  for c in WORKLOAD_NAMES if c != args.config}
     if args.cpu_budget > 0:
-        out["cpu_baseline"] = cpu_baseline(shapes, sigma, args.seed, args.cpu_budget, args.series_order)
+        out["cpu_baseline"] = dict(cpu_baseline(shapes, res["sigma"], args.seed, args.cpu_budget,
+                                                args.series_order), **cpu_info())
     print(json.dumps(out), flush=True)
     return 0
 

@@ -16,6 +16,20 @@
  * does not synchronise the host unless the comment says so. Arguments are
  * validated before any HIP call; an invalid call changes no state.
  *
+ * A HIP error part-way through jorge_step is different: kernels queued before
+ * it have run, so some state tensors (m_SGD, factors, momentum, parameters)
+ * may hold the new step's values and others the old ones, and the step
+ * counter has not advanced. The call returns JORGE_ERR_HIP and the context is
+ * poisoned: every later jorge_step returns JORGE_ERR_HIP without queueing
+ * anything, until the caller has restored the state from a checkpoint
+ * (jorge_set_state for every tensor, the parameters by itself) and calls
+ * jorge_set_step.
+ *
+ * The interface takes the step's scalars (lr, beta2, beta1, weight_decay) per
+ * call, as doubles: they may change every step (a learning-rate schedule), and
+ * the scalar arithmetic they enter runs in fp64 on the device. The options
+ * fixed at creation (jorge_hparams) therefore carry none of them.
+ *
  * A context is not re-entrant: calls on one context must not overlap.
  * Distinct contexts are independent.
  */
@@ -205,20 +219,30 @@ jorge_status jorge_set_state(jorge_ctx* ctx, int32_t layer, int32_t kind, const 
                              int64_t ld_src);
 
 /* Lends the device pointer of one state tensor and its row stride in floats
- * (factors are stored with rows padded to a multiple of 32, zero outside the
- * valid block). Valid until jorge_destroy. */
+ * (*ld: factors are stored with rows padded to a multiple of 32, zero outside
+ * the valid block, so a caller that reads or writes them in place needs the
+ * stride). Valid until jorge_destroy. */
 jorge_status jorge_state_ptr(jorge_ctx* ctx, int32_t layer, int32_t kind, float** dev_ptr,
                              int64_t* ld);
 
-/* Step counter: the number of steps taken (0 after create). */
+/* Step counter: the number of steps taken (0 after create). jorge_set_step
+ * (t >= 0) also lifts the refusal that follows a step failed part-way (see the
+ * top of this file): call it once the state has been restored. */
 jorge_status jorge_get_step(const jorge_ctx* ctx, int64_t* t);
-jorge_status jorge_set_step(jorge_ctx* ctx, int64_t t);            /* t >= 0 */
+jorge_status jorge_set_step(jorge_ctx* ctx, int64_t t);
 
 /* Diagnostics of the last step for one layer: out[JORGE_DIAG_COUNT] on the
  * host. Synchronises the context's stream. */
 jorge_status jorge_read_diag(jorge_ctx* ctx, int32_t layer, double* out);
 
-/* Changes the stream later calls queue on (NULL = the null stream). */
+/* Changes the stream later calls queue on (NULL = the null stream). Work
+ * queued later on the new stream waits for everything already queued on the
+ * old one (an event recorded on the old stream, waited on by the new one), so
+ * the switch needs no synchronisation by the caller; jorge_synchronize and
+ * jorge_destroy then cover the old stream's work too. Exception: when either
+ * stream is being captured into a graph, no such wait is queued (a capture
+ * cannot wait on an event recorded outside it); the capture's owner orders
+ * the two streams. */
 jorge_status jorge_set_stream(jorge_ctx* ctx, void* hip_stream);
 
 /* Waits for all work queued by the context. */

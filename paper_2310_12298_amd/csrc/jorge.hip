@@ -181,6 +181,10 @@ struct jorge_ctx {
     double stage_ms[ST_COUNT] = {};
     int64_t stage_launches[ST_COUNT] = {};
     std::string last_error;
+    hipEvent_t order_event = nullptr;  // orders a stream switch (jorge_set_stream)
+    // A step failed after its first launch: part of the state may be updated
+    // and part not. Further steps are refused until jorge_set_step.
+    bool poisoned = false;
 };
 
 namespace {
@@ -1351,6 +1355,7 @@ void free_ctx(jorge_ctx* c) {
         (void)hipEventDestroy(l.stop);
     }
     for (auto e : c->free_events) (void)hipEventDestroy(e);
+    if (c->order_event) (void)hipEventDestroy(c->order_event);
     delete c;
 }
 
@@ -1389,6 +1394,48 @@ jorge_status run_update(jorge_ctx* c, double beta2) {
     }
     return JORGE_OK;
 }
+
+// The launches of step t (everything jorge_step queues after validating).
+jorge_status launch_step(jorge_ctx* c, float* const* params, const float* const* grads, int64_t t, double lr,
+                         double beta2, double beta1, double weight_decay) {
+    const int nl = (int)c->layers.size();
+    const bool update = (t - 1) % c->hp.precond_interval == 0;
+    const int nbatch = (nl + kPtrBatch - 1) / kPtrBatch;
+    for (int b = 0; b < nbatch; ++b) {
+        PtrBatch pb{};
+        for (int i = b * kPtrBatch; i < std::min(nl, (b + 1) * kPtrBatch); ++i) pb.p[i - b * kPtrBatch] = grads[i];
+        const int c0 = c->stage_batch_start[b], c1 = c->stage_batch_start[b + 1];
+        TimedLaunch tl(c, ST_STAGEIN);
+        hipLaunchKernelGGL(stagein_kernel, dim3(c1 - c0), dim3(kEwThreads), 0, c->stream, c->dlayers,
+                           c->dstage + c0, b * kPtrBatch, pb, (float)beta1);
+        tl.finish();
+        JORGE_HIP(c, hipGetLastError());
+    }
+    jorge_status s;
+    if (update && (s = run_update(c, beta2)) != JORGE_OK) return s;
+    // Update steps take the preconditioning tables that reuse the update's low-rank terms.
+    if ((s = launch_stage(c, update ? ST_UPRECOND_L : ST_PRECOND_L, 0.f)) != JORGE_OK) return s;
+    if ((s = launch_stage(c, update ? ST_UPRECOND_R : ST_PRECOND_R, (float)beta1)) != JORGE_OK) return s;
+    {
+        TimedLaunch tl(c, ST_LFINAL);
+        hipLaunchKernelGGL(layer_finalize_kernel, dim3(nl), dim3(64), 0, c->stream, c->dlayers, lr,
+                           weight_decay, (int)c->hp.graft);
+        tl.finish();
+        JORGE_HIP(c, hipGetLastError());
+    }
+    for (int b = 0; b < nbatch; ++b) {
+        MutPtrBatch pb{};
+        for (int i = b * kPtrBatch; i < std::min(nl, (b + 1) * kPtrBatch); ++i) pb.p[i - b * kPtrBatch] = params[i];
+        const int c0 = c->flat_batch_start[b], c1 = c->flat_batch_start[b + 1];
+        TimedLaunch tl(c, ST_WEIGHT);
+        hipLaunchKernelGGL(weight_kernel, dim3(c1 - c0), dim3(kEwThreads), 0, c->stream, c->dlayers,
+                           c->dflat + c0, b * kPtrBatch, pb);
+        tl.finish();
+        JORGE_HIP(c, hipGetLastError());
+    }
+    return JORGE_OK;
+}
+
 
 bool valid_kind(const jorge_ctx* c, int32_t layer, int32_t kind) {
     return c && layer >= 0 && layer < (int32_t)c->layers.size() && kind >= JORGE_STATE_L &&
@@ -1537,40 +1584,15 @@ jorge_status jorge_step(jorge_ctx* c, float* const* params, const float* const* 
     const int nl = (int)c->layers.size();
     for (int i = 0; i < nl; ++i)
         if (!params[i] || !grads[i]) return fail(c, JORGE_ERR_INVALID_ARGUMENT, "jorge_step: null tensor");
+    if (c->poisoned)
+        return fail(c, JORGE_ERR_HIP,
+                    "jorge_step: an earlier step failed part-way; restore the state (jorge_set_state) and "
+                    "the step counter (jorge_set_step) first");
     const int64_t t = c->t + 1;
-    const bool update = (t - 1) % c->hp.precond_interval == 0;
-    const int nbatch = (nl + kPtrBatch - 1) / kPtrBatch;
-    for (int b = 0; b < nbatch; ++b) {
-        PtrBatch pb{};
-        for (int i = b * kPtrBatch; i < std::min(nl, (b + 1) * kPtrBatch); ++i) pb.p[i - b * kPtrBatch] = grads[i];
-        const int c0 = c->stage_batch_start[b], c1 = c->stage_batch_start[b + 1];
-        TimedLaunch tl(c, ST_STAGEIN);
-        hipLaunchKernelGGL(stagein_kernel, dim3(c1 - c0), dim3(kEwThreads), 0, c->stream, c->dlayers,
-                           c->dstage + c0, b * kPtrBatch, pb, (float)beta1);
-        tl.finish();
-        JORGE_HIP(c, hipGetLastError());
-    }
-    jorge_status s;
-    if (update && (s = run_update(c, beta2)) != JORGE_OK) return s;
-    // Update steps take the preconditioning tables that reuse the update's low-rank terms.
-    if ((s = launch_stage(c, update ? ST_UPRECOND_L : ST_PRECOND_L, 0.f)) != JORGE_OK) return s;
-    if ((s = launch_stage(c, update ? ST_UPRECOND_R : ST_PRECOND_R, (float)beta1)) != JORGE_OK) return s;
-    {
-        TimedLaunch tl(c, ST_LFINAL);
-        hipLaunchKernelGGL(layer_finalize_kernel, dim3(nl), dim3(64), 0, c->stream, c->dlayers, lr,
-                           weight_decay, (int)c->hp.graft);
-        tl.finish();
-        JORGE_HIP(c, hipGetLastError());
-    }
-    for (int b = 0; b < nbatch; ++b) {
-        MutPtrBatch pb{};
-        for (int i = b * kPtrBatch; i < std::min(nl, (b + 1) * kPtrBatch); ++i) pb.p[i - b * kPtrBatch] = params[i];
-        const int c0 = c->flat_batch_start[b], c1 = c->flat_batch_start[b + 1];
-        TimedLaunch tl(c, ST_WEIGHT);
-        hipLaunchKernelGGL(weight_kernel, dim3(c1 - c0), dim3(kEwThreads), 0, c->stream, c->dlayers,
-                           c->dflat + c0, b * kPtrBatch, pb);
-        tl.finish();
-        JORGE_HIP(c, hipGetLastError());
+    const jorge_status s = launch_step(c, params, grads, t, lr, beta2, beta1, weight_decay);
+    if (s != JORGE_OK) {
+        c->poisoned = true;
+        return s;
     }
     c->t = t;
     return JORGE_OK;
@@ -1614,6 +1636,7 @@ jorge_status jorge_get_step(const jorge_ctx* c, int64_t* t) {
 jorge_status jorge_set_step(jorge_ctx* c, int64_t t) {
     if (!c || t < 0) return JORGE_ERR_INVALID_ARGUMENT;
     c->t = t;
+    c->poisoned = false;
     return JORGE_OK;
 }
 
@@ -1641,7 +1664,22 @@ jorge_status jorge_read_diag(jorge_ctx* c, int32_t layer, double* out) {
 
 jorge_status jorge_set_stream(jorge_ctx* c, void* hip_stream) {
     if (!c) return JORGE_ERR_INVALID_ARGUMENT;
-    c->stream = reinterpret_cast<hipStream_t>(hip_stream);
+    const hipStream_t s = reinterpret_cast<hipStream_t>(hip_stream);
+    if (s == c->stream) return JORGE_OK;
+    // Work queued later on the new stream waits for all work already queued
+    // on the old one. Not when either stream is being captured into a graph:
+    // a capture cannot wait on an event recorded outside it, nor the reverse,
+    // and the capture's owner orders the streams (torch.cuda.graph
+    // synchronises the device before it starts capturing).
+    hipStreamCaptureStatus cap_new = hipStreamCaptureStatusNone, cap_old = hipStreamCaptureStatusNone;
+    JORGE_HIP(c, hipStreamIsCapturing(s, &cap_new));
+    if (cap_new == hipStreamCaptureStatusNone && hipStreamIsCapturing(c->stream, &cap_old) == hipSuccess &&
+        cap_old == hipStreamCaptureStatusNone) {
+        if (!c->order_event) JORGE_HIP(c, hipEventCreateWithFlags(&c->order_event, hipEventDisableTiming));
+        JORGE_HIP(c, hipEventRecord(c->order_event, c->stream));
+        JORGE_HIP(c, hipStreamWaitEvent(s, c->order_event, 0));
+    }
+    c->stream = s;
     return JORGE_OK;
 }
 

@@ -397,8 +397,8 @@ __global__ __launch_bounds__(kGemmThreads) void lds_chain_kernel(const FactorDev
 }
 
 // Per-layer norms of m and m_SGD from their partial sums, and the grafted
-// step g (Algorithm 3) with the decoupled decay factor (Section 4). One wave
-// per layer.
+// step g (Algorithm 3) with the decoupled decay rate lr * wd (Section 4). One
+// wave per layer.
 __global__ void layer_finalize_kernel(const LayerDev* __restrict__ layers, double lr, double wd,
                                       int graft) {
     const LayerDev L = layers[blockIdx.x];
@@ -412,18 +412,21 @@ __global__ void layer_finalize_kernel(const LayerDev* __restrict__ layers, doubl
     out.norm_sgd = ns;
     out.g = g;
     out.gf = (float)g;
-    out.decay = (float)(1.0 - lr * wd);
+    out.lw = (float)(lr * wd);
     *L.ls = out;
 }
 
-// theta <- theta (1 - lr wd) - g m over a flat chunk of one layer.
+// theta <- theta (1 - lr wd) - g m over a flat chunk of one layer, evaluated as
+// theta - (lr wd theta + g m): the small correction is formed first, so the
+// stored parameter is rounded once (1 - lr wd in fp32 would itself be off by up
+// to 2^-25, a systematic error of that size on every parameter).
 __global__ __launch_bounds__(kEwThreads) void weight_kernel(const LayerDev* __restrict__ layers,
                                                             const FlatChunk* __restrict__ chunks,
                                                             int layer_base, MutPtrBatch params) {
     const FlatChunk ck = chunks[blockIdx.x];
     const LayerDev& L = layers[ck.layer];
     float* __restrict__ th = params.p[ck.layer - layer_base];
-    const float g = L.ls->gf, decay = L.ls->decay;
+    const float g = L.ls->gf, lw = L.ls->lw;
     const float* __restrict__ m = L.mom;
     if ((ck.count & 3) == 0 && (reinterpret_cast<uintptr_t>(th) & 15) == 0) {
         const int n4 = ck.count >> 2;
@@ -443,7 +446,7 @@ __global__ __launch_bounds__(kEwThreads) void weight_kernel(const LayerDev* __re
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
 #pragma unroll
-                for (int q = 0; q < 4; ++q) t[i][q] = t[i][q] * decay - g * mv[i][q];
+                for (int q = 0; q < 4; ++q) t[i][q] = t[i][q] - (lw * t[i][q] + g * mv[i][q]);
                 t4[e + i * kEwThreads] = t[i];
             }
         }
@@ -451,13 +454,13 @@ __global__ __launch_bounds__(kEwThreads) void weight_kernel(const LayerDev* __re
             f32x4 t = t4[e];
             const f32x4 mv = m4[e];
 #pragma unroll
-            for (int q = 0; q < 4; ++q) t[q] = t[q] * decay - g * mv[q];
+            for (int q = 0; q < 4; ++q) t[q] = t[q] - (lw * t[q] + g * mv[q]);
             t4[e] = t;
         }
     } else {
         for (int e = threadIdx.x; e < ck.count; e += kEwThreads) {
             const int i = ck.start + e;
-            th[i] = th[i] * decay - g * m[i];
+            th[i] = th[i] - (lw * th[i] + g * m[i]);
         }
     }
 }

@@ -49,7 +49,7 @@ struct LayerScalars {
     double norm_sgd;  // ||m_SGD,t||_F
     double g;         // step applied to m_t
     float gf;         // g as fp32
-    float decay;      // 1 - lr * weight_decay as fp32
+    float lw;         // lr * weight_decay as fp32 (theta <- theta - (lw theta + g m))
 };
 
 // One product of a grouped launch. With both operands K-major (the "NT"

@@ -77,11 +77,16 @@ _SIGNATURES = {
 }
 
 
-def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
-    """Loads libjorge.so (built by paper_2310_12298_amd.build); raises if absent."""
+def load_library(path: str | None = None) -> ctypes.CDLL:
+    """Loads libjorge.so (built by paper_2310_12298_amd.build); raises if absent.
+
+    path: the library file, LIB_PATH by default (read at call time, so a test can
+    point the binding at another build of the same sources).
+    """
     global _LIB
     if _LIB is not None:
         return _LIB
+    path = LIB_PATH if path is None else path
     if not os.path.exists(path):
         raise FileNotFoundError(f"{path} is not built; run __graft_entry__.build() or "
                                 f"python -m paper_2310_12298_amd.build")

@@ -1,15 +1,17 @@
-"""GPU checks of the torch.optim front end: it is exactly the library's grouped
-step on the matrix parameters, column order does not matter (channels-last
-weights are used in place), vectors follow heavy-ball SGD, and its state
-round-trips."""
+"""GPU checks of the torch.optim front end: it matches the fp64 oracle on a small
+convolutional model, it is exactly the library's grouped step on the matrix
+parameters, column order does not matter (channels-last weights are used in
+place), vectors follow heavy-ball SGD, and its state round-trips."""
 import io
 
 import pytest
 
 torch = pytest.importorskip("torch")
 
+from oracle import JorgeOracle  # noqa: E402
 from paper_2310_12298_amd.jorge import Jorge  # noqa: E402
 from paper_2310_12298_amd.optim import JorgeOptimizer  # noqa: E402
+from parity_metrics import STEP, TRAJ, check_layer  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 HP = dict(lr=0.1, beta1=0.9, beta2=0.9, weight_decay=5e-4)
@@ -26,6 +28,31 @@ def grads_for(m, t):
     gen = torch.Generator(device="cuda").manual_seed(1000 + t)
     for p in m.parameters():
         p.grad = torch.randn(p.shape, generator=gen, device="cuda").mul_(1e-2).to(memory_format=torch.contiguous_format)
+
+
+def test_optimizer_matches_the_oracle():
+    """The drop-in optimizer (Section 4) on a small conv net against the fp64 oracle: each
+    matrix parameter is its weight collapsed to out x in*kh*kw (Section 3), stepped by
+    Algorithm 2 with Algorithm 3's grafting and the decoupled decay of Section 4. One-step
+    gates after step 1, trajectory gates after steps 2-5, on theta, L_hat, R_hat, m and m_SGD."""
+    m = model()
+    mats = [p for p in m.parameters() if p.dim() >= 2]
+    shapes = [(p.shape[0], p.numel() // p.shape[0]) for p in mats]
+    opt = JorgeOptimizer(m.parameters(), **HP)
+    orc = JorgeOracle(shapes)
+    po = [p.detach().double().cpu().numpy().reshape(s) for p, s in zip(mats, shapes)]
+    for t in range(1, 6):
+        grads_for(m, t)
+        G = [p.grad.detach().reshape(s).cpu().numpy() for p, s in zip(mats, shapes)]
+        opt.step()
+        prev = po
+        po = orc.step(po, G, HP["lr"], HP["beta2"], HP["beta1"], HP["weight_decay"])
+        for i, (p, s) in enumerate(zip(mats, shapes)):
+            st = orc.layers[i]
+            gpu = {k: opt.ctx.get_state(i, k).cpu().numpy() for k in ("L", "R", "mom", "mom_sgd")}
+            check_layer(gpu, {"L": st.L, "R": st.R, "mom": st.m, "mom_sgd": st.m_sgd},
+                        p.detach().reshape(s).cpu().numpy(), po[i], prev[i], HP["lr"], HP["weight_decay"],
+                        STEP if t == 1 else TRAJ, f"step {t} parameter {i} {s}")
 
 
 def test_matches_direct_library_steps_bitwise():
