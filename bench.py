@@ -104,6 +104,8 @@ GEMM_STAGES = ("gram", "pow4", "xform", "chain4", "chain5", "poly", "poly2", "up
 NON_UPDATE_STAGES = ("precond_L", "precond_R")
 # Launches of the grouped GEMM's split-tile fixup: their time is part of the GEMM stages' time.
 FIXUP_STAGE = "split_fixup"
+# The LDS chain kernels (whole factor updates of small factors in one workgroup each).
+CHAIN_STAGE = "lds_chain"
 
 
 def copy_reference_gbs(mib=1024, reps=10):
@@ -184,7 +186,7 @@ def cpu_info():
 
 
 def measure(config, steps, warmup, interval=1, form="auto", split_k=1, series_order=2, seed=0,
-            copy_probe_mib=0):
+            copy_probe_mib=0, chain_max=128):
     """Times one workload: W warm-up steps, then K steps twice (clean, then with per-launch events)."""
     import torch
 
@@ -195,7 +197,7 @@ def measure(config, steps, warmup, interval=1, form="auto", split_k=1, series_or
     steps = steps if steps is not None else run_steps
     hp = DEFAULT_HPARAMS
     opt = Jorge(shapes, eps=hp["eps"], precond_interval=interval, factor_form=form,
-                split_k=bool(split_k), series_order=series_order)
+                split_k=bool(split_k), series_order=series_order, lds_chain_max=chain_max)
     params = [device_initial_params(seed, l, s) for l, s in enumerate(shapes)]
     grads = [[device_gradient(seed, l, t, s, sigma) for l, s in enumerate(shapes)]
              for t in range(1, warmup + steps + 1)]
@@ -248,10 +250,11 @@ def measure(config, steps, warmup, interval=1, form="auto", split_k=1, series_or
     # Algorithmic flops of each stage in one factor-updating step, from the library's launch tables.
     flops = opt.stage_flops()
     ran = {k: (steps - updates if k in NON_UPDATE_STAGES else updates) for k in GEMM_STAGES}
+    ran[CHAIN_STAGE] = updates
     per_stage = {}
     for k, (ms, n) in timing.items():
         e = {"ms_per_launch": ms / n if n else 0.0, "launches": n}
-        if k in GEMM_STAGES and ms > 0:
+        if k in ran and ms > 0:
             e["tflops"] = flops[k] * ran[k] / (ms * 1e-3) / 1e12
         per_stage[k] = e
     # Dominant kernel: the grouped NT GEMM; every GEMM stage of the step is a launch of it.
@@ -266,7 +269,8 @@ def measure(config, steps, warmup, interval=1, form="auto", split_k=1, series_or
         k_ms = timing[k][0] / max(1, timing[k][1])
         gbs = nbytes / (k_ms * 1e-3) / 1e9 if k_ms else 0.0
         hbm[k] = {"achieved": gbs, "frac": gbs / PEAK_HBM_GBS, "bytes_per_launch": nbytes}
-    step_f = g_flops / steps
+    # the step's flops: the grouped levels' and the LDS chains' (these run on a second stream, beside the levels)
+    step_f = (g_flops + flops[CHAIN_STAGE] * updates) / steps
     step_b = (step_bytes(shapes, True) * updates + step_bytes(shapes, False) * (steps - updates)) / steps
     t_mfma, t_hbm = step_f / (PEAK_FP32_MFMA_TFLOPS * 1e12), step_b / (PEAK_HBM_GBS * 1e9)
     step_roof = {"flops": step_f, "bytes": step_b, "t_mfma_ms": t_mfma * 1e3, "t_hbm_ms": t_hbm * 1e3,
@@ -317,6 +321,8 @@ def main():
     ap.add_argument("--series-order", type=int, default=2, choices=(2, 3),
                     help="last power of X kept from the binomial series (Section 3 keeps 2)")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--chain-max", type=int, default=128, choices=(0, 32, 64, 96, 128),
+                    help="largest padded factor size the LDS chain kernels take (0: every factor in the levels)")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time (0 = skip)")
     ap.add_argument("--others", type=int, default=1, choices=(0, 1),
                     help="also time the other four workloads, each for its stated number of steps, and report "
@@ -335,7 +341,7 @@ def main():
 
     torch.cuda.set_device(0)
     res = measure(args.config, args.steps, args.warmup, args.interval, args.form, args.split_k, args.series_order,
-                  args.seed, args.copy_probe_mib)
+                  args.seed, args.copy_probe_mib, args.chain_max)
     shapes, steps = res["shapes"], res["steps"]
     traffic = measured_traffic(args.config)
     ms_launch = res["gemm"]["ms_per_launch"]
@@ -363,7 +369,8 @@ def main():
         "config": {"workload": WORKLOAD_NAMES[args.config], "name": args.config, "layers": len(shapes),
                    "params": sum(m * n for m, n in shapes), "precond_interval": args.interval,
                    "factor_updates": res["updates"], "factor_form": args.form, "factors": res["forms"],
-                   "split_k": args.split_k, "series_order": args.series_order, "seed": args.seed},
+                   "split_k": args.split_k, "series_order": args.series_order, "lds_chain_max": args.chain_max,
+                   "seed": args.seed},
         "roofline": {"bound": "mfma", "kernel": "gemm_grouped<true, true> (every GEMM stage of the step)",
                      "achieved": achieved, "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_FP32_MFMA_TFLOPS, "flop_basis": FLOP_BASIS,
@@ -384,7 +391,7 @@ def main():
         "stages": res["stages"],
     }
     if args.others and args.copy_probe_mib == 0:
-        out["other_workloads"] = {c: summary(measure(c, None, args.warmup, seed=args.seed))
+        out["other_workloads"] = {c: summary(measure(c, None, args.warmup, seed=args.seed, chain_max=args.chain_max))
                                   for c in WORKLOAD_NAMES if c != args.config}
     if args.cpu_budget > 0:
         out["cpu_baseline"] = dict(cpu_baseline(shapes, res["sigma"], args.seed, args.cpu_budget,

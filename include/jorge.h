@@ -128,10 +128,11 @@ typedef struct jorge_hparams {
                                  Default 1. */
     int32_t lds_chain_max;    /* when every factor's size rounded up to 32 is at most this, each
                                  factor update runs in the explicit order in one workgroup with
-                                 every matrix in LDS (one launch for all of them) instead of the
-                                 grouped levels. With any larger factor present the levels run
-                                 anyway and take the small factors too. 0 disables. In [0, 64].
-                                 Default 64. */
+                                 its matrices in LDS (one launch for the factors up to 64, one
+                                 for those of 96 and 128, which need symmetrize = 1) instead of
+                                 the grouped levels. With any larger factor present the levels
+                                 run anyway and take the small factors too. 0 disables.
+                                 In [0, 128]. Default 128. */
     int32_t precond_lowrank;  /* 1: on update steps, a factored factor A with d > 3k preconditions
                                  through A_new H = s A H - (s/2)(W H^T H + H W^T H), built from
                                  the update's own terms (about 6 k^2 d flops instead of a d x d

@@ -48,9 +48,11 @@
 //             update's own terms instead (low-rank preconditioning)
 //   lfinal    ||m||, ||m_SGD||, grafted step g
 //   weight    theta <- theta (1 - lr wd) - g m
-// When every factor has padded size up to hp.lds_chain_max (at most 64), the
-// levels are replaced by one launch of lds_chain_kernel, which runs each
-// factor's whole explicit-order update in one workgroup with every matrix in LDS.
+// When every factor has padded size up to hp.lds_chain_max (at most 128), the
+// levels are replaced by LDS chain kernels, which run each factor's whole
+// explicit-order update in one workgroup with its matrices in LDS
+// (lds_chain_kernel up to 64, lds_chain128_kernel for 96 and 128; one launch
+// each for all their factors).
 // Non-update steps run stage-in, precond, lfinal and weight only.
 #include <hip/hip_runtime.h>
 
@@ -127,7 +129,7 @@ struct FactorHost {
     int layer, side, d, dp, k, kp;
     bool expl = true;
     bool squared = false;  // (not explicit) the squared order: A^2 formed, the chain in steps of A^2
-    bool chain = false;  // small: the whole update in one workgroup (lds_chain_kernel), explicit order
+    bool chain = false;  // small: the whole update in one workgroup (an LDS chain kernel), explicit order
     // Low-rank preconditioning on update steps (factored, symmetric, d > 3k): the
     // layer's A_new H comes from the chain's A H, W, Q and H^T W (see add_factored).
     bool lrp = false;
@@ -166,9 +168,13 @@ struct jorge_ctx {
     std::vector<FlatChunk> flat_chunks;
     std::vector<int> stage_batch_start, flat_batch_start;  // first block of each layer batch
     std::vector<SymTile> sym_tiles;
-    std::vector<int> grouped, chain;   // factors of the grouped levels / of the LDS chain
+    // factors of the grouped levels, of the LDS chain (padded size <= 64) and of
+    // the LDS chain for padded sizes 96 and 128
+    std::vector<int> grouped, chain, chain2;
     int* dgrouped = nullptr;
     int* dchain = nullptr;
+    int* dchain2 = nullptr;
+    double chain_flops = 0.0;  // algorithmic flops of the chains' factor updates
     float* splitws = nullptr;     // partial products of split tiles (shared by the stages, in turn)
     int64_t splitws_blocks = 0;
     // Per stage: products with both operands K-major, and (literal mode only)
@@ -635,7 +641,7 @@ jorge_status validate_hparams(const jorge_hparams* hp) {
         return JORGE_ERR_INVALID_ARGUMENT;
     if (hp->factor_form == JORGE_FORM_SQUARED && hp->symmetrize != 1) return JORGE_ERR_INVALID_ARGUMENT;
     if (hp->split_k != 0 && hp->split_k != 1) return JORGE_ERR_INVALID_ARGUMENT;
-    if (hp->lds_chain_max < 0 || hp->lds_chain_max > kChainMax) return JORGE_ERR_INVALID_ARGUMENT;
+    if (hp->lds_chain_max < 0 || hp->lds_chain_max > kChain2Max) return JORGE_ERR_INVALID_ARGUMENT;
     if (hp->precond_lowrank != 0 && hp->precond_lowrank != 1) return JORGE_ERR_INVALID_ARGUMENT;
     if (hp->series_order != 2 && hp->series_order != 3) return JORGE_ERR_INVALID_ARGUMENT;
     return JORGE_OK;
@@ -679,12 +685,16 @@ size_t plan(jorge_ctx* c) {
         return o;
     };
     const bool sym = c->hp.symmetrize != 0;
-    // The LDS chain takes the factor updates only when it replaces the grouped
-    // levels altogether: with any larger factor present the levels run anyway,
-    // and the small factors' tiles fill slots of theirs that would idle.
+    // The LDS chains take the factor updates (explicit order, one workgroup per
+    // factor) when every factor of the context has padded size up to
+    // lds_chain_max, replacing the grouped levels altogether (sizes 96 and 128
+    // need symmetric factors). With any larger factor present the levels run
+    // anyway, and the small factors' tiles fill slots of theirs that would
+    // otherwise idle: taking the small factors out to the chains, on a second
+    // stream beside the levels or before them, measured no faster.
     int max_dp = 0;
     for (const auto& L : c->layers) max_dp = std::max(max_dp, std::max(L.mp, L.np));
-    const bool use_chain = max_dp <= c->hp.lds_chain_max;
+    const bool all_small = max_dp <= c->hp.lds_chain_max && (max_dp <= kChainMax || sym);
     for (auto& L : c->layers) {
         for (int side = 0; side < 2; ++side) {
             FactorHost F{};
@@ -694,20 +704,24 @@ size_t plan(jorge_ctx* c) {
             F.dp = side == 0 ? L.mp : L.np;
             F.k = side == 0 ? L.n : L.m;
             F.kp = side == 0 ? L.np : L.mp;
-            F.chain = use_chain;
             // A_new H (d x k) replaces a d x d product in the preconditioning when
             // 6 k^2 d < 2 d^2 k, i.e. d > 3 k (both orders then cost 2 k^2 d more).
             const bool lrp_ok = sym && c->hp.precond_lowrank && (int64_t)F.d > 3 * (int64_t)F.k;
-            const int form = F.chain ? JORGE_FORM_EXPLICIT
-                             : c->hp.factor_form != JORGE_FORM_AUTO
-                                 ? c->hp.factor_form
-                                 : choose_form(F.dp, F.kp, sym, c->hp.series_order, lrp_ok);
+            const int level_form = c->hp.factor_form != JORGE_FORM_AUTO
+                                       ? c->hp.factor_form
+                                       : choose_form(F.dp, F.kp, sym, c->hp.series_order, lrp_ok);
+            F.chain = all_small;
+            const int form = F.chain ? JORGE_FORM_EXPLICIT : level_form;
             F.expl = form == JORGE_FORM_EXPLICIT;
             F.squared = form == JORGE_FORM_SQUARED;
             const size_t dd = (size_t)F.dp * F.dp * sizeof(float);
             F.off_A = take(dd);
             if (F.chain) {
                 F.nparts = 1;  // unused: the chain kernel reduces ||X|| itself
+                // the explicit order's algorithmic flops (symmetric products counted once)
+                const double d = F.d, k = F.k;
+                c->chain_flops += d * d * k + (sym ? 2.0 : 4.0) * d * d * d +
+                                  (c->hp.series_order == 3 ? 8.0 : 6.0) * d * d * d;
             } else if (F.expl) {
                 for (int w = 0; w < 4; ++w) F.off_w[w] = take(dd);
                 F.nparts = tile_count(F.dp, F.dp);
@@ -1002,7 +1016,7 @@ void build_tables(jorge_ctx* c, std::vector<LayerDev>& ld, std::vector<FactorDev
         const float* Hr = F.side == 0 ? l.Gp : l.Gpt;
         const float* Ht = F.side == 0 ? l.Gpt : l.Gp;
         if (F.chain) {
-            c->chain.push_back(fi);
+            (F.dp <= kChainMax ? c->chain : c->chain2).push_back(fi);
             continue;
         }
         c->grouped.push_back(fi);
@@ -1251,15 +1265,20 @@ std::string check_tables(const jorge_ctx* c, const std::vector<FactorDev>& fd) {
     for (const FactorDev& F : fd)
         if (!in_buffer(c, F.partials, (int64_t)F.nparts * kWaveSlots * (int64_t)sizeof(double)) || F.nparts < 1)
             return "factor partials";
-    for (int fi : c->chain) {  // lds_chain_kernel: A (dp x dp), H (dp x kp), scalars
-        const FactorDev& F = fd[fi];
-        if (F.dp > kChainMax || F.dp % 32 || F.kp % kSlab || F.kp < kSlab ||
-            !in_buffer(c, F.A, (int64_t)F.dp * F.dp * (int64_t)sizeof(float)) ||
-            !in_buffer(c, F.H, (int64_t)F.dp * F.kp * (int64_t)sizeof(float)) ||
-            !in_buffer(c, F.sc, (int64_t)sizeof(FactorScalars)))
-            return "lds chain factor";
-    }
-    if (c->grouped.size() + c->chain.size() != fd.size()) return "factor lists";
+    // The LDS chain kernels: A (dp x dp), H (dp x kp), scalars; dp <= 64 for
+    // lds_chain_kernel, 64 < dp <= 128 (symmetric factors) for lds_chain128_kernel.
+    for (int which = 0; which < 2; ++which)
+        for (int fi : which ? c->chain2 : c->chain) {
+            const FactorDev& F = fd[fi];
+            const bool size_ok = which ? (F.dp > kChainMax && F.dp <= kChain2Max && c->hp.symmetrize)
+                                       : F.dp <= kChainMax;
+            if (!size_ok || F.dp % 32 || F.kp % kSlab || F.kp < kSlab ||
+                !in_buffer(c, F.A, (int64_t)F.dp * F.dp * (int64_t)sizeof(float)) ||
+                !in_buffer(c, F.H, (int64_t)F.dp * F.kp * (int64_t)sizeof(float)) ||
+                !in_buffer(c, F.sc, (int64_t)sizeof(FactorScalars)))
+                return "lds chain factor";
+        }
+    if (c->grouped.size() + c->chain.size() + c->chain2.size() != fd.size()) return "factor lists";
     return "";
 }
 
@@ -1319,10 +1338,13 @@ template <typename T>
 jorge_status upload(jorge_ctx* c, const std::vector<T>& v, T** dptr) {
     *dptr = nullptr;
     if (v.empty()) return JORGE_OK;
-    JORGE_HIP(c, hipMalloc(reinterpret_cast<void**>(dptr), v.size() * sizeof(T)));
-    JORGE_HIP(c, hipMemcpy(*dptr, v.data(), v.size() * sizeof(T), hipMemcpyHostToDevice));
+    const size_t bytes = v.size() * sizeof(T);
+    JORGE_HIP(c, hipMalloc(reinterpret_cast<void**>(dptr), bytes));
+    JORGE_HIP(c, hipMemcpy(*dptr, v.data(), bytes, hipMemcpyHostToDevice));
     return JORGE_OK;
 }
+
+
 
 jorge_status upload_stage(jorge_ctx* c, GemmStage& st) {
     jorge_status s = upload(c, st.probs, &st.dprobs);
@@ -1330,6 +1352,23 @@ jorge_status upload_stage(jorge_ctx* c, GemmStage& st) {
     if ((s = upload(c, st.fix, &st.dfix)) != JORGE_OK) return s;
     if ((s = upload(c, st.small, &st.dsmall)) != JORGE_OK) return s;
     return upload(c, st.tiles, &st.dtiles);
+}
+
+// Every device table of a context whose host tables are built.
+jorge_status upload_tables(jorge_ctx* c, const std::vector<LayerDev>& ld, const std::vector<FactorDev>& fd) {
+    jorge_status st;
+    if ((st = upload(c, ld, &c->dlayers)) != JORGE_OK) return st;
+    if ((st = upload(c, fd, &c->dfactors)) != JORGE_OK) return st;
+    if ((st = upload(c, c->stage_tiles, &c->dstage)) != JORGE_OK) return st;
+    if ((st = upload(c, c->flat_chunks, &c->dflat)) != JORGE_OK) return st;
+    if ((st = upload(c, c->sym_tiles, &c->dsym)) != JORGE_OK) return st;
+    if ((st = upload(c, c->grouped, &c->dgrouped)) != JORGE_OK) return st;
+    if ((st = upload(c, c->chain, &c->dchain)) != JORGE_OK) return st;
+    if ((st = upload(c, c->chain2, &c->dchain2)) != JORGE_OK) return st;
+    for (int i = 0; i < ST_COUNT; ++i)
+        for (GemmStage* s : {&c->nt[i], &c->nn[i]})
+            if ((st = upload_stage(c, *s)) != JORGE_OK) return st;
+    return JORGE_OK;
 }
 
 void free_ctx(jorge_ctx* c) {
@@ -1349,6 +1388,7 @@ void free_ctx(jorge_ctx* c) {
     if (c->dsym) (void)hipFree(c->dsym);
     if (c->dgrouped) (void)hipFree(c->dgrouped);
     if (c->dchain) (void)hipFree(c->dchain);
+    if (c->dchain2) (void)hipFree(c->dchain2);
     if (c->arena) (void)hipFree(c->arena);
     for (auto& l : c->pending) {
         (void)hipEventDestroy(l.start);
@@ -1367,7 +1407,15 @@ jorge_status launch_stage(jorge_ctx* c, int stage, float beta1) {
 
 jorge_status run_update(jorge_ctx* c, double beta2) {
     jorge_status s;
-    if (!c->chain.empty()) {  // every factor of the context (the levels below are then empty)
+    // The LDS chains: every factor of the context (the levels below are then empty).
+    if (!c->chain2.empty()) {
+        TimedLaunch tl(c, ST_LDS_CHAIN);
+        hipLaunchKernelGGL(lds_chain128_kernel, dim3((unsigned)c->chain2.size()), dim3(kGemmThreads), 0, c->stream,
+                           c->dfactors, c->dchain2, beta2, (int)c->hp.beta_mode, (int)c->hp.series_order);
+        tl.finish();
+        JORGE_HIP(c, hipGetLastError());
+    }
+    if (!c->chain.empty()) {
         TimedLaunch tl(c, ST_LDS_CHAIN);
         hipLaunchKernelGGL(lds_chain_kernel, dim3((unsigned)c->chain.size()), dim3(kGemmThreads), 0, c->stream,
                            c->dfactors, c->dchain, beta2, (int)c->hp.beta_mode, (int)c->hp.symmetrize,
@@ -1472,7 +1520,7 @@ jorge_status jorge_hparams_default(jorge_hparams* hp) {
     hp->symmetrize = 1;
     hp->factor_form = JORGE_FORM_AUTO;
     hp->split_k = 1;
-    hp->lds_chain_max = kChainMax;
+    hp->lds_chain_max = kChain2Max;
     hp->precond_lowrank = 1;
     hp->series_order = 2;
     return JORGE_OK;
@@ -1505,16 +1553,7 @@ jorge_status jorge_create(const jorge_shape* shapes, int32_t num_layers, const j
         e = hipMalloc(reinterpret_cast<void**>(&c->splitws), (size_t)c->splitws_blocks * kSplitBlock * sizeof(float));
         if (e != hipSuccess) return bail(e == hipErrorOutOfMemory ? JORGE_ERR_OUT_OF_MEMORY : JORGE_ERR_HIP);
     }
-    if ((st = upload(c, ld, &c->dlayers)) != JORGE_OK) return bail(st);
-    if ((st = upload(c, fd, &c->dfactors)) != JORGE_OK) return bail(st);
-    if ((st = upload(c, c->stage_tiles, &c->dstage)) != JORGE_OK) return bail(st);
-    if ((st = upload(c, c->flat_chunks, &c->dflat)) != JORGE_OK) return bail(st);
-    if ((st = upload(c, c->sym_tiles, &c->dsym)) != JORGE_OK) return bail(st);
-    if ((st = upload(c, c->grouped, &c->dgrouped)) != JORGE_OK) return bail(st);
-    if ((st = upload(c, c->chain, &c->dchain)) != JORGE_OK) return bail(st);
-    for (int i = 0; i < ST_COUNT; ++i)
-        for (GemmStage* s : {&c->nt[i], &c->nn[i]})
-            if ((st = upload_stage(c, *s)) != JORGE_OK) return bail(st);
+    if ((st = upload_tables(c, ld, fd)) != JORGE_OK) return bail(st);
     hipLaunchKernelGGL(init_factors_kernel, dim3((unsigned)c->factors.size()), dim3(256), 0, c->stream,
                        c->dfactors, (float)std::pow(h.eps, -0.25));
     if (hipGetLastError() != hipSuccess) return bail(JORGE_ERR_HIP);
@@ -1734,7 +1773,8 @@ int32_t jorge_num_stages(void) { return ST_COUNT; }
 
 jorge_status jorge_stage_flops(const jorge_ctx* c, double* flops, int32_t n) {
     if (!c || !flops || n < 0) return JORGE_ERR_INVALID_ARGUMENT;
-    for (int i = 0; i < std::min<int>(n, ST_COUNT); ++i) flops[i] = c->nt[i].flops + c->nn[i].flops;
+    for (int i = 0; i < std::min<int>(n, ST_COUNT); ++i)
+        flops[i] = c->nt[i].flops + c->nn[i].flops + (i == ST_LDS_CHAIN ? c->chain_flops : 0.0);
     return JORGE_OK;
 }
 

@@ -121,7 +121,7 @@ class Jorge:
     """
 
     def __init__(self, shapes, eps=1e-6, precond_interval=1, beta_mode="clamped", graft=True,
-                 symmetrize=True, factor_form="auto", split_k=True, lds_chain_max=64, precond_lowrank=True,
+                 symmetrize=True, factor_form="auto", split_k=True, lds_chain_max=128, precond_lowrank=True,
                  series_order=2, stream=None):
         self.lib = load_library()
         self.shapes = [(int(m), int(n)) for m, n in shapes]
@@ -136,7 +136,7 @@ class Jorge:
 
     @staticmethod
     def hparams(eps=1e-6, precond_interval=1, beta_mode="clamped", graft=True, symmetrize=True,
-                factor_form="auto", split_k=True, lds_chain_max=64, precond_lowrank=True, series_order=2):
+                factor_form="auto", split_k=True, lds_chain_max=128, precond_lowrank=True, series_order=2):
         lib = load_library()
         hp = HParams()
         _check(lib, lib.jorge_hparams_default(ctypes.byref(hp)))

@@ -47,7 +47,7 @@ def test_hparams_default(lib):
     assert lib.jorge_hparams_default(ctypes.byref(hp)) == 0
     assert (hp.eps, hp.precond_interval, hp.beta_mode, hp.graft, hp.symmetrize,
             hp.factor_form, hp.split_k, hp.lds_chain_max, hp.precond_lowrank,
-            hp.series_order) == (1e-6, 1, 2, 1, 1, 0, 1, 64, 1, 2)
+            hp.series_order) == (1e-6, 1, 2, 1, 1, 0, 1, 128, 1, 2)
     assert lib.jorge_hparams_default(None) == ERR_INVALID
 
 
@@ -74,7 +74,7 @@ def test_create_rejects_oversize(lib):
                                          ("beta_mode", 3), ("beta_mode", -1), ("graft", 2),
                                          ("symmetrize", -1), ("factor_form", -1),
                                          ("factor_form", 4), ("split_k", 2), ("split_k", -1),
-                                         ("lds_chain_max", -1), ("lds_chain_max", 65),
+                                         ("lds_chain_max", -1), ("lds_chain_max", 129),
                                          ("precond_lowrank", 2), ("series_order", 1),
                                          ("series_order", 4), ("series_order", 0)])
 def test_create_rejects_bad_hparams(lib, field, value):
@@ -230,7 +230,7 @@ def test_plan_tables_of_edge_shapes(lib, form, symmetrize):
     for s in shapes:
         assert J.Jorge.plan([s], symmetrize=symmetrize, factor_form=form) > 0
         assert J.Jorge.plan([s], symmetrize=symmetrize, factor_form=form, split_k=False) > 0
-        for lds in (0, 32):
+        for lds in (0, 32, 64, 96, 128):
             assert J.Jorge.plan([s], symmetrize=symmetrize, factor_form=form, lds_chain_max=lds) > 0
         assert J.Jorge.plan([s], symmetrize=symmetrize, factor_form=form, precond_lowrank=False) > 0
         assert J.Jorge.plan([s], symmetrize=symmetrize, factor_form=form, series_order=3) > 0
@@ -254,3 +254,21 @@ def test_plan_rejects_what_create_rejects(lib):
         J.Jorge.plan([(4, 32769)])
     with pytest.raises(J.JorgeError):
         J.Jorge.plan([(4, 4)], factor_form=7)
+
+
+def test_plan_small_contexts_take_the_lds_chains(lib):
+    """Every factor of padded size <= lds_chain_max: the LDS chains replace the grouped
+    levels (no GEMM units); sizes 96 and 128 need symmetric factors; one larger factor
+    brings the levels back for all."""
+    levels = ("gram", "pow4", "xform", "chain4", "chain5", "poly", "poly2", "update")
+
+    def units(shapes, **kw):   # work units of the factor-update levels (the preconditioning stays)
+        st = J.Jorge.plan_stages(shapes, **kw)
+        return sum(st[k][0] for k in levels)
+
+    small = [(128, 128), (96, 128), (100, 70), (128, 40), (65, 97), (3, 128), (128, 90)]
+    assert units(small) == 0
+    assert units(small, lds_chain_max=64) > 0 and units(small, lds_chain_max=0) > 0
+    assert units(small, symmetrize=False) > 0                 # the 96- and 128-wide chain needs symmetry
+    assert units([(64, 64), (40, 33)], symmetrize=False) == 0
+    assert units(small + [(64, 576)]) > 0

@@ -365,6 +365,8 @@ def test_split_k_parity_and_determinism(form):
 
 
 SMALL_SHAPES = [(64, 64), (32, 48), (5, 3), (40, 1), (33, 60), (64, 32), (1, 64), (50, 17)]
+# Padded sizes 96 and 128 (and smaller ones beside them), for lds_chain128_kernel.
+SMALL128_SHAPES = [(128, 128), (96, 128), (100, 70), (128, 40), (65, 97), (3, 128), (128, 90)]
 
 
 @pytest.mark.parametrize("symmetrize", [True, False])
@@ -397,6 +399,34 @@ def test_lds_chain_small_factors(symmetrize):
             for k in ("L", "R"):
                 A = a[0].get_state(l, k)
                 assert torch.equal(A, A.T), (l, k)
+        d = a[0].read_diag(l)
+        assert d["nu_L"] == pytest.approx(a[1].last_diag[l]["nu_L"], rel=1e-5)
+        assert d["nu_R"] == pytest.approx(a[1].last_diag[l]["nu_R"], rel=1e-5)
+
+
+@pytest.mark.parametrize("series_order", [2, 3])
+def test_lds_chain128_small_factors(series_order):
+    """In a context whose factors all have padded size <= 128, those of 96 and 128 run
+    their whole update in lds_chain128_kernel (and the smaller ones in lds_chain_kernel):
+    against the oracle, against the grouped levels, bitwise symmetric."""
+    shapes = SMALL128_SHAPES
+    say("LDS chain 128, series order", series_order)
+    kw = dict(series_order=series_order)
+    opt = Jorge(shapes, **kw)
+    opt.set_timing(True)
+    opt.step([torch.zeros(s, device="cuda") for s in shapes],
+             [to_dev(gradient(0, l, 1, s, 1e-2)) for l, s in enumerate(shapes)], **HP)
+    tm = opt.read_timing()
+    assert tm["lds_chain"][1] == 2 and tm["gram"][1] == 0     # both chain kernels, no levels
+    a = run_pair(shapes, 6, 1e-2, check_every=2, gpu_kw=kw, orc_kw=kw)
+    b = run_pair(shapes, 6, 1e-2, gpu_kw=dict(kw, lds_chain_max=0), orc_kw=kw)
+    for l in range(len(shapes)):
+        for k in KINDS:
+            x, y = a[0].get_state(l, k), b[0].get_state(l, k)
+            assert rel(x.cpu().numpy(), y.cpu().numpy()) < 1e-5, (l, k)
+        for k in ("L", "R"):
+            A = a[0].get_state(l, k)
+            assert torch.equal(A, A.T), (l, k)
         d = a[0].read_diag(l)
         assert d["nu_L"] == pytest.approx(a[1].last_diag[l]["nu_L"], rel=1e-5)
         assert d["nu_R"] == pytest.approx(a[1].last_diag[l]["nu_R"], rel=1e-5)
