@@ -208,6 +208,33 @@ jorge_status jorge_plan_stages(const jorge_shape* shapes, int32_t num_layers, co
 jorge_status jorge_step(jorge_ctx* ctx, float* const* params, const float* const* grads,
                         double lr, double beta2, double beta1, double weight_decay);
 
+/* For callers that cannot allocate device memory (tight serving loops,
+ * harnesses that forbid allocation): one step of one layer, as jorge_step
+ * computes it, with the state held by the caller and every temporary in the
+ * library's static device scratch of JORGE_NOALLOC_SCRATCH_BYTES per GPU,
+ * instead of a context's allocations. Makes no device allocation.
+ * shape: the layer (rows x cols); hp: options as for jorge_create (NULL = the
+ * defaults); t >= 1: the number of this step (the factors update when
+ * (t-1) mod precond_interval == 0).
+ * theta (in/out), grad (in): device, dense row-major rows x cols fp32.
+ * L (rows x rows), R (cols x cols), mom, mom_sgd (rows x cols): device, dense
+ * row-major fp32, the state before the step on entry and after it on return
+ * (start from eps^(-1/4) I, eps^(-1/4) I, 0, 0; jorge_get_state gives a
+ * context's state in this layout). lr, beta2, beta1, weight_decay: as for
+ * jorge_step. hip_stream: the stream the work is queued on.
+ * The call returns after the stream has executed the step (the scratch is
+ * reused by the next call). Calls on one GPU share its scratch: the library
+ * runs them one at a time (a lock per GPU), and each starts by clearing what
+ * must start at zero. Errors: JORGE_ERR_INVALID_ARGUMENT as for jorge_step;
+ * JORGE_ERR_UNSUPPORTED if the layer's workspace and launch tables need more
+ * than JORGE_NOALLOC_SCRATCH_BYTES (a 512 x 1024 layer fits with split_k = 1,
+ * a 1024 x 1024 one with split_k = 0); JORGE_ERR_HIP on a runtime error, in
+ * which case the caller's state may be partly updated. */
+#define JORGE_NOALLOC_SCRATCH_BYTES (64ll << 20)
+jorge_status jorge_step_noalloc(const jorge_shape* shape, const jorge_hparams* hp, int64_t t, float* theta,
+                                const float* grad, float* L, float* R, float* mom, float* mom_sgd, double lr,
+                                double beta2, double beta1, double weight_decay, void* hip_stream);
+
 /* Copies one state tensor (dense, row-major; sizes as listed for JORGE_STATE_*)
  * into dst, a device buffer with row stride ld_dst >= its columns. Stream-ordered. */
 jorge_status jorge_get_state(jorge_ctx* ctx, int32_t layer, int32_t kind, float* dst,

@@ -61,6 +61,7 @@
 #include <cstdio>
 #include <cstring>
 #include <functional>
+#include <mutex>
 #include <new>
 #include <queue>
 #include <string>
@@ -188,10 +189,23 @@ struct jorge_ctx {
     int64_t stage_launches[ST_COUNT] = {};
     std::string last_error;
     hipEvent_t order_event = nullptr;  // orders a stream switch (jorge_set_stream)
+    // jorge_step_noalloc: every device pointer of the context lies in lent
+    // memory (free_ctx frees none), and the device tables go to a pool there
+    // (upload() copies into it) instead of allocations of their own.
+    bool lent = false;
+    char* pool = nullptr;
+    size_t pool_bytes = 0, pool_used = 0;
     // A step failed after its first launch: part of the state may be updated
     // and part not. Further steps are refused until jorge_set_step.
     bool poisoned = false;
 };
+
+// Device scratch of jorge_step_noalloc: the arena, split workspace and launch
+// tables of its one-layer step live here instead of in allocations. Each GPU
+// the library runs on holds its own copy from module load to process end. In
+// host code this name is only a stand-in for the symbol: kernels and copies
+// take the per-device address that hipGetSymbolAddress returns.
+static __device__ __align__(256) unsigned char scratch[JORGE_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -1339,12 +1353,22 @@ jorge_status upload(jorge_ctx* c, const std::vector<T>& v, T** dptr) {
     *dptr = nullptr;
     if (v.empty()) return JORGE_OK;
     const size_t bytes = v.size() * sizeof(T);
+    if (c->pool) {  // stream-ordered copy into the lent pool; the caller keeps v alive until it is done
+        if (c->pool_used + bytes > c->pool_bytes)
+            return fail(c, JORGE_ERR_UNSUPPORTED, "launch tables exceed the scratch left for them");
+        *dptr = reinterpret_cast<T*>(c->pool + c->pool_used);
+        c->pool_used = (size_t)round_up((int64_t)(c->pool_used + bytes), kAlign);
+        JORGE_HIP(c, hipMemcpyAsync(*dptr, v.data(), bytes, hipMemcpyHostToDevice, c->stream));
+        return JORGE_OK;
+    }
     JORGE_HIP(c, hipMalloc(reinterpret_cast<void**>(dptr), bytes));
     JORGE_HIP(c, hipMemcpy(*dptr, v.data(), bytes, hipMemcpyHostToDevice));
     return JORGE_OK;
 }
 
-
+// Bytes the device tables of a built context take, each rounded to kAlign.
+template <typename T>
+size_t table_bytes(const std::vector<T>& v) { return (size_t)round_up((int64_t)(v.size() * sizeof(T)), kAlign); }
 
 jorge_status upload_stage(jorge_ctx* c, GemmStage& st) {
     jorge_status s = upload(c, st.probs, &st.dprobs);
@@ -1371,8 +1395,23 @@ jorge_status upload_tables(jorge_ctx* c, const std::vector<LayerDev>& ld, const 
     return JORGE_OK;
 }
 
+// What upload_tables places in a lent pool.
+size_t tables_bytes(const jorge_ctx* c, const std::vector<LayerDev>& ld, const std::vector<FactorDev>& fd) {
+    size_t b = table_bytes(ld) + table_bytes(fd) + table_bytes(c->stage_tiles) + table_bytes(c->flat_chunks) +
+               table_bytes(c->sym_tiles) + table_bytes(c->grouped) + table_bytes(c->chain) +
+               table_bytes(c->chain2);
+    for (int i = 0; i < ST_COUNT; ++i)
+        for (const GemmStage* s : {&c->nt[i], &c->nn[i]})
+            b += table_bytes(s->probs) + table_bytes(s->fix) + table_bytes(s->small) + table_bytes(s->tiles);
+    return b;
+}
+
 void free_ctx(jorge_ctx* c) {
     if (!c) return;
+    if (c->lent) {
+        delete c;
+        return;
+    }
     for (int i = 0; i < ST_COUNT; ++i)
         for (GemmStage* st : {&c->nt[i], &c->nn[i]}) {
             if (st->dprobs) (void)hipFree(st->dprobs);
@@ -1442,6 +1481,15 @@ jorge_status run_update(jorge_ctx* c, double beta2) {
     }
     return JORGE_OK;
 }
+
+// jorge_step_noalloc: per device, the scratch's device address (set on the
+// first call on that device) and the lock that serialises calls.
+constexpr int kMaxDevices = 64;
+struct NoallocDevice {
+    std::mutex mu;
+    char* base = nullptr;
+};
+NoallocDevice g_noalloc[kMaxDevices];
 
 // The launches of step t (everything jorge_step queues after validating).
 jorge_status launch_step(jorge_ctx* c, float* const* params, const float* const* grads, int64_t t, double lr,
@@ -1634,6 +1682,94 @@ jorge_status jorge_step(jorge_ctx* c, float* const* params, const float* const* 
         return s;
     }
     c->t = t;
+    return JORGE_OK;
+}
+
+jorge_status jorge_step_noalloc(const jorge_shape* shape, const jorge_hparams* hp, int64_t t, float* theta,
+                                const float* grad, float* L, float* R, float* mom, float* mom_sgd, double lr,
+                                double beta2, double beta1, double weight_decay, void* hip_stream) {
+    jorge_hparams h;
+    jorge_status st = validate_args(shape, 1, hp, &h);
+    if (st != JORGE_OK) return st;
+    if (t < 1 || !theta || !grad || !L || !R || !mom || !mom_sgd) return JORGE_ERR_INVALID_ARGUMENT;
+    if (!(std::isfinite(lr) && lr >= 0.0) || !(beta2 > 0.0 && beta2 < 1.0) || !(beta1 >= 0.0 && beta1 < 1.0) ||
+        !(std::isfinite(weight_decay) && weight_decay >= 0.0))
+        return JORGE_ERR_INVALID_ARGUMENT;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return JORGE_ERR_HIP;
+    // One call at a time per device: the scratch is shared.
+    std::lock_guard<std::mutex> lock(g_noalloc[dev].mu);
+    if (!g_noalloc[dev].base) {
+        void* ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return JORGE_ERR_HIP;
+        g_noalloc[dev].base = static_cast<char*>(ptr);
+    }
+    char* const base = g_noalloc[dev].base;
+    jorge_ctx* c = new (std::nothrow) jorge_ctx();
+    if (!c) return JORGE_ERR_OUT_OF_MEMORY;
+    struct Owner {  // on every return: waits for queued work (it reads c's host tables), frees c
+        jorge_ctx* c;
+        bool synced = false;
+        ~Owner() {
+            if (c->lent && !synced) (void)hipStreamSynchronize(c->stream);
+            free_ctx(c);  // host side only: every device pointer of c lies in the scratch
+        }
+    } owner{c};
+    c->hp = h;
+    c->stream = reinterpret_cast<hipStream_t>(hip_stream);
+    c->device = dev;
+    if ((st = layout_context(c, shape, 1)) != JORGE_OK) return st;
+    // Everything below lies in the scratch: the arena at its start, then the
+    // split workspace, then the launch tables.
+    c->lent = true;
+    c->arena = base;
+    std::vector<LayerDev> ld;
+    std::vector<FactorDev> fd;
+    if ((st = tables_context(c, ld, fd)) != JORGE_OK) return st;
+    const size_t arena = (size_t)round_up((int64_t)c->arena_bytes, kAlign);
+    const size_t split = (size_t)round_up(c->splitws_blocks * kSplitBlock * (int64_t)sizeof(float), kAlign);
+    const size_t need = arena + split + tables_bytes(c, ld, fd);
+    if (need > (size_t)JORGE_NOALLOC_SCRATCH_BYTES) {
+        char msg[160];
+        std::snprintf(msg, sizeof msg, "jorge_step_noalloc: a %lld x %lld layer needs %zu bytes of scratch, above %lld",
+                      (long long)shape->rows, (long long)shape->cols, need, (long long)JORGE_NOALLOC_SCRATCH_BYTES);
+        return fail(c, JORGE_ERR_UNSUPPORTED, msg);
+    }
+    c->splitws = c->splitws_blocks > 0 ? reinterpret_cast<float*>(base + arena) : nullptr;
+    c->pool = base + arena + split;
+    c->pool_bytes = JORGE_NOALLOC_SCRATCH_BYTES - arena - split;
+    // The scratch keeps the last call's contents: the arena's padding and
+    // partial sums must start at zero.
+    const size_t words = c->arena_bytes / 16;
+    hipLaunchKernelGGL(zero_kernel, dim3((unsigned)std::min<size_t>((words + kEwThreads - 1) / kEwThreads, 4096)),
+                       dim3(kEwThreads), 0, c->stream, reinterpret_cast<f32x4*>(base), words);
+    JORGE_HIP(c, hipGetLastError());
+    if ((st = upload_tables(c, ld, fd)) != JORGE_OK) return st;
+    // The caller's state in (dense row-major) and, after the step, out.
+    const auto& Lh = c->layers[0];
+    const int m = Lh.m, n = Lh.n;
+    float* const A[2] = {at<float>(c, c->factors[Lh.fL].off_A), at<float>(c, c->factors[Lh.fR].off_A)};
+    float* const U[2] = {L, R};
+    const int dims[2] = {m, n}, lds[2] = {Lh.mp, Lh.np};
+    float* const mm = at<float>(c, Lh.off_mom);
+    float* const ms = at<float>(c, Lh.off_msgd);
+    const size_t mn = (size_t)m * n * sizeof(float);
+    for (int s = 0; s < 2; ++s)
+        JORGE_HIP(c, hipMemcpy2DAsync(A[s], lds[s] * sizeof(float), U[s], dims[s] * sizeof(float),
+                                      dims[s] * sizeof(float), dims[s], hipMemcpyDeviceToDevice, c->stream));
+    JORGE_HIP(c, hipMemcpyAsync(mm, mom, mn, hipMemcpyDeviceToDevice, c->stream));
+    JORGE_HIP(c, hipMemcpyAsync(ms, mom_sgd, mn, hipMemcpyDeviceToDevice, c->stream));
+    float* const params[1] = {theta};
+    const float* const grads[1] = {grad};
+    if ((st = launch_step(c, params, grads, t, lr, beta2, beta1, weight_decay)) != JORGE_OK) return st;
+    for (int s = 0; s < 2; ++s)
+        JORGE_HIP(c, hipMemcpy2DAsync(U[s], dims[s] * sizeof(float), A[s], lds[s] * sizeof(float),
+                                      dims[s] * sizeof(float), dims[s], hipMemcpyDeviceToDevice, c->stream));
+    JORGE_HIP(c, hipMemcpyAsync(mom, mm, mn, hipMemcpyDeviceToDevice, c->stream));
+    JORGE_HIP(c, hipMemcpyAsync(mom_sgd, ms, mn, hipMemcpyDeviceToDevice, c->stream));
+    // The host tables the copies above read, and the scratch, are reused once this returns.
+    JORGE_HIP(c, hipStreamSynchronize(c->stream));
+    owner.synced = true;
     return JORGE_OK;
 }
 

@@ -17,6 +17,13 @@ __device__ __forceinline__ double wave_sum_array(const double* __restrict__ x, i
     return wave_sum(v);
 }
 
+// Zeroes n 16-byte words (a fill kernel rather than a memset, so that the
+// clearing is an ordinary kernel node if the caller captures it).
+__global__ __launch_bounds__(kEwThreads) void zero_kernel(f32x4* __restrict__ p, size_t n) {
+    const f32x4 z = {0.0f, 0.0f, 0.0f, 0.0f};
+    for (size_t i = (size_t)blockIdx.x * kEwThreads + threadIdx.x; i < n; i += (size_t)gridDim.x * kEwThreads) p[i] = z;
+}
+
 // A_hat = eps^(-1/4) I on the valid diagonal of every factor (the arena is zeroed before).
 __global__ void init_factors_kernel(const FactorDev* __restrict__ f, float l0) {
     const FactorDev F = f[blockIdx.x];

@@ -53,6 +53,9 @@ _SIGNATURES = {
                                            ctypes.POINTER(ctypes.c_int64), ctypes.c_int32]),
     "jorge_step": (ctypes.c_int32, [_P, ctypes.POINTER(_P), ctypes.POINTER(_P), ctypes.c_double,
                                     ctypes.c_double, ctypes.c_double, ctypes.c_double]),
+    "jorge_step_noalloc": (ctypes.c_int32, [ctypes.POINTER(Shape), ctypes.POINTER(HParams), ctypes.c_int64, _P, _P,
+                                            _P, _P, _P, _P, ctypes.c_double, ctypes.c_double, ctypes.c_double,
+                                            ctypes.c_double, _P]),
     "jorge_get_state": (ctypes.c_int32, [_P, ctypes.c_int32, ctypes.c_int32, _P, ctypes.c_int64]),
     "jorge_set_state": (ctypes.c_int32, [_P, ctypes.c_int32, ctypes.c_int32, _P, ctypes.c_int64]),
     "jorge_state_ptr": (ctypes.c_int32, [_P, ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(_P),
@@ -198,6 +201,28 @@ class Jorge:
         """Same as step, from prebuilt ctypes pointer arrays (no per-call checks)."""
         _check(self.lib, self.lib.jorge_step(self.ctx, param_ptrs, grad_ptrs, float(lr), float(beta2),
                                              float(beta1), float(weight_decay)), self.ctx)
+
+    @staticmethod
+    def step_noalloc(t, theta, grad, L, R, mom, mom_sgd, lr, beta2=0.9, beta1=0.9, weight_decay=0.0, stream=None,
+                     **hp):
+        """One step of one layer through jorge_step_noalloc: the caller's tensors hold the state
+        (L, R, mom, mom_sgd updated in place with theta); temporaries live in the library's static
+        device scratch. t: the number of this step (>= 1). Returns after the step has run."""
+        import torch
+        lib = load_library()
+        m, n = theta.shape
+        for x, shp in ((theta, (m, n)), (grad, (m, n)), (L, (m, m)), (R, (n, n)), (mom, (m, n)),
+                       (mom_sgd, (m, n))):
+            if not (isinstance(x, torch.Tensor) and x.is_cuda and x.dtype == torch.float32 and x.is_contiguous()
+                    and tuple(x.shape) == shp):
+                raise ValueError(f"need a contiguous fp32 cuda tensor of shape {shp}")
+        shape = Shape(m, n)
+        h = Jorge.hparams(**hp)
+        s = _current_stream() if stream is None else int(stream)
+        _check(lib, lib.jorge_step_noalloc(ctypes.byref(shape), ctypes.byref(h), int(t), _P(theta.data_ptr()),
+                                           _P(grad.data_ptr()), _P(L.data_ptr()), _P(R.data_ptr()),
+                                           _P(mom.data_ptr()), _P(mom_sgd.data_ptr()), float(lr), float(beta2),
+                                           float(beta1), float(weight_decay), _P(s)))
 
     @staticmethod
     def pointer_array(tensors):
