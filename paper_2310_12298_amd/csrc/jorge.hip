@@ -123,7 +123,9 @@ struct LayerHost {
 };
 
 // One factor: A (d x d) with statistic H H^T, H being d x k.
-//   explicit workspace: w[0] M then P^T, w[1] A^2 then X, w[2] A^4 then Z, w[3] X^T (dp x dp each)
+//   explicit workspace: w[0] M (kept until the next step's gram level: a factored factor of the
+//   same layer reads it as its H^T H), w[1] A^2, then X, then Z, w[2] A^4 then P^T (with the cubic
+//   term, V^T), w[3] X^T (with the cubic term, then P^T) (dp x dp each)
 //   factored workspace: w[0], w[1] kp x dp (Yt_j, A^5 H, W), w[2] Q = H^T H, w[3] S (kp x kp),
 //   and with series order 3 s2: b S - e S^2 (kp x kp)
 struct FactorHost {
@@ -807,27 +809,30 @@ void add_explicit(jorge_ctx* c, const FactorHost& F, const FactorDev& fd, const 
     x.C = W1; x.ldc = dp; x.C2 = W3; x.ldc2 = dp;
     x.flags = EF_STORE | EF_STORE_T | EF_NORM; x.partials = fd.partials;
     add_problem(c->nt[ST_XFORM], x, 2 * d * d * d);
+    float* Pt;  // P^T, the K-major B of A P
     if (c->hp.series_order == 3) {
         // V = b X - e X X, stored transposed over A^4 (the K-major B of X V) ...
         GemmProblem v = product(W1, dp, W3, dp, dp, dp, dp);
         v.C2 = W2; v.ldc2 = dp; v.X = W1; v.ldx = dp; v.sc = fd.sc;
         v.flags = EF_STORE_T | EF_READX; v.coef = CO_VSER;
         add_problem(c->nt[ST_POLY], v, 2 * d * d * d);
-        // ... then P = I - a X + X V, stored transposed.
+        // ... then P = I - a X + X V, stored transposed over X^T.
         GemmProblem p = product(W1, dp, W2, dp, dp, dp, dp);
-        p.C2 = W0; p.ldc2 = dp; p.X = W1; p.ldx = dp; p.sc = fd.sc;
+        p.C2 = W3; p.ldc2 = dp; p.X = W1; p.ldx = dp; p.sc = fd.sc;
         p.flags = EF_STORE_T | EF_READX; p.coef = CO_POLY3; p.valid_m = p.valid_n = F.d;
         add_problem(c->nt[ST_POLY2], p, 2 * d * d * d);
+        Pt = W3;
     } else {
-        // P = I - a X + b X X, stored transposed (the K-major B of the next product).
+        // P = I - a X + b X X, stored transposed over A^4.
         GemmProblem p = product(W1, dp, W3, dp, dp, dp, dp);
-        p.C2 = W0; p.ldc2 = dp; p.X = W1; p.ldx = dp; p.sc = fd.sc;
+        p.C2 = W2; p.ldc2 = dp; p.X = W1; p.ldx = dp; p.sc = fd.sc;
         p.flags = EF_STORE_T | EF_READX; p.coef = CO_POLY; p.valid_m = p.valid_n = F.d;
         add_problem(c->nt[ST_POLY], p, 2 * d * d * d);
+        Pt = W2;
     }
-    // Z = s A P
-    GemmProblem z = product(A, dp, W0, dp, dp, dp, dp);
-    z.C = W2; z.ldc = dp; z.sc = fd.sc; z.flags = EF_STORE; z.coef = CO_SCALE;
+    // Z = s A P, over X
+    GemmProblem z = product(A, dp, Pt, dp, dp, dp, dp);
+    z.C = W1; z.ldc = dp; z.sc = fd.sc; z.flags = EF_STORE; z.coef = CO_SCALE;
     add_problem(c->nt[ST_UPDATE], z, 2 * d * d * d);
     const int fi = (int)(&F - &c->factors[0]);
     for (int ti = 0; ti * 64 < dp; ++ti)
@@ -838,7 +843,7 @@ void add_explicit(jorge_ctx* c, const FactorHost& F, const FactorDev& fd, const 
 // Hr: H row-major (dp x kp, ld kp); Ht: H^T row-major (kp x dp, ld dp).
 // Mo: the other factor's statistic when that factor is in the explicit order
 // (H^T H is exactly it: G^T G for L_hat, G G^T for R_hat; kp x kp, ld kp,
-// computed in the gram level and kept until poly), or null.
+// computed in the gram level and kept until the next step's), or null.
 int add_factored(jorge_ctx* c, const FactorHost& F, const FactorDev& fd, const float* Hr, const float* Ht,
                  const float* Mo) {
     const bool sym = c->hp.symmetrize != 0;
@@ -974,7 +979,7 @@ void build_tables(jorge_ctx* c, std::vector<LayerDev>& ld, std::vector<FactorDev
         d.A = at<float>(c, F.off_A);
         d.sc = at<FactorScalars>(c, F.off_sc);
         d.partials = at<double>(c, F.off_part);
-        d.Z = (F.expl && !F.chain) ? at<float>(c, F.off_w[2]) : nullptr;
+        d.Z = (F.expl && !F.chain) ? at<float>(c, F.off_w[1]) : nullptr;
         const auto& L = c->layers[F.layer];
         d.H = at<float>(c, F.side == 0 ? L.off_Gp : L.off_Gpt);
         d.d = F.d;
@@ -1039,9 +1044,9 @@ void build_tables(jorge_ctx* c, std::vector<LayerDev>& ld, std::vector<FactorDev
         } else {
             const auto& L = c->layers[F.layer];
             const FactorHost& O = c->factors[F.side == 0 ? L.fR : L.fL];
-            // (Not for a low-rank-preconditioning factor: it reads Q after the poly level,
-            // where the explicit factor's statistic buffer receives P^T.)
-            const float* Mo = (O.expl && !O.chain && !F.lrp) ? at<float>(c, O.off_w[0]) : nullptr;
+            // (The explicit factor keeps its statistic until the next step's gram level,
+            // past the low-rank preconditioning that reads Q.)
+            const float* Mo = (O.expl && !O.chain) ? at<float>(c, O.off_w[0]) : nullptr;
             F.nparts = add_factored(c, F, fd[fi], Hr, Ht, Mo);
             fd[fi].nparts = F.nparts;
         }

@@ -67,6 +67,8 @@ def main():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--intervals", default="50,1", help="Jorge preconditioner update intervals to time")
+    ap.add_argument("--repeats", type=int, default=3,
+                    help="rounds of (SGD, Jorge at each interval), interleaved in one process; medians reported")
     args = ap.parse_args()
 
     import torch
@@ -114,19 +116,31 @@ def main():
         return ms, n2d
 
     out = {"metric": "ResNet-50 training iteration time (one data-parallel rank)", "unit": "ms/iteration",
-           "batch_per_gpu": args.batch, "steps": args.steps, "warmup": args.warmup, "dtype": "bf16 autocast",
-           "data": "synthetic", "results": {}}
-    sgd_ms, _ = run(lambda m: torch.optim.SGD(m.parameters(), foreach=True, **sgd_hp), "sgd")
-    out["results"]["sgd"] = {"ms_per_iteration": sgd_ms, "images_per_s": args.batch / sgd_ms * 1e3}
+           "batch_per_gpu": args.batch, "steps": args.steps, "warmup": args.warmup, "repeats": args.repeats,
+           "dtype": "bf16 autocast", "data": "synthetic", "results": {}}
     jhp = sgd_to_jorge(sgd_hp["lr"], sgd_hp["momentum"], sgd_hp["weight_decay"])
-    for k in [int(v) for v in args.intervals.split(",") if v]:
-        ms, n2d = run(lambda m: JorgeOptimizer(m.parameters(), lr=jhp["lr"], beta1=jhp["beta1"],
-                                               weight_decay=jhp["weight_decay"],
-                                               vector_weight_decay=sgd_hp["weight_decay"],
-                                               precond_interval=k), f"jorge k={k}")
-        out["results"][f"jorge_k{k}"] = {"ms_per_iteration": ms, "images_per_s": args.batch / ms * 1e3,
-                                         "overhead_vs_sgd_pct": 100.0 * (ms - sgd_ms) / sgd_ms,
-                                         "matrix_params": n2d}
+    intervals = [int(v) for v in args.intervals.split(",") if v]
+    runs = {"sgd": []}
+    runs.update({f"jorge_k{k}": [] for k in intervals})
+    n2d = None
+    # Rounds interleave the optimizers, so drifts of the clock or of the box hit all of them alike.
+    for r in range(args.repeats):
+        runs["sgd"].append(run(lambda m: torch.optim.SGD(m.parameters(), foreach=True, **sgd_hp), f"sgd #{r}")[0])
+        for k in intervals:
+            ms, n2d = run(lambda m: JorgeOptimizer(m.parameters(), lr=jhp["lr"], beta1=jhp["beta1"],
+                                                   weight_decay=jhp["weight_decay"],
+                                                   vector_weight_decay=sgd_hp["weight_decay"],
+                                                   precond_interval=k), f"jorge k={k} #{r}")
+            runs[f"jorge_k{k}"].append(ms)
+    med = {name: sorted(v)[len(v) // 2] for name, v in runs.items()}
+    for name, v in runs.items():
+        e = {"ms_per_iteration": med[name], "runs_ms": v, "images_per_s": args.batch / med[name] * 1e3}
+        if name != "sgd":
+            e["overhead_vs_sgd_pct"] = 100.0 * (med[name] - med["sgd"]) / med["sgd"]
+            # per round, against that round's SGD run
+            e["overhead_per_round_pct"] = [100.0 * (a - b) / b for a, b in zip(v, runs["sgd"])]
+            e["matrix_params"] = n2d
+        out["results"][name] = e
     print(json.dumps(out), flush=True)
     return 0
 
