@@ -55,12 +55,9 @@ def step_bytes(shapes, update):
     return sum(4 * (7 * m * n + (2 if update else 1) * (m * m + n * n)) for m, n in shapes)
 
 
-# Committed rocprofv3 summaries that carry HBM counter figures for a workload.
-PROFILES = {"resnet50": os.path.join(ROOT, "profiles", "gemm_grouped_resnet50.md")}
-
-
 def profile_path(config):
-    return PROFILES.get(config, os.path.join(ROOT, "profiles", f"jorge_step_{config}.md"))
+    """The committed rocprofv3 summary of a workload, which carries its HBM counter figures."""
+    return os.path.join(ROOT, "profiles", f"jorge_step_{config}.md")
 
 
 # The sources that decide what the grouped GEMM runs: the kernel itself and the
@@ -304,6 +301,7 @@ def summary(res):
             "ms_per_step": res["ms_per_step"], "gemm_frac": res["gemm"]["achieved"] / PEAK_FP32_MFMA_TFLOPS,
             "gemm_tflops": res["gemm"]["achieved"], "step_roofline_frac": res["step_roofline"]["frac"],
             "step_roofline_bound": res["step_roofline"]["bound"], "factors": res["forms"],
+            "hbm_frac": {k: v["frac"] for k, v in res["hbm"].items()},
             "traffic_bytes_per_launch": measured_traffic(res["config"])}
 
 
