@@ -361,9 +361,14 @@ __device__ __forceinline__ void gemm_mainloop(const GemmProblem& p, int tm, int 
     finish_slab<BK>(s0, rb);
     float fa[4][4], fb[4][4];
     group_fragments<AK, BK>(s0.a, s0.b, wy, wx, lane, 0, fa, fb);
-    // On a diagonal tile of a symmetric result the quadrant below the
-    // diagonal is not needed and the diagonal quadrants only on and above it.
-    if (p.upper && tm == tn) {
+    // A quadrant that lies wholly past the product's padded extent (a product
+    // 32 or 64 rows or columns wide, or an edge tile) multiplies nothing: its
+    // outputs are discarded. On a diagonal tile of a symmetric result the
+    // quadrant below the diagonal is not needed and the diagonal quadrants
+    // only on and above it.
+    if (row0 + wy * 64 >= p.M || col0 + wx * 64 >= p.N) {
+        slab_loop<AK, BK, BS_NONE>(p, tl, col0, k0, nk, s0, s1, rb, wy, wx, lane, fa, fb, acc);
+    } else if (p.upper && tm == tn) {
         if (wy > wx) slab_loop<AK, BK, BS_NONE>(p, tl, col0, k0, nk, s0, s1, rb, wy, wx, lane, fa, fb, acc);
         else if (wy == wx) slab_loop<AK, BK, BS_UPPER>(p, tl, col0, k0, nk, s0, s1, rb, wy, wx, lane, fa, fb, acc);
         else slab_loop<AK, BK, BS_ALL>(p, tl, col0, k0, nk, s0, s1, rb, wy, wx, lane, fa, fb, acc);
@@ -706,22 +711,23 @@ __device__ __forceinline__ void small_fragment(const float* s, int mn, int k, fl
 // The MFMAs of one small-mode slab: lane l contributes k = 4 (l / 16) + s
 // to step s, for A and B alike (as in mma_slab). UPPER: a block on the
 // diagonal of a symmetric result, whose 16 x 16 blocks below the diagonal are
-// left out.
-template <bool UPPER>
+// left out. BI x BJ: the 16 x 16 blocks of the 64 x 64 block that lie inside
+// the product (a product 32 rows or columns wide fills half of it; the
+// others are left out rather than computed from padding and discarded).
+template <bool UPPER, int BI, int BJ>
 __device__ __forceinline__ void small_mma(const float* sa, const float* sb, int lane, f32x4 (&acc)[16]) {
     const int r = lane & 15, g = lane >> 4;
-    float a[4][4], b[4][4];
+    float a[BI][4], b[BJ][4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        small_fragment(sa, i * 16 + r, g * 4, a[i]);
-        small_fragment(sb, i * 16 + r, g * 4, b[i]);
-    }
+    for (int i = 0; i < BI; ++i) small_fragment(sa, i * 16 + r, g * 4, a[i]);
+#pragma unroll
+    for (int j = 0; j < BJ; ++j) small_fragment(sb, j * 16 + r, g * 4, b[j]);
 #pragma unroll
     for (int st = 0; st < 4; ++st)
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < BI; ++i)
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
+            for (int j = 0; j < BJ; ++j)
                 if (!UPPER || i <= j)
                     acc[i * 4 + j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i][st], b[j][st], acc[i * 4 + j], 0, 0, 0);
 }
@@ -733,21 +739,13 @@ __device__ __forceinline__ void small_issue(const GemmProblem& p, int row0, int 
     small_load(src.b, src.ldb, col0, p.N, src.k, s + kSmallOperand);
 }
 
-// One small-mode block, computed by the calling wave alone in its own LDS
-// stages s0, s1 (2 x 64 x 16 floats each), with no workgroup barrier: slab
-// k + 1 loads while slab k is multiplied. Then the epilogue of the block's
-// quadrant, and the zeroing of the partial sums of its tile's quadrants that
-// no block computes.
-__device__ __forceinline__ void small_unit(const GemmProblem& p, const SmallUnit& su, float* s0, float* s1,
-                                           float beta1, int lane) {
-    f32x4 acc[16];
-#pragma unroll
-    for (int b = 0; b < 16; ++b)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) acc[b][e] = 0.0f;
-    const int row0 = su.bm * kSmallDim, col0 = su.bn * kSmallDim;
-    const int nk = p.K / kSmallSlab;
-    const bool diag = p.upper && su.bm == su.bn;   // uniform: the block is read with scalar loads
+// The K loop of a small-mode block computed by the calling wave alone in its
+// own LDS stages s0, s1 (2 x 64 x 16 floats each), with no workgroup barrier:
+// slab k + 1 loads while slab k is multiplied. One copy per block shape, so
+// the loop has no branches on it.
+template <bool UPPER, int BI, int BJ>
+__device__ __forceinline__ void small_loop(const GemmProblem& p, int row0, int col0, int nk, float* s0, float* s1,
+                                           int lane, f32x4 (&acc)[16]) {
     small_issue(p, row0, col0, 0, s0);
     for (int kt = 0; kt < nk; ++kt) {
         float* cur = (kt & 1) ? s1 : s0;
@@ -760,8 +758,37 @@ __device__ __forceinline__ void small_unit(const GemmProblem& p, const SmallUnit
         } else {
             asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         }
-        if (diag) small_mma<true>(cur, cur + kSmallOperand, lane, acc);
-        else small_mma<false>(cur, cur + kSmallOperand, lane, acc);
+        small_mma<UPPER, BI, BJ>(cur, cur + kSmallOperand, lane, acc);
+    }
+}
+
+// One small-mode block: its K loop, then the epilogue of the block's
+// quadrant, and the zeroing of the partial sums of its tile's quadrants that
+// no block computes. The block's shape (on the diagonal of a symmetric
+// result or not; 2 or 4 of its 16-row and 16-column strips inside the
+// product) is uniform over the wave and picks the loop once.
+__device__ __forceinline__ void small_unit(const GemmProblem& p, const SmallUnit& su, float* s0, float* s1,
+                                           float beta1, int lane) {
+    f32x4 acc[16];
+#pragma unroll
+    for (int b = 0; b < 16; ++b)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[b][e] = 0.0f;
+    const int row0 = su.bm * kSmallDim, col0 = su.bn * kSmallDim;
+    const int nk = p.K / kSmallSlab;
+    const bool diag = p.upper && su.bm == su.bn;   // uniform: the block is read with scalar loads
+    // Strips inside the product: M and N are multiples of 32.
+    const int bi = min(4, (p.M - row0) / 16), bj = min(4, (p.N - col0) / 16);
+    if (diag) {
+        if (bi == 4 && bj == 4) small_loop<true, 4, 4>(p, row0, col0, nk, s0, s1, lane, acc);
+        else if (bi == 4) small_loop<true, 4, 2>(p, row0, col0, nk, s0, s1, lane, acc);
+        else if (bj == 4) small_loop<true, 2, 4>(p, row0, col0, nk, s0, s1, lane, acc);
+        else small_loop<true, 2, 2>(p, row0, col0, nk, s0, s1, lane, acc);
+    } else {
+        if (bi == 4 && bj == 4) small_loop<false, 4, 4>(p, row0, col0, nk, s0, s1, lane, acc);
+        else if (bi == 4) small_loop<false, 4, 2>(p, row0, col0, nk, s0, s1, lane, acc);
+        else if (bj == 4) small_loop<false, 2, 4>(p, row0, col0, nk, s0, s1, lane, acc);
+        else small_loop<false, 2, 2>(p, row0, col0, nk, s0, s1, lane, acc);
     }
     const int quadrant = ((su.bm & 1) << 1) | (su.bn & 1);
     gemm_epilogue(p, su.bm >> 1, su.bn >> 1, su.slot, beta1, acc, lane, quadrant);
