@@ -242,7 +242,9 @@ jorge_status jorge_get_state(jorge_ctx* ctx, int32_t layer, int32_t kind, float*
 
 /* Overwrites one state tensor from src, a device buffer with row stride
  * ld_src >= its columns (for checkpoint restore and state injection). The
- * caller keeps factors symmetric if it relies on symmetry. Stream-ordered. */
+ * caller keeps factors symmetric if it relies on symmetry. A factor's storage
+ * padding (rows and columns past its size) is reset to zeros as well, so a
+ * restore also undoes a step that met non-finite values. Stream-ordered. */
 jorge_status jorge_set_state(jorge_ctx* ctx, int32_t layer, int32_t kind, const float* src,
                              int64_t ld_src);
 
@@ -262,6 +264,19 @@ jorge_status jorge_set_step(jorge_ctx* ctx, int64_t t);
 /* Diagnostics of the last step for one layer: out[JORGE_DIAG_COUNT] on the
  * host. Synchronises the context's stream. */
 jorge_status jorge_read_diag(jorge_ctx* ctx, int32_t layer, double* out);
+
+/* Non-finite gradients (failure detection). A step sets a layer's flag in
+ * device memory when the fp64 norm ||m_SGD||_F that it sums for the grafting
+ * anyway comes out non-finite (no host synchronisation, no extra pass over
+ * G). Any NaN or infinity in the layer's gradient does that, through m_SGD =
+ * beta1 m_SGD + G (Algorithm 3); so does an m_SGD element that overflows fp32.
+ * The step itself runs to its end; the layer's m_SGD, m and parameters
+ * are then non-finite, and stay so in later steps until the caller restores
+ * its state (jorge_set_state, jorge_set_step). This call synchronises the
+ * context's stream, sets *count to the number of layers flagged by any step
+ * since the context was created or this call last ran, and *first (if not
+ * NULL) to the lowest such layer index or -1, then clears the flags. */
+jorge_status jorge_nonfinite(jorge_ctx* ctx, int32_t* count, int32_t* first);
 
 /* Changes the stream later calls queue on (NULL = the null stream). Work
  * queued later on the new stream waits for everything already queued on the

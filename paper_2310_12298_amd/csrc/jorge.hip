@@ -160,6 +160,7 @@ struct jorge_ctx {
     std::vector<FactorHost> factors;
     char* arena = nullptr;
     size_t arena_bytes = 0;
+    size_t off_nonfinite = 0;  // int per layer (count rounded up to 4): non-finite ||m_SGD|| seen
     std::vector<std::pair<size_t, size_t>> regions;  // (offset, bytes) of every arena buffer
     // device tables
     LayerDev* dlayers = nullptr;
@@ -216,7 +217,11 @@ jorge_status fail(jorge_ctx* c, jorge_status s, const std::string& msg) {
     return s;
 }
 
+// A failed runtime call is reported once, here: its error is also taken off
+// the runtime's last-error state (where a later launch check would find it
+// again); errors that stay with the device, such as a fault, remain.
 jorge_status hip_fail(jorge_ctx* c, hipError_t e, const char* what) {
+    (void)hipGetLastError();
     std::string msg = std::string(what) + ": " + hipGetErrorString(e);
     return fail(c, e == hipErrorOutOfMemory ? JORGE_ERR_OUT_OF_MEMORY : JORGE_ERR_HIP, msg);
 }
@@ -777,6 +782,7 @@ size_t plan(jorge_ctx* c) {
         L.off_part_sgd = take((size_t)L.n_part_sgd * sizeof(double));
         L.off_ls = take(sizeof(LayerScalars));
     }
+    c->off_nonfinite = take(round_up((int64_t)c->layers.size(), 4) * sizeof(int));
     return off;
 }
 
@@ -1001,6 +1007,7 @@ void build_tables(jorge_ctx* c, std::vector<LayerDev>& ld, std::vector<FactorDev
         d.part_m = at<double>(c, L.off_part_m);
         d.part_sgd = at<double>(c, L.off_part_sgd);
         d.ls = at<LayerScalars>(c, L.off_ls);
+        d.nonfinite = at<int>(c, c->off_nonfinite) + li;
         d.m = L.m; d.n = L.n; d.mp = L.mp; d.np = L.np;
         d.n_part_m = L.n_part_m;
         d.n_part_sgd = L.n_part_sgd;
@@ -1596,15 +1603,20 @@ jorge_status jorge_create(const jorge_shape* shapes, int32_t num_layers, const j
     };
     if ((st = layout_context(c, shapes, num_layers)) != JORGE_OK) return bail(st);
     if (hipGetDevice(&c->device) != hipSuccess) return bail(JORGE_ERR_HIP);
+    // As in hip_fail: the failed allocation's error leaves the last-error state.
+    auto alloc_failed = [&](hipError_t err) {
+        (void)hipGetLastError();
+        return bail(err == hipErrorOutOfMemory ? JORGE_ERR_OUT_OF_MEMORY : JORGE_ERR_HIP);
+    };
     hipError_t e = hipMalloc(reinterpret_cast<void**>(&c->arena), c->arena_bytes);
-    if (e != hipSuccess) return bail(e == hipErrorOutOfMemory ? JORGE_ERR_OUT_OF_MEMORY : JORGE_ERR_HIP);
+    if (e != hipSuccess) return alloc_failed(e);
     if (hipMemsetAsync(c->arena, 0, c->arena_bytes, c->stream) != hipSuccess) return bail(JORGE_ERR_HIP);
     std::vector<LayerDev> ld;
     std::vector<FactorDev> fd;
     if ((st = tables_context(c, ld, fd)) != JORGE_OK) return bail(st);
     if (c->splitws_blocks > 0) {
         e = hipMalloc(reinterpret_cast<void**>(&c->splitws), (size_t)c->splitws_blocks * kSplitBlock * sizeof(float));
-        if (e != hipSuccess) return bail(e == hipErrorOutOfMemory ? JORGE_ERR_OUT_OF_MEMORY : JORGE_ERR_HIP);
+        if (e != hipSuccess) return alloc_failed(e);
     }
     if ((st = upload_tables(c, ld, fd)) != JORGE_OK) return bail(st);
     hipLaunchKernelGGL(init_factors_kernel, dim3((unsigned)c->factors.size()), dim3(256), 0, c->stream,
@@ -1795,6 +1807,15 @@ jorge_status jorge_set_state(jorge_ctx* c, int32_t layer, int32_t kind, const fl
     int64_t rows, cols, ld;
     state_view(c, layer, kind, &p, &rows, &cols, &ld);
     if (ld_src < cols) return fail(c, JORGE_ERR_INVALID_ARGUMENT, "jorge_set_state: ld_src < cols");
+    if ((kind == JORGE_STATE_L || kind == JORGE_STATE_R) && ld > cols) {
+        // A factor's padding rows and columns must hold zeros, which the step
+        // keeps; a step that met a non-finite value filled them with it
+        // (0 * NaN), so a restored factor gets them cleared too.
+        const size_t words = (size_t)ld * ld / 4;
+        hipLaunchKernelGGL(zero_kernel, dim3((unsigned)std::min<size_t>((words + kEwThreads - 1) / kEwThreads, 4096)),
+                           dim3(kEwThreads), 0, c->stream, reinterpret_cast<f32x4*>(p), words);
+        JORGE_HIP(c, hipGetLastError());
+    }
     JORGE_HIP(c, hipMemcpy2DAsync(p, ld * sizeof(float), src, ld_src * sizeof(float), cols * sizeof(float),
                                   rows, hipMemcpyDeviceToDevice, c->stream));
     return JORGE_OK;
@@ -1839,6 +1860,33 @@ jorge_status jorge_read_diag(jorge_ctx* c, int32_t layer, double* out) {
     out[JORGE_DIAG_NORM_M] = ls.norm_m;
     out[JORGE_DIAG_NORM_SGD] = ls.norm_sgd;
     out[JORGE_DIAG_STEP] = ls.g;
+    return JORGE_OK;
+}
+
+jorge_status jorge_nonfinite(jorge_ctx* c, int32_t* count, int32_t* first) {
+    if (!c || !count) return JORGE_ERR_INVALID_ARGUMENT;
+    const size_t nl = c->layers.size(), words = (nl + 3) / 4;
+    std::vector<int> flags;
+    try {
+        flags.assign(nl, 0);
+    } catch (const std::bad_alloc&) {
+        return JORGE_ERR_OUT_OF_MEMORY;
+    }
+    // Read, then clear behind the read on the same stream.
+    JORGE_HIP(c, hipMemcpyAsync(flags.data(), at<int>(c, c->off_nonfinite), nl * sizeof(int), hipMemcpyDeviceToHost,
+                                c->stream));
+    hipLaunchKernelGGL(zero_kernel, dim3((unsigned)((words + kEwThreads - 1) / kEwThreads)), dim3(kEwThreads), 0,
+                       c->stream, at<f32x4>(c, c->off_nonfinite), words);
+    JORGE_HIP(c, hipGetLastError());
+    JORGE_HIP(c, hipStreamSynchronize(c->stream));
+    int32_t n = 0, f = -1;
+    for (size_t i = 0; i < nl; ++i)
+        if (flags[i]) {
+            if (f < 0) f = (int32_t)i;
+            ++n;
+        }
+    *count = n;
+    if (first) *first = f;
     return JORGE_OK;
 }
 

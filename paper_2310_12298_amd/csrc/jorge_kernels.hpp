@@ -656,6 +656,9 @@ __global__ void layer_finalize_kernel(const LayerDev* __restrict__ layers, doubl
     const double nm = sqrt(wave_sum_array(L.part_m, L.n_part_m * kWaveSlots));
     const double ns = sqrt(wave_sum_array(L.part_sgd, L.n_part_sgd));
     if (threadIdx.x != 0) return;
+    // A NaN or infinity anywhere in this step's G reaches m_SGD = beta1 m_SGD + G,
+    // and with it this norm: the layer's flag records it for the host.
+    if (!isfinite(ns)) *L.nonfinite = 1;
     double g = lr;
     if (graft) g = nm > 0.0 ? lr * ns / nm : 0.0;
     LayerScalars out;

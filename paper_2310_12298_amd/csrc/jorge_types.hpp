@@ -158,6 +158,7 @@ struct LayerDev {
     double* part_m;        // sums of m_ij^2: kWaveSlots per tile slot
     double* part_sgd;      // per-block sums of m_SGD,ij^2
     LayerScalars* ls;
+    int* nonfinite;        // set to 1 by a step whose ||m_SGD|| is not finite; cleared by the host
     int m, n, mp, np;
     int n_part_m, n_part_sgd;
 };

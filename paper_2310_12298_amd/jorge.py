@@ -63,6 +63,7 @@ _SIGNATURES = {
     "jorge_get_step": (ctypes.c_int32, [_P, ctypes.POINTER(ctypes.c_int64)]),
     "jorge_set_step": (ctypes.c_int32, [_P, ctypes.c_int64]),
     "jorge_read_diag": (ctypes.c_int32, [_P, ctypes.c_int32, ctypes.POINTER(ctypes.c_double)]),
+    "jorge_nonfinite": (ctypes.c_int32, [_P, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32)]),
     "jorge_set_stream": (ctypes.c_int32, [_P, _P]),
     "jorge_synchronize": (ctypes.c_int32, [_P]),
     "jorge_device_bytes": (ctypes.c_int32, [_P, ctypes.POINTER(ctypes.c_int64)]),
@@ -273,6 +274,13 @@ class Jorge:
         out = (ctypes.c_double * len(DIAG_NAMES))()
         _check(self.lib, self.lib.jorge_read_diag(self.ctx, layer, out), self.ctx)
         return dict(zip(DIAG_NAMES, list(out)))
+
+    def nonfinite(self):
+        """(count, first): layers whose gradient held a NaN or an infinity in any step since the
+        last call (first = the lowest such layer, -1 if none); clears the flags. Synchronises."""
+        n, f = ctypes.c_int32(), ctypes.c_int32()
+        _check(self.lib, self.lib.jorge_nonfinite(self.ctx, ctypes.byref(n), ctypes.byref(f)), self.ctx)
+        return n.value, f.value
 
     def synchronize(self):
         _check(self.lib, self.lib.jorge_synchronize(self.ctx), self.ctx)

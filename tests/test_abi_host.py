@@ -98,6 +98,7 @@ def test_null_arguments(lib):
     assert lib.jorge_get_step(None, ctypes.byref(ctypes.c_int64())) == ERR_INVALID
     assert lib.jorge_set_step(None, 0) == ERR_INVALID
     assert lib.jorge_read_diag(None, 0, (ctypes.c_double * 7)()) == ERR_INVALID
+    assert lib.jorge_nonfinite(None, ctypes.byref(ctypes.c_int32()), None) == ERR_INVALID
     assert lib.jorge_set_stream(None, None) == ERR_INVALID
     assert lib.jorge_synchronize(None) == ERR_INVALID
     assert lib.jorge_device_bytes(None, ctypes.byref(ctypes.c_int64())) == ERR_INVALID
