@@ -1461,7 +1461,7 @@ jorge_status run_update(jorge_ctx* c, double beta2) {
     // The LDS chains: every factor of the context (the levels below are then empty).
     if (!c->chain2.empty()) {
         TimedLaunch tl(c, ST_LDS_CHAIN);
-        hipLaunchKernelGGL(lds_chain128_kernel, dim3((unsigned)c->chain2.size()), dim3(kGemmThreads), 0, c->stream,
+        hipLaunchKernelGGL(lds_chain128_kernel, dim3((unsigned)c->chain2.size()), dim3(kC2Threads), 0, c->stream,
                            c->dfactors, c->dchain2, beta2, (int)c->hp.beta_mode, (int)c->hp.series_order);
         tl.finish();
         JORGE_HIP(c, hipGetLastError());

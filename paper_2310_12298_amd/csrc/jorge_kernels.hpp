@@ -405,22 +405,27 @@ __global__ __launch_bounds__(kGemmThreads) void lds_chain_kernel(const FactorDev
 
 // ---------------------------------------------------------------- LDS chain, sizes 96 and 128
 // The same whole-factor update (explicit order of Algorithm 2, symmetric
-// factors) for padded sizes 64 < dp <= 128, by one workgroup of four waves.
-// Two dp x dp matrices stay in LDS and A is read from global memory when a
-// product needs it: M = H H^T (H streamed in 32-column slabs, the next slab
-// held in registers while the current one is multiplied), A^2, A^4,
-// X = A^4 M with ||X||_F, (beta, c, s) (Appendix A.1, Eq. 8-9),
+// factors) for padded sizes 64 < dp <= 128, by one workgroup of eight waves
+// (two per SIMD, so one wave's MFMAs run while the other waits at a barrier
+// or for memory). Two dp x dp matrices stay in LDS and A is read from global
+// memory when a product needs it: M = H H^T (H streamed in 32-column slabs,
+// the next slab held in registers while the current one is multiplied), A^2,
+// A^4, X = A^4 M with ||X||_F, (beta, c, s) (Appendix A.1, Eq. 8-9),
 // P = I - (c/4) X + (5c^2/32) X X (Eq. 6; with series order 3,
 // P = I - a X + X V, V = b X - e X X), Z = s A P and A <- (Z + Z^T)/2.
 // Every product is C = A B with both operands held as rows that are
 // contiguous in k: A's rows, and B's columns, i.e. the rows of B^T. The
 // symmetric operands (A, A^2, A^4, M) are their own transposes; X is stored
 // beside X^T, and P and V only transposed.
-// Each wave owns a 64 x 64 quadrant of the product as 4 x 4 blocks of
-// v_mfma_f32_16x16x4_f32; lane l reads 16 bytes of its row for k = k0 + 4 (l / 16)
-// .. + 3 and feeds them to the four steps of a 16-deep k group (A and B alike,
-// so every A[i][k] B[k][j] is formed once). Blocks outside dp are skipped.
+// Wave w owns the 64 x 32 piece at rows 64 (w / 4), columns 32 (w % 4) of
+// the product, as 4 x 2 blocks of v_mfma_f32_16x16x4_f32; lane l reads 16
+// bytes of its row for k = k0 + 4 (l / 16) .. + 3 and feeds them to the four
+// steps of a 16-deep k group (A and B alike, so every A[i][k] B[k][j] is
+// formed once). Blocks outside dp are skipped.
 constexpr int kChain2Max = 128;
+constexpr int kC2Threads = 512;          // eight waves
+constexpr int kC2Waves = kC2Threads / 64;
+constexpr int kC2PieceCols = 32;         // a wave's piece: 64 rows x 32 columns
 constexpr int kC2Ld = kChain2Max + 4;    // LDS row stride: 16-byte reads of 16 rows fall in distinct bank quads
 constexpr int kC2Mat = kChain2Max * kC2Ld;
 constexpr int kC2HLd = kSlab + 4;        // H slab row stride
@@ -429,12 +434,12 @@ struct Chain2Lds {
     float m0[kC2Mat];
     float m1[kC2Mat];
     float h[kChain2Max * kC2HLd];
-    double red[4];
+    double red[kC2Waves];
     float coef[4];  // a, b, s, e
 };
 
 // Fragments of one 16-deep k group: lane l's 16 bytes of rows 16 i + l % 16
-// of its quadrant (A) and of its columns (B), at k = k0 + 4 (l / 16) .. + 3.
+// of its piece (A) and of its columns (B), at k = k0 + 4 (l / 16) .. + 3.
 template <int NBI, int NBJ>
 __device__ __forceinline__ void c2_frags(const float* pa, int lda, const float* pb, int ldb, int k0, f32x4 (&fa)[NBI],
                                          f32x4 (&fb)[NBJ]) {
@@ -445,26 +450,26 @@ __device__ __forceinline__ void c2_frags(const float* pa, int lda, const float* 
 }
 
 template <int NBI, int NBJ>
-__device__ __forceinline__ void c2_group(const f32x4 (&fa)[NBI], const f32x4 (&fb)[NBJ], f32x4 (&acc)[16]) {
+__device__ __forceinline__ void c2_group(const f32x4 (&fa)[NBI], const f32x4 (&fb)[NBJ], f32x4 (&acc)[8]) {
 #pragma unroll
     for (int st = 0; st < 4; ++st)
 #pragma unroll
         for (int i = 0; i < NBI; ++i)
 #pragma unroll
             for (int j = 0; j < NBJ; ++j)
-                acc[i * 4 + j] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[i][st], fb[j][st], acc[i * 4 + j], 0, 0, 0);
+                acc[i * 2 + j] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[i][st], fb[j][st], acc[i * 2 + j], 0, 0, 0);
 }
 
 // acc += a (rows, stride lda) x b^T (rows, stride ldb) over k in [0, K) (K a
-// multiple of 32) for the NBI x NBJ blocks of the calling wave's quadrant
-// that lie inside the product. The next group's fragments are read while the
+// multiple of 32) for the NBI x NBJ blocks of the calling wave's piece that
+// lie inside the product. The next group's fragments are read while the
 // current group's MFMAs run.
 template <int NBI, int NBJ>
 __device__ __forceinline__ void c2_mma_t(const float* a, int lda, const float* b, int ldb, int K, int wy, int wx,
-                                         f32x4 (&acc)[16]) {
+                                         f32x4 (&acc)[8]) {
     const int lane = threadIdx.x & 63, r = lane & 15, q = lane >> 4;
     const float* pa = a + (wy * 64 + r) * lda + 4 * q;
-    const float* pb = b + (wx * 64 + r) * ldb + 4 * q;
+    const float* pb = b + (wx * kC2PieceCols + r) * ldb + 4 * q;
     f32x4 fa0[NBI], fb0[NBJ], fa1[NBI], fb1[NBJ];
     c2_frags<NBI, NBJ>(pa, lda, pb, ldb, 0, fa0, fb0);
     for (int k0 = 0; k0 < K; k0 += 32) {
@@ -478,36 +483,34 @@ __device__ __forceinline__ void c2_mma_t(const float* a, int lda, const float* b
     }
 }
 
-// The wave's part of a product: nbi x nbj (2 or 4 each, uniform per wave) of
-// its 4 x 4 blocks lie inside it; a wave with none returns.
+// The wave's part of a product: nbi (2 or 4) x 2 of its 4 x 2 blocks lie
+// inside it (uniform per wave); a wave with none returns.
 __device__ __forceinline__ void c2_mma(const float* a, int lda, const float* b, int ldb, int K, int wy, int wx,
-                                       int nbi, int nbj, f32x4 (&acc)[16]) {
-    if (nbi == 4 && nbj == 4) c2_mma_t<4, 4>(a, lda, b, ldb, K, wy, wx, acc);
-    else if (nbi == 4 && nbj == 2) c2_mma_t<4, 2>(a, lda, b, ldb, K, wy, wx, acc);
-    else if (nbi == 2 && nbj == 4) c2_mma_t<2, 4>(a, lda, b, ldb, K, wy, wx, acc);
-    else if (nbi == 2 && nbj == 2) c2_mma_t<2, 2>(a, lda, b, ldb, K, wy, wx, acc);
+                                       int nbi, f32x4 (&acc)[8]) {
+    if (nbi == 4) c2_mma_t<4, 2>(a, lda, b, ldb, K, wy, wx, acc);
+    else if (nbi == 2) c2_mma_t<2, 2>(a, lda, b, ldb, K, wy, wx, acc);
 }
 
-__device__ __forceinline__ void c2_zero(f32x4 (&acc)[16]) {
+__device__ __forceinline__ void c2_zero(f32x4 (&acc)[8]) {
 #pragma unroll
-    for (int b = 0; b < 16; ++b) acc[b] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    for (int b = 0; b < 8; ++b) acc[b] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 }
 
 // The wave's blocks to LDS: m[row][col] = f(row, col, value), row-major
 // (stride kC2Ld); with T, m[col][row] instead (four consecutive rows of a
 // column are one 16-byte store).
 template <bool T, typename Fn>
-__device__ __forceinline__ void c2_store(float* m, int wy, int wx, int nbi, int nbj, const f32x4 (&acc)[16], Fn f) {
+__device__ __forceinline__ void c2_store(float* m, int wy, int wx, int nbi, const f32x4 (&acc)[8], Fn f) {
     const int lane = threadIdx.x & 63;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            if (i >= nbi || j >= nbj) continue;
-            const int row = wy * 64 + 16 * i + 4 * (lane >> 4), col = wx * 64 + 16 * j + (lane & 15);
+        for (int j = 0; j < 2; ++j) {
+            if (i >= nbi) continue;
+            const int row = wy * 64 + 16 * i + 4 * (lane >> 4), col = wx * kC2PieceCols + 16 * j + (lane & 15);
             f32x4 v;
 #pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] = f(row + e, col, acc[i * 4 + j][e]);
+            for (int e = 0; e < 4; ++e) v[e] = f(row + e, col, acc[i * 2 + j][e]);
             if constexpr (T) {
                 *reinterpret_cast<f32x4*>(m + col * kC2Ld + row) = v;
             } else {
@@ -520,33 +523,43 @@ __device__ __forceinline__ void c2_store(float* m, int wy, int wx, int nbi, int 
 // A (dp x dp, global, row stride dp) into LDS rows of stride kC2Ld.
 __device__ __forceinline__ void c2_load_a(float* m, const float* __restrict__ A, int dp) {
     const int nv = dp * dp / 4;
-    for (int v = threadIdx.x; v < nv; v += kGemmThreads) {
+    for (int v = threadIdx.x; v < nv; v += kC2Threads) {
         const int e = 4 * v, r = e / dp, c = e - r * dp;
         *reinterpret_cast<f32x4*>(m + r * kC2Ld + c) = gload4(A + e);
     }
 }
 
-__global__ __launch_bounds__(kGemmThreads) void lds_chain128_kernel(const FactorDev* __restrict__ f,
-                                                                    const int* __restrict__ list, double beta2,
-                                                                    int mode, int order) {
+// Sum of one double per thread over the workgroup's eight waves, in a fixed order.
+__device__ __forceinline__ double c2_block_sum(double v, double* red) {
+    v = wave_sum(v);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+    __syncthreads();
+    return ((red[0] + red[1]) + (red[2] + red[3])) + ((red[4] + red[5]) + (red[6] + red[7]));
+}
+
+__global__ __launch_bounds__(kC2Threads) void lds_chain128_kernel(const FactorDev* __restrict__ f,
+                                                                  const int* __restrict__ list, double beta2,
+                                                                  int mode, int order) {
+    static_assert(kC2Waves == 8, "the block sum and the piece layout assume eight waves");
     __shared__ __attribute__((aligned(16))) Chain2Lds sm;
     const FactorDev F = f[list[blockIdx.x]];
     const int dp = F.dp, d = F.d, tid = threadIdx.x;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), wy = wave >> 1, wx = wave & 1;
-    // 16-row blocks of this wave's quadrant inside dp (dp is 96 or 128: 2 or 4)
-    const int nbi = min(4, (dp - wy * 64) / 16), nbj = min(4, (dp - wx * 64) / 16);
-    const bool active = nbi > 0 && nbj > 0;
-    f32x4 acc[16];
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), wy = wave >> 2, wx = wave & 3;
+    // 16-row blocks of this wave's piece inside dp (dp is 96 or 128: 2 or 4);
+    // its two 16-column blocks are inside dp or outside it together.
+    const int nbi = min(4, (dp - wy * 64) / 16);
+    const bool active = nbi > 0 && wx * kC2PieceCols < dp;
+    f32x4 acc[8];
 
     // M = H H^T, H (dp x kp, row stride kp) in 32-column slabs; thread t
-    // moves four 16-byte pieces of each slab: row (t + 256 p) / 8, columns
-    // 4 ((t + 256 p) % 8) .. + 3.
+    // moves two 16-byte pieces of each slab: row (t + 512 p) / 8, columns
+    // 4 ((t + 512 p) % 8) .. + 3.
     c2_zero(acc);
-    f32x4 hv[4];
+    f32x4 hv[2];
     auto load_h = [&](int k0) {
 #pragma unroll
-        for (int p = 0; p < 4; ++p) {
-            const int u = tid + kGemmThreads * p, r = u >> 3;
+        for (int p = 0; p < 2; ++p) {
+            const int u = tid + kC2Threads * p, r = u >> 3;
             if (r < dp) hv[p] = gload4(F.H + (size_t)r * F.kp + k0 + 4 * (u & 7));
         }
     };
@@ -554,23 +567,23 @@ __global__ __launch_bounds__(kGemmThreads) void lds_chain128_kernel(const Factor
     for (int k0 = 0; k0 < F.kp; k0 += kSlab) {
         __syncthreads();  // every wave is done with the previous slab
 #pragma unroll
-        for (int p = 0; p < 4; ++p) {
-            const int u = tid + kGemmThreads * p, r = u >> 3;
+        for (int p = 0; p < 2; ++p) {
+            const int u = tid + kC2Threads * p, r = u >> 3;
             if (r < dp) *reinterpret_cast<f32x4*>(sm.h + r * kC2HLd + 4 * (u & 7)) = hv[p];
         }
         __syncthreads();
         if (k0 + kSlab < F.kp) load_h(k0 + kSlab);
-        if (active) c2_mma(sm.h, kC2HLd, sm.h, kC2HLd, kSlab, wy, wx, nbi, nbj, acc);
+        if (active) c2_mma(sm.h, kC2HLd, sm.h, kC2HLd, kSlab, wy, wx, nbi, acc);
     }
-    if (active) c2_store<false>(sm.m0, wy, wx, nbi, nbj, acc, [](int, int, float v) { return v; });
+    if (active) c2_store<false>(sm.m0, wy, wx, nbi, acc, [](int, int, float v) { return v; });
     c2_load_a(sm.m1, F.A, dp);
     __syncthreads();
     // A^2 and A^4, each over the last in m1
     for (int pw = 0; pw < 2; ++pw) {
         c2_zero(acc);
-        if (active) c2_mma(sm.m1, kC2Ld, sm.m1, kC2Ld, dp, wy, wx, nbi, nbj, acc);
+        if (active) c2_mma(sm.m1, kC2Ld, sm.m1, kC2Ld, dp, wy, wx, nbi, acc);
         __syncthreads();
-        if (active) c2_store<false>(sm.m1, wy, wx, nbi, nbj, acc, [](int, int, float v) { return v; });
+        if (active) c2_store<false>(sm.m1, wy, wx, nbi, acc, [](int, int, float v) { return v; });
         __syncthreads();
     }
     // X = A^4 M (M symmetric: its rows are its columns) with ||X||_F^2; X to
@@ -578,16 +591,16 @@ __global__ __launch_bounds__(kGemmThreads) void lds_chain128_kernel(const Factor
     c2_zero(acc);
     double part = 0.0;
     if (active) {
-        c2_mma(sm.m1, kC2Ld, sm.m0, kC2Ld, dp, wy, wx, nbi, nbj, acc);
+        c2_mma(sm.m1, kC2Ld, sm.m0, kC2Ld, dp, wy, wx, nbi, acc);
 #pragma unroll
-        for (int b = 0; b < 16; ++b)
+        for (int b = 0; b < 8; ++b)
 #pragma unroll
             for (int e = 0; e < 4; ++e) part += (double)acc[b][e] * (double)acc[b][e];
     }
-    const double nu2 = block_sum_256(part, sm.red);  // (its barrier also ends the reads of m0 and m1)
+    const double nu2 = c2_block_sum(part, sm.red);  // (its barrier also ends the reads of m0 and m1)
     if (active) {
-        c2_store<false>(sm.m0, wy, wx, nbi, nbj, acc, [](int, int, float v) { return v; });
-        c2_store<true>(sm.m1, wy, wx, nbi, nbj, acc, [](int, int, float v) { return v; });
+        c2_store<false>(sm.m0, wy, wx, nbi, acc, [](int, int, float v) { return v; });
+        c2_store<true>(sm.m1, wy, wx, nbi, acc, [](int, int, float v) { return v; });
     }
     if (tid == 0) {
         const FactorScalars fs = factor_scalars(sqrt(nu2), beta2, mode);
@@ -602,27 +615,27 @@ __global__ __launch_bounds__(kGemmThreads) void lds_chain128_kernel(const Factor
     const float* X = sm.m0;
     // X X (B = X, whose rows-in-k are the rows of X^T in m1)
     c2_zero(acc);
-    if (active) c2_mma(sm.m0, kC2Ld, sm.m1, kC2Ld, dp, wy, wx, nbi, nbj, acc);
+    if (active) c2_mma(sm.m0, kC2Ld, sm.m1, kC2Ld, dp, wy, wx, nbi, acc);
     __syncthreads();
     if (order == 3) {
         // V = b X - e X X, stored transposed over X^T; then X V
         if (active)
-            c2_store<true>(sm.m1, wy, wx, nbi, nbj, acc,
+            c2_store<true>(sm.m1, wy, wx, nbi, acc,
                            [&](int row, int col, float v) { return b * X[row * kC2Ld + col] - ce * v; });
         __syncthreads();
         c2_zero(acc);
-        if (active) c2_mma(sm.m0, kC2Ld, sm.m1, kC2Ld, dp, wy, wx, nbi, nbj, acc);
+        if (active) c2_mma(sm.m0, kC2Ld, sm.m1, kC2Ld, dp, wy, wx, nbi, acc);
         __syncthreads();
         // P = I - a X + X V, stored transposed
         if (active)
-            c2_store<true>(sm.m1, wy, wx, nbi, nbj, acc, [&](int row, int col, float v) {
+            c2_store<true>(sm.m1, wy, wx, nbi, acc, [&](int row, int col, float v) {
                 const float id = (row == col && row < d) ? 1.0f : 0.0f;
                 return (id - a * X[row * kC2Ld + col]) + v;
             });
     } else {
         // P = I - a X + b X X, stored transposed
         if (active)
-            c2_store<true>(sm.m1, wy, wx, nbi, nbj, acc, [&](int row, int col, float v) {
+            c2_store<true>(sm.m1, wy, wx, nbi, acc, [&](int row, int col, float v) {
                 const float id = (row == col && row < d) ? 1.0f : 0.0f;
                 return (id - a * X[row * kC2Ld + col]) + b * v;
             });
@@ -632,13 +645,13 @@ __global__ __launch_bounds__(kGemmThreads) void lds_chain128_kernel(const Factor
     __syncthreads();
     // Z = s A P (B = P: its rows-in-k are the rows of P^T in m1)
     c2_zero(acc);
-    if (active) c2_mma(sm.m0, kC2Ld, sm.m1, kC2Ld, dp, wy, wx, nbi, nbj, acc);
+    if (active) c2_mma(sm.m0, kC2Ld, sm.m1, kC2Ld, dp, wy, wx, nbi, acc);
     __syncthreads();
-    if (active) c2_store<false>(sm.m0, wy, wx, nbi, nbj, acc, [&](int, int, float v) { return sf * v; });
+    if (active) c2_store<false>(sm.m0, wy, wx, nbi, acc, [&](int, int, float v) { return sf * v; });
     __syncthreads();
     // A <- (Z + Z^T)/2: fp32 addition commutes, so the result is bitwise symmetric.
     const int nv = dp * dp / 4;
-    for (int v = tid; v < nv; v += kGemmThreads) {
+    for (int v = tid; v < nv; v += kC2Threads) {
         const int e = 4 * v, r = e / dp, c = e - r * dp;
         f32x4 o;
 #pragma unroll
