@@ -99,8 +99,15 @@ def _one_step_from(orc, po, shapes, layers, pg, G, t, what):
     return w
 
 
+# A context of small layers only (every factor at most 128 wide), so both LDS
+# chain kernels take every factor update: sizes 96 and 128 in the eight-wave
+# kernel, up to 64 in the other; ragged sizes pad to 32.
+SMALL_CHAIN = ([(128, 128), (96, 128), (100, 70), (128, 40), (65, 97), (3, 128), (128, 90), (64, 64),
+                (32, 48), (40, 1), (1, 64), (50, 17), (128, 33), (77, 128), (96, 96), (20, 100)], 1e-2, 100)
+
+
 def _trajectory(name, checks, one_step_at=(), sample=None, seed=0):
-    shapes, sigma, steps = CONFIGS[name]
+    shapes, sigma, steps = SMALL_CHAIN if name == "small_chain" else CONFIGS[name]
     layers = list(range(len(shapes))) if sample is None else list(sample)
     say(f"{name}: {len(shapes)} layers, {steps} steps, oracle on {len(layers)} layers")
     opt = Jorge(shapes)
@@ -143,3 +150,11 @@ def test_trajectory_many_small_all_layers_200_steps():
 def test_trajectory_large_dense_sampled_layers_20_steps():
     # layer 3 is 4096 x 4096, layer 12 is 4096 x 1024
     _trajectory("large_dense", checks=(10, 20), one_step_at=(20,), sample=(3, 12))
+
+
+def test_trajectory_lds_chains_100_steps():
+    opt = Jorge(SMALL_CHAIN[0])
+    assert opt.stage_flops()["lds_chain"] > 0 and all(
+        opt.factor_form(l, side) == "explicit" for l in range(len(SMALL_CHAIN[0])) for side in (0, 1))
+    del opt
+    _trajectory("small_chain", checks=(25, 50, 75, 100), one_step_at=(50, 100))
