@@ -1,9 +1,9 @@
 """torch.optim front end of the Jorge library, with the paper's single-shot tuning.
 
-JorgeOptimizer hands every parameter of two or more dimensions to one Jorge
-context (the C ABI of include/jorge.h): an N-d weight is the out x
-(numel / out) matrix its storage already is (Section 3 collapses weights to
-2-D). The order of the collapsed columns does not matter: permuting them
+JorgeOptimizer hands the parameters of two or more dimensions of each
+parameter group to one Jorge context (the C ABI of include/jorge.h): an N-d
+weight is the out x (numel / out) matrix its storage already is (Section 3
+collapses weights to 2-D). The order of the collapsed columns does not matter: permuting them
 permutes R_hat the same way (Jorge commutes with orthogonal changes of basis
 of either side, and the initial eps^(-1/4) I is invariant), so channels-last
 weights are used in place. Parameters of fewer than two dimensions (biases,
@@ -69,38 +69,53 @@ def split_params(params) -> tuple[list, list]:
 
 
 class JorgeOptimizer(torch.optim.Optimizer):
-    """torch.optim-style Jorge: one grouped library step for all matrix parameters.
+    """torch.optim-style Jorge: one grouped library step per parameter group.
 
-    Hyperparameters (one group): lr (grafted step size), beta1 (momentum of
-    both m and m_SGD), beta2 (the floor of the dynamic beta by default),
-    weight_decay (decoupled, lr-scaled, on matrices), vector_weight_decay
-    (coupled L2 of the SGD update of vector parameters). Context options
-    (eps, precond_interval, beta_mode, graft, symmetrize, factor_form, ...)
-    go to the Jorge context. lr is read from the group on every step, so
-    torch learning-rate schedulers work.
+    Hyperparameters (per group, as in torch.optim): lr (grafted step size),
+    beta1 (momentum of both m and m_SGD), beta2 (the floor of the dynamic beta
+    by default), weight_decay (decoupled, lr-scaled, on matrices),
+    vector_weight_decay (coupled L2 of the SGD update of vector parameters).
+    Each group's matrix parameters form one Jorge context, stepped with that
+    group's values (one group keeps every layer in the same grouped launches,
+    which is the fastest). Context options (eps, precond_interval, beta_mode,
+    graft, symmetrize, factor_form, ...) apply to every group's context. lr
+    and the other values are read from the groups on every step, so torch
+    learning-rate schedulers work.
     """
 
     def __init__(self, params, lr: float, beta1: float = 0.9, beta2: float = 0.9, weight_decay: float = 0.0,
                  vector_weight_decay: float = 0.0, **context_options):
+        self._context_options = dict(context_options)
+        self._groups = []   # per parameter group: matrices, vectors, context, pointer array
+        self._zero = {}
         defaults = dict(lr=lr, beta1=beta1, beta2=beta2, weight_decay=weight_decay,
                         vector_weight_decay=vector_weight_decay)
         super().__init__(params, defaults)
-        if len(self.param_groups) != 1:
-            raise ValueError("JorgeOptimizer takes a single parameter group")
-        self.mats, self.vecs = split_params(self.param_groups[0]["params"])
-        for p in self.mats:
+
+    def add_param_group(self, param_group):
+        super().add_param_group(param_group)
+        mats, vecs = split_params(self.param_groups[-1]["params"])
+        for p in mats:
             if not (p.is_cuda and p.dtype == torch.float32):
                 raise ValueError("matrix parameters must be fp32 CUDA tensors")
-        self.shapes = [matrix_view(p) for p in self.mats]
-        self.ctx = Jorge(self.shapes, **context_options) if self.mats else None
-        self._param_ptrs = Jorge.pointer_array(self.mats) if self.mats else None
-        self._zero = {}
+        ctx = Jorge([matrix_view(p) for p in mats], **self._context_options) if mats else None
+        self._groups.append({"mats": mats, "vecs": vecs, "ctx": ctx,
+                             "ptrs": Jorge.pointer_array(mats) if mats else None})
 
-    def _grad_ptrs(self):
+    @property
+    def ctx(self):
+        """The Jorge context of the first parameter group that has matrix parameters (or None)."""
+        return next((g["ctx"] for g in self._groups if g["ctx"] is not None), None)
+
+    @property
+    def mats(self):
+        """Every matrix parameter, group by group."""
+        return [p for g in self._groups for p in g["mats"]]
+
+    def _grad_ptrs(self, mats):
         """Device pointers of the matrix gradients, each in its parameter's layout."""
         ptrs = []
-        self._keep = []
-        for p in self.mats:
+        for p in mats:
             g = p.grad
             if g is None:  # no gradient this step: a zero gradient of the same layout
                 g = self._zero.get(id(p))
@@ -118,43 +133,50 @@ class JorgeOptimizer(torch.optim.Optimizer):
         if closure is not None:
             with torch.enable_grad():
                 loss = closure()
-        group = self.param_groups[0]
-        lr, b1, b2, wd = group["lr"], group["beta1"], group["beta2"], group["weight_decay"]
-        if self.ctx is not None:
-            self.ctx.set_stream(torch.cuda.current_stream().cuda_stream)
-            self.ctx.step_ptrs(self._param_ptrs, self._grad_ptrs(), lr, b2, b1, wd)
-        vec = [p for p in self.vecs if p.grad is not None]
-        if vec:
-            grads = [p.grad for p in vec]
-            vwd = group["vector_weight_decay"]
-            if vwd:
-                grads = torch._foreach_add(grads, [p for p in vec], alpha=vwd)
-            bufs = []
-            for p, g in zip(vec, grads):
-                st = self.state[p]
-                if "momentum_buffer" not in st:
-                    st["momentum_buffer"] = torch.clone(g).detach()
-                else:
-                    st["momentum_buffer"].mul_(b1).add_(g)
-                bufs.append(st["momentum_buffer"])
-            torch._foreach_add_(vec, bufs, alpha=-lr)
+        self._keep = []
+        for group, g in zip(self.param_groups, self._groups):
+            lr, b1, b2, wd = group["lr"], group["beta1"], group["beta2"], group["weight_decay"]
+            if g["ctx"] is not None:
+                g["ctx"].set_stream(torch.cuda.current_stream().cuda_stream)
+                g["ctx"].step_ptrs(g["ptrs"], self._grad_ptrs(g["mats"]), lr, b2, b1, wd)
+            vec = [p for p in g["vecs"] if p.grad is not None]
+            if vec:
+                grads = [p.grad for p in vec]
+                vwd = group["vector_weight_decay"]
+                if vwd:
+                    grads = torch._foreach_add(grads, [p for p in vec], alpha=vwd)
+                bufs = []
+                for p, gr in zip(vec, grads):
+                    st = self.state[p]
+                    if "momentum_buffer" not in st:
+                        st["momentum_buffer"] = torch.clone(gr).detach()
+                    else:
+                        st["momentum_buffer"].mul_(b1).add_(gr)
+                    bufs.append(st["momentum_buffer"])
+                torch._foreach_add_(vec, bufs, alpha=-lr)
         return loss
 
     def state_dict(self):
-        """The torch state plus the Jorge context's state tensors and step counter (host copies)."""
+        """The torch state plus, per parameter group, its Jorge context's state tensors and step counter
+        (host copies)."""
         sd = super().state_dict()
-        if self.ctx is not None:
-            sd["jorge"] = {"t": self.ctx.t,
-                           "tensors": [{k: self.ctx.get_state(l, k).cpu() for k in ("L", "R", "mom", "mom_sgd")}
-                                       for l in range(len(self.mats))]}
+        sd["jorge"] = [None if g["ctx"] is None else
+                       {"t": g["ctx"].t,
+                        "tensors": [{k: g["ctx"].get_state(l, k).cpu() for k in ("L", "R", "mom", "mom_sgd")}
+                                    for l in range(len(g["mats"]))]}
+                       for g in self._groups]
         return sd
 
     def load_state_dict(self, state_dict):
         sd = dict(state_dict)
         jorge = sd.pop("jorge", None)
         super().load_state_dict(sd)
-        if jorge is not None and self.ctx is not None:
-            for l, tensors in enumerate(jorge["tensors"]):
+        if isinstance(jorge, dict):   # a single group's record
+            jorge = [jorge]
+        for g, rec in zip(self._groups, jorge or []):
+            if rec is None or g["ctx"] is None:
+                continue
+            for l, tensors in enumerate(rec["tensors"]):
                 for k, v in tensors.items():
-                    self.ctx.set_state(l, k, v)
-            self.ctx.t = jorge["t"]
+                    g["ctx"].set_state(l, k, v)
+            g["ctx"].t = rec["t"]

@@ -1,7 +1,8 @@
 """GPU checks of the torch.optim front end: it matches the fp64 oracle on a small
 convolutional model, it is exactly the library's grouped step on the matrix
 parameters, column order does not matter (channels-last weights are used in
-place), vectors follow heavy-ball SGD, and its state round-trips."""
+place), vectors follow heavy-ball SGD, its state round-trips, and parameter
+groups step like separate optimizers with their own hyperparameters."""
 import io
 
 import pytest
@@ -141,6 +142,59 @@ def test_learning_rate_scheduler_drives_the_step():
         oa.step()
         sched.step()
         ob.param_groups[0]["lr"] = 0.1 if t <= 2 else 0.01   # MultiStepLR drops after two scheduler steps
+        ob.step()
+    for pa, pb in zip(a.parameters(), b.parameters()):
+        assert torch.equal(pa.detach(), pb.detach())
+
+
+def two_group_params(m):
+    """Convolution weights in one group, the linear layer and the vectors in another."""
+    convs = [p for n, p in m.named_parameters() if p.dim() == 4]
+    rest = [p for n, p in m.named_parameters() if p.dim() != 4]
+    return convs, rest
+
+
+def test_parameter_groups_step_like_separate_optimizers_bitwise():
+    """Each group's matrices form their own context and take their group's lr, beta and decay."""
+    a, b = model(), model()
+    ca, ra = two_group_params(a)
+    cb, rb = two_group_params(b)
+    oa = JorgeOptimizer([{"params": ca}, {"params": ra, "lr": 0.03, "weight_decay": 0.0, "beta2": 0.95}], **HP)
+    ob1 = JorgeOptimizer(cb, **HP)
+    ob2 = JorgeOptimizer(rb, **dict(HP, lr=0.03, weight_decay=0.0, beta2=0.95))
+    assert len(oa.param_groups) == 2 and oa.param_groups[1]["lr"] == 0.03
+    for t in range(1, 5):
+        grads_for(a, t)
+        for pa, pb in zip(a.parameters(), b.parameters()):
+            pb.grad = pa.grad.clone()
+        oa.step()
+        ob1.step()
+        ob2.step()
+    for pa, pb in zip(a.parameters(), b.parameters()):
+        assert torch.equal(pa.detach(), pb.detach())
+
+
+def test_parameter_groups_state_dict_round_trip():
+    a = model()
+    ca, ra = two_group_params(a)
+    oa = JorgeOptimizer([{"params": ca}, {"params": ra, "lr": 0.03}], **HP)
+    for t in range(1, 3):
+        grads_for(a, t)
+        oa.step()
+    buf = io.BytesIO()
+    torch.save(oa.state_dict(), buf)
+    buf.seek(0)
+    sd = torch.load(buf, weights_only=True)
+    b = model()
+    b.load_state_dict(a.state_dict())
+    cb, rb = two_group_params(b)
+    ob = JorgeOptimizer([{"params": cb}, {"params": rb, "lr": 0.03}], **HP)
+    ob.load_state_dict(sd)
+    for t in range(3, 5):
+        grads_for(a, t)
+        for pa, pb in zip(a.parameters(), b.parameters()):
+            pb.grad = pa.grad.clone()
+        oa.step()
         ob.step()
     for pa, pb in zip(a.parameters(), b.parameters()):
         assert torch.equal(pa.detach(), pb.detach())

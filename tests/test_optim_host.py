@@ -44,3 +44,16 @@ def test_split_params_by_dimension():
     mats, vecs = split_params(ps)
     assert [tuple(p.shape) for p in mats] == [(4, 3, 3, 3), (10, 4)]
     assert [tuple(p.shape) for p in vecs] == [(4,), (10,), ()]
+
+
+def test_parameter_groups_validate_their_matrices_without_a_gpu():
+    import torch
+    from paper_2310_12298_amd.optim import JorgeOptimizer
+    vec = torch.nn.Parameter(torch.zeros(8))
+    opt = JorgeOptimizer([{"params": [vec]}, {"params": [torch.nn.Parameter(torch.zeros(3))], "lr": 0.5}], lr=0.1)
+    assert opt.ctx is None and opt.mats == [] and [g["lr"] for g in opt.param_groups] == [0.1, 0.5]
+    vec.grad = torch.ones(8)
+    opt.step()                                  # vectors only: heavy-ball SGD on the host tensors
+    assert torch.allclose(vec.detach(), torch.full((8,), -0.1))
+    with pytest.raises(ValueError, match="fp32 CUDA"):
+        JorgeOptimizer([{"params": [vec]}, {"params": [torch.nn.Parameter(torch.zeros(4, 4))]}], lr=0.1)
