@@ -77,7 +77,7 @@ def _check(opt, orc, layers, pg, po, prev, gates, what):
     return worst(ms)
 
 
-def _one_step_from(orc, po, shapes, layers, pg, G, t, what):
+def _one_step_from(orc, po, shapes, layers, pg, G, t, what, interval=1):
     """Step t of a fresh context and of a copy of the oracle, both from the oracle's state after
     t - 1 steps rounded to fp32; the one-step gates."""
     o2 = copy.deepcopy(orc)
@@ -85,7 +85,7 @@ def _one_step_from(orc, po, shapes, layers, pg, G, t, what):
         for k in ("L", "R", "m", "m_sgd"):
             setattr(st, k, getattr(st, k).astype(np.float32).astype(np.float64))
     p_in = [p.astype(np.float32).astype(np.float64) for p in po]
-    opt2 = Jorge(shapes)
+    opt2 = Jorge(shapes, precond_interval=interval)
     p2 = [p.clone() for p in pg]          # layers outside the sample keep the run's parameters
     for i, l in enumerate(layers):
         for k, v in _ostate(o2.layers[i]).items():
@@ -106,12 +106,12 @@ SMALL_CHAIN = ([(128, 128), (96, 128), (100, 70), (128, 40), (65, 97), (3, 128),
                 (32, 48), (40, 1), (1, 64), (50, 17), (128, 33), (77, 128), (96, 96), (20, 100)], 1e-2, 100)
 
 
-def _trajectory(name, checks, one_step_at=(), sample=None, seed=0):
+def _trajectory(name, checks, one_step_at=(), sample=None, seed=0, interval=1):
     shapes, sigma, steps = SMALL_CHAIN if name == "small_chain" else CONFIGS[name]
     layers = list(range(len(shapes))) if sample is None else list(sample)
-    say(f"{name}: {len(shapes)} layers, {steps} steps, oracle on {len(layers)} layers")
-    opt = Jorge(shapes)
-    orc = JorgeOracle([shapes[l] for l in layers])
+    say(f"{name}: {len(shapes)} layers, {steps} steps, interval {interval}, oracle on {len(layers)} layers")
+    opt = Jorge(shapes, precond_interval=interval)
+    orc = JorgeOracle([shapes[l] for l in layers], precond_interval=interval)
     pg = [device_initial_params(seed, l, s) for l, s in enumerate(shapes)]
     po = [pg[l].double().cpu().numpy() for l in layers]
     report = {}
@@ -119,7 +119,7 @@ def _trajectory(name, checks, one_step_at=(), sample=None, seed=0):
     for t in range(1, steps + 1):
         G = [device_gradient(seed, l, t, s, sigma) for l, s in enumerate(shapes)]
         if t in one_step_at:
-            report[f"one step {t}"] = _one_step_from(orc, po, shapes, layers, pg, G, t, name)
+            report[f"one step {t}"] = _one_step_from(orc, po, shapes, layers, pg, G, t, name, interval)
             say(f"  one step {t}: {report[f'one step {t}']}")
         opt.step(pg, G, **HP)
         prev = po
@@ -158,3 +158,9 @@ def test_trajectory_lds_chains_100_steps():
         opt.factor_form(l, side) == "explicit" for l in range(len(SMALL_CHAIN[0])) for side in (0, 1))
     del opt
     _trajectory("small_chain", checks=(25, 50, 75, 100), one_step_at=(50, 100))
+
+
+def test_trajectory_single_512x4608_interval_50_100_steps():
+    # The paper's operating point (Table 1 updates the factors every 50 steps): steps 1 and 51
+    # update L_hat and R_hat, the other 98 precondition with the factors they hold.
+    _trajectory("single_512x4608", checks=(25, 50, 51, 75, 100), one_step_at=(51, 100), interval=50)
