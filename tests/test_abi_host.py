@@ -273,3 +273,38 @@ def test_plan_small_contexts_take_the_lds_chains(lib):
     assert units(small, symmetrize=False) > 0                 # the 96- and 128-wide chain needs symmetry
     assert units([(64, 64), (40, 33)], symmetrize=False) == 0
     assert units(small + [(64, 576)]) > 0
+
+
+# Property-based: any valid combination of shapes and options plans, and its
+# launch tables pass the library's own bounds and coverage check (jorge_plan
+# builds and checks them on the host); an invalid one is refused, never planned.
+from hypothesis import HealthCheck, given, settings  # noqa: E402
+from hypothesis import strategies as hs  # noqa: E402
+
+_dims = hs.one_of(hs.integers(1, 300), hs.sampled_from([31, 32, 33, 64, 96, 127, 128, 129, 256, 576, 1152, 2304]))
+_opts = hs.fixed_dictionaries({
+    "factor_form": hs.sampled_from(FORMS),
+    "symmetrize": hs.booleans(),
+    "split_k": hs.booleans(),
+    "lds_chain_max": hs.sampled_from([0, 32, 64, 96, 128]),
+    "precond_interval": hs.integers(1, 60),
+    "beta_mode": hs.sampled_from(["fixed", "dynamic", "clamped"]),
+    "graft": hs.booleans(),
+    "precond_lowrank": hs.booleans(),
+    "series_order": hs.sampled_from([2, 3]),
+})
+
+
+@settings(max_examples=120, deadline=None, suppress_health_check=[HealthCheck.function_scoped_fixture])
+@given(shapes=hs.lists(hs.tuples(_dims, _dims), min_size=1, max_size=6), opts=_opts)
+def test_plan_any_valid_options(lib, shapes, opts):
+    if opts["factor_form"] == "squared" and not opts["symmetrize"]:
+        with pytest.raises(J.JorgeError):
+            J.Jorge.plan(shapes, **opts)
+        return
+    assert J.Jorge.plan(shapes, **opts) > 0
+    st = J.Jorge.plan_stages(shapes, **opts)
+    for name, (units, split, small) in st.items():
+        assert units >= 0 and 0 <= split <= units and small >= 0, (name, units, split, small)
+        if not opts["split_k"]:
+            assert split == 0, name
