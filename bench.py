@@ -188,15 +188,35 @@ def cpu_info():
     return {"os_cpu_count": os.cpu_count(), "cpu_model": model}
 
 
+def parse_layers(spec):
+    """Layer shapes from a list such as "128x128*256,96x96*8,64x576" (m x n, optional * count)."""
+    shapes = []
+    for item in spec.split(","):
+        item = item.strip()
+        dims, _, count = item.partition("*")
+        m, _, n = dims.partition("x")
+        try:
+            m, n, count = int(m), int(n), int(count) if count else 1
+        except ValueError:
+            raise SystemExit(f"--layers: cannot read {item!r} (expected MxN or MxN*COUNT)")
+        if m < 1 or n < 1 or count < 1:
+            raise SystemExit(f"--layers: {item!r} must have positive sizes and count")
+        shapes += [(m, n)] * count
+    return shapes
+
+
 def measure(config, steps, warmup, interval=1, form="auto", split_k=1, series_order=2, seed=0,
-            copy_probe_mib=0, chain_max=128):
-    """Times one workload: W warm-up steps, then K steps twice (clean, then with per-launch events)."""
+            copy_probe_mib=0, chain_max=128, layers=None, sigma=1e-2):
+    """Times one workload: W warm-up steps, then K steps twice (clean, then with per-launch events).
+
+    layers: a list of shapes to time instead of a named workload (gradients of
+    standard deviation sigma, 30 steps by default)."""
     import torch
 
     from paper_2310_12298_amd.jorge import Jorge
     from paper_2310_12298_amd.workloads import CONFIGS, DEFAULT_HPARAMS, device_gradient, device_initial_params
 
-    shapes, sigma, run_steps = CONFIGS[config]
+    shapes, sigma, run_steps = CONFIGS[config] if layers is None else (layers, sigma, 30)
     steps = steps if steps is not None else run_steps
     hp = DEFAULT_HPARAMS
     opt = Jorge(shapes, eps=hp["eps"], precond_interval=interval, factor_form=form,
@@ -272,7 +292,8 @@ def measure(config, steps, warmup, interval=1, form="auto", split_k=1, series_or
         k_ms = timing[k][0] / max(1, timing[k][1])
         gbs = nbytes / (k_ms * 1e-3) / 1e9 if k_ms else 0.0
         hbm[k] = {"achieved": gbs, "frac": gbs / PEAK_HBM_GBS, "bytes_per_launch": nbytes}
-    # the step's flops: the grouped levels' and the LDS chains' (these run on a second stream, beside the levels)
+    # the step's flops: the grouped levels' and the LDS chains' (in a context of small factors only, the
+    # chains take every factor update in place of the levels)
     step_f = (g_flops + flops[CHAIN_STAGE] * updates) / steps
     step_b = (step_bytes(shapes, True) * updates + step_bytes(shapes, False) * (steps - updates)) / steps
     t_mfma, t_hbm = step_f / (PEAK_FP32_MFMA_TFLOPS * 1e12), step_b / (PEAK_HBM_GBS * 1e9)
@@ -331,6 +352,10 @@ def main():
     ap.add_argument("--others", type=int, default=1, choices=(0, 1),
                     help="also time the other four workloads, each for its stated number of steps, and report "
                          "them in the same line (with the default interval, order and options)")
+    ap.add_argument("--layers", default=None,
+                    help="time this list of layers instead of a named workload, e.g. 128x128*256,64x576 "
+                         "(no other workloads are timed)")
+    ap.add_argument("--sigma", type=float, default=1e-2, help="gradient standard deviation for --layers")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="before timing, copy a buffer of this many MiB once (calibrates HBM byte counters; "
                          "skips the copy-rate reference and the other workloads)")
@@ -343,9 +368,13 @@ def main():
 
     import torch
 
+    layers = parse_layers(args.layers) if args.layers else None
+    if layers is not None:
+        args.config, args.others = "custom", 0
+        WORKLOAD_NAMES["custom"] = f"layers {args.layers}, G ~ N(0, {args.sigma:g}^2)"
     torch.cuda.set_device(0)
     res = measure(args.config, args.steps, args.warmup, args.interval, args.form, args.split_k, args.series_order,
-                  args.seed, args.copy_probe_mib, args.chain_max)
+                  args.seed, args.copy_probe_mib, args.chain_max, layers, args.sigma)
     shapes, steps = res["shapes"], res["steps"]
     traffic = measured_traffic(args.config)
     ms_launch = res["gemm"]["ms_per_launch"]

@@ -69,3 +69,11 @@ def test_workload_sub_record_fields():
     assert rec["workload"] == bench.WORKLOAD_NAMES["many_small"] and rec["unit"] == "steps/s"
     assert set(rec["hbm_frac"]) == {"weight", "stage_in"}
     json.dumps(rec)
+
+
+def test_layers_option_parses_shape_lists():
+    assert bench.parse_layers("128x128*3,64x576") == [(128, 128)] * 3 + [(64, 576)]
+    assert bench.parse_layers(" 1x1 ") == [(1, 1)]
+    for bad in ("128", "0x4", "4x4*0", "axb", "4x4*z"):
+        with pytest.raises(SystemExit):
+            bench.parse_layers(bad)
