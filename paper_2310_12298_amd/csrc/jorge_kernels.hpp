@@ -163,24 +163,33 @@ __global__ void factor_finalize_kernel(const FactorDev* __restrict__ f, const in
 }
 
 // A_hat <- (Z + Z^T)/2 (or Z when not symmetrizing) for the pair of 64 x 64
-// tiles (ti, tj), (tj, ti) of a factor in the explicit form. fp32 addition commutes, so the
-// result is bitwise symmetric. za, zb: 64 x 65 floats of LDS each. All threads
-// of the workgroup call it; it ends with a barrier so the LDS can be reused.
+// tiles (ti, tj), (tj, ti) of a factor in the explicit form; a diagonal tile
+// (ti = tj) is its own partner and is read once. fp32 addition commutes, so
+// the result is bitwise symmetric. za, zb: 64 x 65 floats of LDS each. All
+// threads of the workgroup call it; it ends with a barrier so the LDS can be
+// reused. Global memory is addressed as such (not through generic pointers).
 __device__ __forceinline__ void symmetrize_pair(const FactorDev& F, int ti, int tj, int symmetrize,
                                                 float (*za)[65], float (*zb)[65]) {
     const int dp = F.dp, i0 = ti * 64, j0 = tj * 64;
     const int tid = threadIdx.x;
-    // 64 rows x 16 float4 per tile, 4 per thread.
+    const bool diag = ti == tj;
+    float (*const pb)[65] = diag ? za : zb;  // the partner tile's LDS copy
+    // 64 rows x 16 float4 per tile, 4 per thread; every load before the first LDS store.
+    f32x4 va[4], vb[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int u = tid + q * kEwThreads, r = u >> 4, c = (u & 15) * 4;
+        if (i0 + r < dp && j0 + c < dp) va[q] = gload4(F.Z + (size_t)(i0 + r) * dp + j0 + c);
+        if (!diag && j0 + r < dp && i0 + c < dp) vb[q] = gload4(F.Z + (size_t)(j0 + r) * dp + i0 + c);
+    }
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
         const int u = tid + q * kEwThreads, r = u >> 4, c = (u & 15) * 4;
         if (i0 + r < dp && j0 + c < dp) {
-            const f32x4 v = *reinterpret_cast<const f32x4*>(F.Z + (size_t)(i0 + r) * dp + j0 + c);
-            za[r][c] = v[0]; za[r][c + 1] = v[1]; za[r][c + 2] = v[2]; za[r][c + 3] = v[3];
+            za[r][c] = va[q][0]; za[r][c + 1] = va[q][1]; za[r][c + 2] = va[q][2]; za[r][c + 3] = va[q][3];
         }
-        if (j0 + r < dp && i0 + c < dp) {
-            const f32x4 v = *reinterpret_cast<const f32x4*>(F.Z + (size_t)(j0 + r) * dp + i0 + c);
-            zb[r][c] = v[0]; zb[r][c + 1] = v[1]; zb[r][c + 2] = v[2]; zb[r][c + 3] = v[3];
+        if (!diag && j0 + r < dp && i0 + c < dp) {
+            zb[r][c] = vb[q][0]; zb[r][c + 1] = vb[q][1]; zb[r][c + 2] = vb[q][2]; zb[r][c + 3] = vb[q][3];
         }
     }
     __syncthreads();
@@ -191,15 +200,15 @@ __device__ __forceinline__ void symmetrize_pair(const FactorDev& F, int ti, int 
             f32x4 v;
 #pragma unroll
             for (int e = 0; e < 4; ++e)
-                v[e] = symmetrize ? 0.5f * (za[r][c + e] + zb[c + e][r]) : za[r][c + e];
-            *reinterpret_cast<f32x4*>(F.A + (size_t)(i0 + r) * dp + j0 + c) = v;
+                v[e] = symmetrize ? 0.5f * (za[r][c + e] + pb[c + e][r]) : za[r][c + e];
+            *(gfloat4*)(F.A + (size_t)(i0 + r) * dp + j0 + c) = v;
         }
-        if (ti != tj && j0 + r < dp && i0 + c < dp) {
+        if (!diag && j0 + r < dp && i0 + c < dp) {
             f32x4 v;
 #pragma unroll
             for (int e = 0; e < 4; ++e)
                 v[e] = symmetrize ? 0.5f * (zb[r][c + e] + za[c + e][r]) : zb[r][c + e];
-            *reinterpret_cast<f32x4*>(F.A + (size_t)(j0 + r) * dp + i0 + c) = v;
+            *(gfloat4*)(F.A + (size_t)(j0 + r) * dp + i0 + c) = v;
         }
     }
     __syncthreads();
